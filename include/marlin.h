@@ -1,0 +1,155 @@
+/*
+ * marlin.h - C ABI of the MI355X (gfx950) W4A16 GEMM library.
+ *
+ * The library computes the mixed-precision product of MARLIN
+ * (arXiv 2408.11743, Section 3.4 "Kernel Design"):
+ *
+ *     C[m][n] = sum_k A[m][k] * s[k / g][n] * (q[k][n] - 8)
+ *
+ * A is fp16 [M][K] (row-major), q are unsigned 4-bit codes of a K x N weight
+ * matrix quantised symmetrically with zero point 8 (Section 3.4,
+ * "Dequantization and Tensor Cores"), s are fp16 scales, one per group of g
+ * consecutive rows of K in each column or one per column (g = K), and C is
+ * fp16 [M][N] (row-major).  Products accumulate in fp32; C is rounded to
+ * fp16 (round to nearest even) once, at the end.
+ *
+ * Conventions for every entry point:
+ *  - Pointers named as device pointers must be device memory (hipMalloc or a
+ *    PyTorch CUDA tensor) of the current device; the library never
+ *    allocates, frees or synchronises, and never reads host memory.
+ *  - Work is enqueued asynchronously on `stream` (0 = the null stream).
+ *  - Every argument check runs on the host before any HIP call; a failed
+ *    check returns a status and enqueues nothing.
+ *  - The caller owns all buffers.  Outputs must not alias inputs.
+ *  - Shapes: K % 128 == 0, N % 64 == 0, K >= 128, N >= 64, M >= 0
+ *    (M == 0 enqueues nothing and returns MARLIN_OK).  K, N <= 2^20,
+ *    M <= 2^24.
+ *  - Group size `group`: -1 or K (one scale per column), or a multiple of
+ *    128 that divides K (e.g. 128).  G = K / group scale rows (1 per column
+ *    for per-channel scales).
+ *  - Alignment: all device pointers 16-byte aligned.
+ */
+#ifndef MARLIN_MI355X_H
+#define MARLIN_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MARLIN_OK = 0,
+    MARLIN_ERR_NULL_POINTER = 1,      /* a required pointer is NULL                 */
+    MARLIN_ERR_INVALID_SHAPE = 2,     /* M, N or K outside the constraints above    */
+    MARLIN_ERR_UNSUPPORTED_GROUP = 3, /* group not in {-1, K, 128*j dividing K}     */
+    MARLIN_ERR_MISALIGNED = 4,        /* a device pointer is not 16-byte aligned    */
+    MARLIN_ERR_WORKSPACE_TOO_SMALL = 5, /* workspace_bytes < marlin_workspace_bytes */
+    MARLIN_ERR_HIP = 6,               /* a HIP runtime call or launch failed        */
+    MARLIN_ERR_INVALID_SPARSITY = 7   /* reserved for the 2:4 entry points          */
+} marlin_status_t;
+
+/* Version of the packed weight / scale layouts described below.  A packed
+ * buffer is only valid for a library with the same layout version. */
+#define MARLIN_LAYOUT_VERSION 1
+
+/* Returns MARLIN_LAYOUT_VERSION of the library actually loaded. */
+int marlin_layout_version(void);
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char *marlin_status_string(marlin_status_t status);
+
+/* Bytes of the packed weights: K * N / 2 (4 bits per weight; the weights
+ * are streamed exactly once per call, Section 3.4 "Maximizing Loading
+ * Bandwidth").  Returns 0 for shapes that violate the constraints. */
+size_t marlin_packed_weight_bytes(int64_t K, int64_t N);
+
+/* Bytes of the packed scales: 2 * G * N.  Returns 0 for invalid arguments. */
+size_t marlin_packed_scale_bytes(int64_t K, int64_t N, int64_t group);
+
+/* Bytes of the workspace marlin_gemm needs for this problem on the current
+ * device (counters plus fp32 partial sums of the Stream-K style split,
+ * Section 3.4 "Striped Partitioning").  Returns 0 for invalid arguments.
+ * The value depends on the device's compute-unit count; query it on the
+ * device that will run the GEMM. */
+size_t marlin_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t group);
+
+/*
+ * marlin_pack_weights - offline repack of codes and scales into the layout
+ * the GEMM streams (Section 3.4: "Maximizing Loading Bandwidth" reshuffles
+ * weight tiles so each thread issues one 16-byte load; "Dequantization and
+ * Tensor Cores" orders each thread's codes for paired decoding; "Groups and
+ * Instruction Ordering" reorganises the scales the same way).  Done once per
+ * weight matrix; not on the timed path.
+ *
+ *   q        device, uint8 [K][N] row-major; only the low nibble of each byte
+ *            is read (the code 0..15).
+ *   s        device, fp16 bits [G][N] row-major.
+ *   w_packed device, marlin_packed_weight_bytes(K, N) bytes, written.
+ *   s_packed device, marlin_packed_scale_bytes(K, N, group) bytes, written.
+ *
+ * Packed weight layout (uint32 words; c = column tile of 64, ku = block of
+ * 128 rows of K, nb = 16-column block in the tile, l = lane 0..63, t = 0..3):
+ *
+ *   word index  (((c * (K/128) + ku) * 4 + nb) * 64 + l) * 4 + t
+ *   holds the 8 codes of column n = 64c + 16nb + (l % 16) and rows
+ *   k = 128ku + 32t + 8(l / 16) + j, j = 0..7; code j sits in nibble
+ *   p(j) = (j >> 1) + 4 * (j & 1), i.e. bits [4p, 4p + 4).
+ *
+ * so one 16-byte vector (t = 0..3) is a lane's operand for four 16x16x32
+ * MFMA steps, and a 1 KiB run (l = 0..63) is one 16 x 128 block of W^T.
+ *
+ * Packed scale layout (fp16; r = scale row 0..G-1, lg = 0..3, nb = 0..3,
+ * i = 0..3):
+ *
+ *   index  (((c * G + r) * 4 + lg) * 4 + nb) * 4 + i
+ *   holds s[r][64c + 16nb + 4lg + i].
+ *
+ * Pack and unpack are exact inverses for codes 0..15 and any fp16 bits.
+ * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED, HIP.
+ */
+marlin_status_t marlin_pack_weights(const uint8_t *q, const uint16_t *s,
+                                    int64_t K, int64_t N, int64_t group,
+                                    void *w_packed, void *s_packed,
+                                    hipStream_t stream);
+
+/*
+ * marlin_unpack_weights - inverse of marlin_pack_weights (same arguments
+ * and layouts, directions swapped).  q receives codes 0..15 (high nibble 0).
+ */
+marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed,
+                                      int64_t K, int64_t N, int64_t group,
+                                      uint8_t *q, uint16_t *s, hipStream_t stream);
+
+/*
+ * marlin_gemm - C = A * dequant(W) (Section 3.4).
+ *
+ *   A          device, fp16 [M][K] row-major, read only.
+ *   w_packed   device, packed weights (marlin_pack_weights layout).
+ *   s_packed   device, packed scales (marlin_pack_weights layout, same group).
+ *   C          device, fp16 [M][N] row-major, written (every element).
+ *   workspace  device, >= marlin_workspace_bytes(M, N, K, group) bytes.  It
+ *              must be zero-filled once before its first use; every call
+ *              leaves its counters at zero again, so it can be reused by
+ *              later calls on the same stream without clearing.  Calls that
+ *              may overlap (different streams) need separate workspaces.
+ *
+ * Accumulation is fp32; group scales multiply each 128-row fp32 partial sum
+ * (per-channel scales multiply the final sum).  Results are bitwise
+ * reproducible for a given device, shape and input.
+ * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,
+ * WORKSPACE_TOO_SMALL, HIP.
+ */
+marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
+                            const void *s_packed, uint16_t *C,
+                            void *workspace, size_t workspace_bytes,
+                            int64_t M, int64_t N, int64_t K, int64_t group,
+                            hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MARLIN_MI355X_H */
