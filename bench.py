@@ -1,0 +1,285 @@
+#!/usr/bin/env python3
+"""Benchmark of the W4A16 GEMM on one MI355X.
+
+Workload: the Llama-7B attention-projection layer, K = N = 4096, group size
+128, synthetic seeded data (``synth`` workload 1), with the batch sweep
+M = 1, 2, 4, 8, 16, 32, 64, 128.  One step = one GEMM at every M of the
+sweep (8 launches), each on the next of >= 1 GiB of packed weight copies so
+the 256 MB Infinity Cache never serves the weights.  Packing is offline and
+not timed.  Launches are replayed from HIP graphs (one graph per step, 16
+graphs rotating the weight copies) so the host does not throttle
+microsecond kernels.
+
+Output: one JSON line.  ``value`` = TFLOP/s of the whole timed region
+(sum of 2MNK over the launches / elapsed).  Also reported per M: time per
+call, TFLOP/s, effective weight-stream GB/s, fraction of the MI355X roofline
+(t_roof / t), and the speedup over a plain fp16 ``torch.matmul`` of the same
+shape timed the same way in the same run (comparison only).  ``roofline``
+covers the GEMM kernel: algorithmic bytes of the timed launches / elapsed
+(HIP events on the launch stream) against 8 TB/s.  ``cpu_baseline`` times
+the fp64 oracle on the host over the whole sweep (and checks the GPU
+outputs against it).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+K_DIM, N_DIM, GROUP = 4096, 4096, 128
+M_SWEEP = [1, 2, 4, 8, 16, 32, 64, 128]
+WID = 1
+ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies (Infinity Cache is 256 MB)
+GRAPHS = 16
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--per-m-reps", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fp16", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the GEMM would shard by columns or rows with an RCCL all-reduce; "
+              "see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2408_11743_amd as mk
+    import synth
+    from paper_2408_11743_amd import roofline as R
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    mk.lib()
+    K, N, g = K_DIM, N_DIM, GROUP
+
+    # ---- weights: pack once, replicate to >= 1 GiB ----
+    q, s = synth.weights(WID, K, N, g)
+    wp0, sp0 = mk.pack(torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev), group=g)
+    wbytes = wp0.numel() + sp0.numel() * 2
+    nrot = 8 * math.ceil(ROTATION_BYTES / wbytes / 8)
+    wps = [wp0] + [wp0.clone() for _ in range(nrot - 1)]
+    sps = [sp0] + [sp0.clone() for _ in range(nrot - 1)]
+    log("weights %dx%d g=%d: %d B packed per copy, %d copies (%.2f GB)" %
+        (K, N, g, wbytes, nrot, nrot * wbytes / 1e9))
+
+    acts = {M: torch.from_numpy(synth.activations(WID, M, K)).to(dev) for M in M_SWEEP}
+    outs = {M: torch.empty((M, N), dtype=torch.float16, device=dev) for M in M_SWEEP}
+    ws = mk.Workspace(dev)
+    wsb = max(mk.marlin_workspace_bytes(M, N, K, g) for M in M_SWEEP)
+    wsbuf = ws.ensure(wsb)
+    L = mk.lib()
+
+    def launch(M, i, stream):
+        st = L.marlin_gemm(acts[M].data_ptr(), wps[i].data_ptr(), sps[i].data_ptr(),
+                           outs[M].data_ptr(), wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g,
+                           stream.cuda_stream)
+        if st != 0:
+            raise mk.MarlinError("marlin_gemm", st)
+
+    # ---- graphs: one step (the M sweep) per graph, 16 graphs rotating copies ----
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    graphs = []
+    with torch.cuda.stream(stream):
+        for i, M in enumerate(M_SWEEP):  # eager warm-up of every variant
+            launch(M, i % nrot, stream)
+        stream.synchronize()
+        for gi in range(GRAPHS):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=stream):
+                for j, M in enumerate(M_SWEEP):
+                    launch(M, (gi * len(M_SWEEP) + j) % nrot, stream)
+            graphs.append(gr)
+    torch.cuda.synchronize()
+    log("captured %d graphs of %d launches" % (GRAPHS, len(M_SWEEP)))
+
+    step_flops = sum(R.flops(M, N, K) for M in M_SWEEP)
+    step_bytes = sum(R.w4a16_bytes(M, N, K, g) for M in M_SWEEP)
+    step_wbytes = len(M_SWEEP) * R.weight_bytes(N, K, g)
+
+    # ---- warm-up and timed region ----
+    with torch.cuda.stream(stream):
+        for k in range(args.warmup):
+            graphs[k % GRAPHS].replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for k in range(args.steps):
+            graphs[k % GRAPHS].replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+    ev_ms = e0.elapsed_time(e1)
+    wall_ms = (t1 - t0) * 1e3
+    ms_per_step = ev_ms / args.steps
+    value = step_flops / (ms_per_step * 1e-3) / 1e12
+    log("timed %d steps: %.3f ms/step (events), wall %.3f ms/step" %
+        (args.steps, ms_per_step, wall_ms / args.steps))
+    avg_launch_us = ms_per_step * 1e3 / len(M_SWEEP)
+    achieved_gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---- per-M: graph of nrot launches (one per weight copy) ----
+    per_m = []
+    for M in M_SWEEP:
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(gr, stream=stream):
+                for i in range(nrot):
+                    launch(M, i, stream)
+            gr.replay()
+            torch.cuda.synchronize()
+            times = []
+            for _ in range(args.per_m_reps):
+                a0 = torch.cuda.Event(enable_timing=True)
+                a1 = torch.cuda.Event(enable_timing=True)
+                a0.record(stream)
+                gr.replay()
+                a1.record(stream)
+                a1.synchronize()
+                times.append(a0.elapsed_time(a1) * 1e3 / nrot)
+        del gr
+        t_us = float(np.median(times))
+        troof = R.w4a16_t_roof(M, N, K, g) * 1e6
+        per_m.append({
+            "M": M, "us": round(t_us, 3), "us_min": round(min(times), 3),
+            "tflops": round(R.flops(M, N, K) / (t_us * 1e-6) / 1e12, 3),
+            "weight_GBps": round(R.weight_bytes(N, K, g) / (t_us * 1e-6) / 1e9, 1),
+            "roof_us": round(troof, 3), "roof_frac": round(troof / t_us, 4),
+            "bound": R.bound(M, N, K, g),
+        })
+        log("M=%3d: %.3f us/call  %.1f weight GB/s  roofline frac %.3f" %
+            (M, t_us, per_m[-1]["weight_GBps"], troof / t_us))
+
+    # ---- fp16 comparator: torch.matmul with rotated fp16 weights ----
+    if not args.no_fp16:
+        w16 = torch.from_numpy((s.astype(np.float32).repeat(g, axis=0) *
+                                (q.astype(np.float32) - 8)).astype(np.float16)).to(dev)
+        nrot16 = max(2, math.ceil(ROTATION_BYTES / (w16.numel() * 2)))
+        w16s = [w16] + [w16.clone() for _ in range(nrot16 - 1)]
+        for rec in per_m:
+            M = rec["M"]
+            A = acts[M]
+            eager = torch.matmul(A, w16s[0])
+            torch.cuda.synchronize()
+            gr = torch.cuda.CUDAGraph()
+            c16 = [None] * nrot16
+            with torch.cuda.stream(stream):
+                torch.matmul(A, w16s[0])
+                stream.synchronize()
+                with torch.cuda.graph(gr, stream=stream):
+                    for i in range(nrot16):
+                        c16[i] = torch.matmul(A, w16s[i])
+                gr.replay()
+                torch.cuda.synchronize()
+                same = bool(torch.equal(c16[0], eager))
+                times = []
+                for _ in range(args.per_m_reps):
+                    a0 = torch.cuda.Event(enable_timing=True)
+                    a1 = torch.cuda.Event(enable_timing=True)
+                    a0.record(stream)
+                    gr.replay()
+                    a1.record(stream)
+                    a1.synchronize()
+                    times.append(a0.elapsed_time(a1) * 1e3 / nrot16)
+            del gr, c16
+            t16 = float(np.median(times))
+            rec["fp16_us"] = round(t16, 3)
+            rec["speedup_vs_fp16"] = round(t16 / rec["us"], 3)
+            rec["fp16_graph_matches_eager"] = same
+            log("M=%3d: fp16 matmul %.3f us/call -> speedup %.2fx" % (M, t16, t16 / rec["us"]))
+        del w16s, w16
+
+    # ---- CPU baseline: the fp64 oracle over the same sweep (also a parity check) ----
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+        tot = 0.0
+        worst = 0.0
+        ok = True
+        for M in M_SWEEP:
+            A_np = acts[M].cpu().numpy()
+            c0 = time.perf_counter()
+            ref = oracle.gemm(A_np, q, s, g)
+            tot += time.perf_counter() - c0
+            launch(M, 0, torch.cuda.current_stream())
+            torch.cuda.synchronize()
+            got = outs[M].cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref)
+            ok &= bool((err <= 2e-3 + 1e-2 * np.abs(ref)).all())
+            worst = max(worst, float(err.max()))
+        cpu = {"value": round(step_flops / tot / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+               "kind": "oracle", "seconds": round(tot, 3),
+               "sample": "the whole step: fp64 oracle at every M of the sweep, 4096x4096 g=128"}
+        parity = {"ok": ok, "max_abs_err": worst}
+        log("oracle: %.2f s for one step on %d threads; GPU parity %s (max err %.3g)" %
+            (tot, threads, ok, worst))
+
+    small = [r for r in per_m if r["M"] <= 16]
+    out = {
+        "metric": "W4A16 GEMM TFLOP/s & weight GB/s vs roofline, M=1..128; speedup vs fp16 GEMM",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "Llama-7B attention projection W4A16 GEMM, K=4096 N=4096 g=128, "
+                               "M sweep 1..128, weights rotated over %.2f GB" % (nrot * wbytes / 1e9),
+                   "K": K, "N": N, "group": g, "M": M_SWEEP, "weight_copies": nrot,
+                   "launches_per_step": len(M_SWEEP)},
+        "weight_GBps": round(step_wbytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved_gbs, 1),
+                     "peak": R.HBM_BYTES_PER_S / 1e9, "unit": "GB/s",
+                     "frac": round(achieved_gbs * 1e9 / R.HBM_BYTES_PER_S, 4), "traffic": None,
+                     "avg_launch_us": round(avg_launch_us, 3),
+                     "kernel": "w4a16_gemm_kernel (all M variants of the step)"},
+        "roof_frac_step": round(sum(R.w4a16_t_roof(M, N, K, g) for M in M_SWEEP) /
+                                (ms_per_step * 1e-3), 4),
+        "min_roof_frac_M_le_16": min(r["roof_frac"] for r in small),
+        "per_m": per_m,
+        "wall_ms_per_step": round(wall_ms / args.steps, 6),
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -69,11 +69,10 @@ size_t marlin_packed_weight_bytes(int64_t K, int64_t N);
 /* Bytes of the packed scales: 2 * G * N.  Returns 0 for invalid arguments. */
 size_t marlin_packed_scale_bytes(int64_t K, int64_t N, int64_t group);
 
-/* Bytes of the workspace marlin_gemm needs for this problem on the current
- * device (counters plus fp32 partial sums of the Stream-K style split,
- * Section 3.4 "Striped Partitioning").  Returns 0 for invalid arguments.
- * The value depends on the device's compute-unit count; query it on the
- * device that will run the GEMM. */
+/* Bytes of the workspace marlin_gemm needs for this problem (arrival
+ * counters plus fp32 partial tiles of the Stream-K style split, Section 3.4
+ * "Striped Partitioning").  Pure host arithmetic: it makes no HIP call and
+ * does not depend on the device.  Returns 0 for invalid arguments. */
 size_t marlin_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t group);
 
 /*
@@ -136,9 +135,12 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  *              later calls on the same stream without clearing.  Calls that
  *              may overlap (different streams) need separate workspaces.
  *
- * Accumulation is fp32; group scales multiply each 128-row fp32 partial sum
- * (per-channel scales multiply the final sum).  Results are bitwise
- * reproducible for a given device, shape and input.
+ * Accumulation is fp32.  Group scales: for up to 32 rows of A per pass,
+ * each 128-row fp32 partial product is multiplied by its scale; for more
+ * rows the scale multiplies the fp16 weights before the product (one fp16
+ * rounding per weight).  Per-channel scales multiply the final fp32 sum.
+ * M > 128 runs as passes of 128 rows.  Results are bitwise reproducible for
+ * a given device, shape and input.
  * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,
  * WORKSPACE_TOO_SMALL, HIP.
  */

@@ -1,0 +1,229 @@
+// Host side of the C ABI declared in include/marlin.h: argument checks (all
+// before any HIP call), launch configuration, workspace sizing and launches.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <mutex>
+
+#include "marlin.h"
+#include "internal.h"
+
+namespace marlin {
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+std::mutex g_cu_mutex;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// 0 = invalid; otherwise the number of scale rows G.
+int64_t scale_rows(int64_t K, int64_t group)
+{
+    if (group == -1 || group == K) return 1;
+    if (group <= 0 || group % 128 != 0 || K % group != 0) return 0;
+    return K / group;
+}
+
+bool shape_ok(int64_t K, int64_t N)
+{
+    return K >= 128 && N >= 64 && K % 128 == 0 && N % 64 == 0 && K <= (1 << 20) && N <= (1 << 20);
+}
+
+marlin_status_t check_weights(int64_t K, int64_t N, int64_t group)
+{
+    if (!shape_ok(K, N)) return MARLIN_ERR_INVALID_SHAPE;
+    if (scale_rows(K, group) == 0) return MARLIN_ERR_UNSUPPORTED_GROUP;
+    return MARLIN_OK;
+}
+}  // namespace
+
+int device_cu_count(int device)
+{
+    if (device < 0 || device >= kMaxDevices) return 0;
+    int v = g_cu_count[device].load(std::memory_order_acquire);
+    if (v > 0) return v;
+    std::lock_guard<std::mutex> lock(g_cu_mutex);
+    v = g_cu_count[device].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+        cus <= 0)
+        return 0;
+    g_cu_count[device].store(cus, std::memory_order_release);
+    return cus;
+}
+
+// Kernel choice by rows of A per pass:
+//   M <= 16: register-streaming kernel, mb = 1, 4 waves splitting K, 1 per CU;
+//   M <= 32: register-streaming kernel, mb = 2, 4 waves splitting K, 1 per CU;
+//   M <= 64 / 128: LDS-pipeline kernel, mb = 4 / 8, 4 waves splitting N, 1 per
+//   CU (narrower nw when N is not a multiple of 256 or 128).
+// cus bounds the compute units used (the device's when launching, kMaxCus when
+// sizing the workspace, so that the size does not depend on the device).
+GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
+{
+    (void)group_units;
+    GemmConfig cfg;
+    const int tiles64 = N / 64;
+    int per_cu;
+    if (M <= 32) {
+        cfg.kind = kKindStream;
+        cfg.mb = (M <= 16) ? 1 : 2;
+        cfg.nw = 1;
+        cfg.kw = 4;
+        per_cu = 1;
+    } else {
+        cfg.kind = kKindLds;
+        cfg.mb = (M <= 64) ? 4 : 8;
+        cfg.kw = 1;
+        cfg.nw = (tiles64 % 4 == 0) ? 4 : (tiles64 % 2 == 0) ? 2 : 1;
+        per_cu = 1;
+    }
+    const int64_t units = (int64_t)(N / (64 * cfg.nw)) * (K / 128);
+    int64_t grid = (int64_t)(cus < kMaxCus ? cus : kMaxCus) * per_cu;
+    if (grid > units) grid = units;  // every work-group must own at least one unit
+    if (grid < 1) grid = 1;
+    cfg.grid = (int)grid;
+    return cfg;
+}
+
+int slot_floats(const GemmConfig &cfg);
+
+size_t workspace_bytes_for(const GemmConfig &cfg, int N)
+{
+    const size_t cols = (size_t)N / (64 * cfg.nw);
+    const size_t counter_bytes = ((cols * 4 + 255) / 256) * 256;
+    return counter_bytes + (size_t)cfg.grid * 2 * (size_t)slot_floats(cfg) * sizeof(float);
+}
+
+namespace {
+// Largest workspace over the passes of 128 rows that an M-row call makes.
+size_t required_workspace(int64_t M, int N, int K, int gu)
+{
+    const int m_first = M < 128 ? (int)M : 128;
+    size_t need = workspace_bytes_for(choose_config(m_first, N, K, gu, kMaxCus), N);
+    const int m_last = (int)(M % 128);
+    if (M > 128 && m_last != 0) {
+        const size_t b = workspace_bytes_for(choose_config(m_last, N, K, gu, kMaxCus), N);
+        if (b > need) need = b;
+    }
+    return need;
+}
+}  // namespace
+
+}  // namespace marlin
+
+using namespace marlin;
+
+extern "C" {
+
+int marlin_layout_version(void) { return MARLIN_LAYOUT_VERSION; }
+
+const char *marlin_status_string(marlin_status_t status)
+{
+    switch (status) {
+    case MARLIN_OK: return "MARLIN_OK";
+    case MARLIN_ERR_NULL_POINTER: return "MARLIN_ERR_NULL_POINTER";
+    case MARLIN_ERR_INVALID_SHAPE: return "MARLIN_ERR_INVALID_SHAPE";
+    case MARLIN_ERR_UNSUPPORTED_GROUP: return "MARLIN_ERR_UNSUPPORTED_GROUP";
+    case MARLIN_ERR_MISALIGNED: return "MARLIN_ERR_MISALIGNED";
+    case MARLIN_ERR_WORKSPACE_TOO_SMALL: return "MARLIN_ERR_WORKSPACE_TOO_SMALL";
+    case MARLIN_ERR_HIP: return "MARLIN_ERR_HIP";
+    case MARLIN_ERR_INVALID_SPARSITY: return "MARLIN_ERR_INVALID_SPARSITY";
+    }
+    return "MARLIN_ERR_UNKNOWN";
+}
+
+size_t marlin_packed_weight_bytes(int64_t K, int64_t N)
+{
+    if (!shape_ok(K, N)) return 0;
+    return (size_t)K * (size_t)N / 2;
+}
+
+size_t marlin_packed_scale_bytes(int64_t K, int64_t N, int64_t group)
+{
+    if (check_weights(K, N, group) != MARLIN_OK) return 0;
+    return (size_t)scale_rows(K, group) * (size_t)N * 2;
+}
+
+size_t marlin_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t group)
+{
+    if (M < 0 || M > (1 << 24) || check_weights(K, N, group) != MARLIN_OK) return 0;
+    const int64_t gu = (group == -1 || group == K) ? 0 : group / 128;
+    return required_workspace(M > 0 ? M : 1, (int)N, (int)K, (int)gu);
+}
+
+marlin_status_t marlin_pack_weights(const uint8_t *q, const uint16_t *s, int64_t K, int64_t N,
+                                    int64_t group, void *w_packed, void *s_packed,
+                                    hipStream_t stream)
+{
+    if (!q || !s || !w_packed || !s_packed) return MARLIN_ERR_NULL_POINTER;
+    marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (!aligned16(w_packed) || !aligned16(s_packed)) return MARLIN_ERR_MISALIGNED;
+    const hipError_t e = launch_pack(q, s, (int)K, (int)N, (int)scale_rows(K, group),
+                                     (uint32_t *)w_packed, (uint16_t *)s_packed, stream);
+    return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
+}
+
+marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed, int64_t K,
+                                      int64_t N, int64_t group, uint8_t *q, uint16_t *s,
+                                      hipStream_t stream)
+{
+    if (!q || !s || !w_packed || !s_packed) return MARLIN_ERR_NULL_POINTER;
+    marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (!aligned16(w_packed) || !aligned16(s_packed)) return MARLIN_ERR_MISALIGNED;
+    const hipError_t e = launch_unpack((const uint32_t *)w_packed, (const uint16_t *)s_packed,
+                                       (int)K, (int)N, (int)scale_rows(K, group), q, s, stream);
+    return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
+}
+
+marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void *s_packed,
+                            uint16_t *C, void *workspace, size_t workspace_bytes, int64_t M,
+                            int64_t N, int64_t K, int64_t group, hipStream_t stream)
+{
+    if (M < 0 || M > (1 << 24)) return MARLIN_ERR_INVALID_SHAPE;
+    marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (M == 0) return MARLIN_OK;
+    if (!A || !w_packed || !s_packed || !C || !workspace) return MARLIN_ERR_NULL_POINTER;
+    if (!aligned16(A) || !aligned16(w_packed) || !aligned16(s_packed) || !aligned16(C) ||
+        !aligned16(workspace))
+        return MARLIN_ERR_MISALIGNED;
+
+    const int64_t G = scale_rows(K, group);
+    const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
+    if (workspace_bytes < required_workspace(M, (int)N, (int)K, gu))
+        return MARLIN_ERR_WORKSPACE_TOO_SMALL;
+
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return MARLIN_ERR_HIP;
+    const int cus = device_cu_count(device);
+    if (cus <= 0) return MARLIN_ERR_HIP;
+
+    for (int64_t m0 = 0; m0 < M; m0 += 128) {
+        const int mp = (M - m0) < 128 ? (int)(M - m0) : 128;
+        const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus);
+        const size_t cols = (size_t)N / (64 * cfg.nw);
+        const size_t counter_bytes = ((cols * 4 + 255) / 256) * 256;
+        GemmProblem p;
+        p.A = A + m0 * K;
+        p.W = (const uint32_t *)w_packed;
+        p.S = (const uint16_t *)s_packed;
+        p.C = C + m0 * N;
+        p.counters = (uint32_t *)workspace;
+        p.partials = (float *)((char *)workspace + counter_bytes);
+        p.M = mp;
+        p.N = (int)N;
+        p.K = (int)K;
+        p.G = (int)G;
+        p.group_units = gu;
+        const hipError_t e = launch_gemm(cfg, p, stream);
+        if (e != hipSuccess) return MARLIN_ERR_HIP;
+    }
+    return MARLIN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,130 @@
+// Offline repack of int4 codes and fp16 scales into the order the GEMM
+// streams them (Section 3.4: "Maximizing Loading Bandwidth",
+// "Dequantization and Tensor Cores", "Groups and Instruction Ordering").
+//
+// Weight words (uint32), c = 64-column tile, ku = 128-row block, nb = 16-column
+// block, l = lane 0..63, t = 0..3:
+//   word (((c*KU + ku)*4 + nb)*64 + l)*4 + t holds column n = 64c + 16nb + l%16,
+//   rows k = 128ku + 32t + 8(l/16) + j (j = 0..7), code j in nibble
+//   (j >> 1) + 4(j & 1).
+// The nibble order puts codes j and j+1 sixteen bits apart, so one mask-and-or
+// yields two fp16 values at once (see dequant8 in gemm.hip).
+//
+// Scales (fp16), r = scale row, lg = n-row group of the MFMA output, i = 0..3:
+//   index (((c*G + r)*4 + lg)*4 + nb)*4 + i holds s[r][64c + 16nb + 4lg + i],
+// so the 16 scales one output lane needs for a 64-column tile are contiguous.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace marlin {
+namespace {
+
+__device__ __forceinline__ int nibble_of(int j) { return (j >> 1) + 4 * (j & 1); }
+
+__global__ void pack_weights_kernel(const uint8_t *__restrict__ q, int K, int N,
+                                    uint32_t *__restrict__ w)
+{
+    const int64_t words = (int64_t)K * N / 8;
+    const int KU = K / 128;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < words;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int t = (int)(idx & 3);
+        const int l = (int)((idx >> 2) & 63);
+        const int nb = (int)((idx >> 8) & 3);
+        const int64_t tile = idx >> 10;  // c*KU + ku
+        const int ku = (int)(tile % KU);
+        const int c = (int)(tile / KU);
+        const int n = 64 * c + 16 * nb + (l & 15);
+        const int k0 = 128 * ku + 32 * t + 8 * (l >> 4);
+        uint32_t word = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t code = q[(int64_t)(k0 + j) * N + n] & 0xFu;
+            word |= code << (4 * nibble_of(j));
+        }
+        w[idx] = word;
+    }
+}
+
+__global__ void unpack_weights_kernel(const uint32_t *__restrict__ w, int K, int N,
+                                      uint8_t *__restrict__ q)
+{
+    const int64_t words = (int64_t)K * N / 8;
+    const int KU = K / 128;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < words;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int t = (int)(idx & 3);
+        const int l = (int)((idx >> 2) & 63);
+        const int nb = (int)((idx >> 8) & 3);
+        const int64_t tile = idx >> 10;
+        const int ku = (int)(tile % KU);
+        const int c = (int)(tile / KU);
+        const int n = 64 * c + 16 * nb + (l & 15);
+        const int k0 = 128 * ku + 32 * t + 8 * (l >> 4);
+        const uint32_t word = w[idx];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            q[(int64_t)(k0 + j) * N + n] = (uint8_t)((word >> (4 * nibble_of(j))) & 0xFu);
+    }
+}
+
+// dir = 0: natural [G][N] -> packed; dir = 1: packed -> natural.
+__global__ void permute_scales_kernel(const uint16_t *__restrict__ src, int N, int G, int dir,
+                                      uint16_t *__restrict__ dst)
+{
+    const int64_t total = (int64_t)G * N;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int i = (int)(idx & 3);
+        const int nb = (int)((idx >> 2) & 3);
+        const int lg = (int)((idx >> 4) & 3);
+        const int64_t cr = idx >> 6;  // c*G + r
+        const int r = (int)(cr % G);
+        const int c = (int)(cr / G);
+        const int64_t nat = (int64_t)r * N + 64 * c + 16 * nb + 4 * lg + i;
+        if (dir == 0)
+            dst[idx] = src[nat];
+        else
+            dst[nat] = src[idx];
+    }
+}
+
+int blocks_for(int64_t work, int threads)
+{
+    int64_t b = (work + threads - 1) / threads;
+    if (b > 65536) b = 65536;
+    return (int)(b < 1 ? 1 : b);
+}
+
+}  // namespace
+
+hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
+                       uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream)
+{
+    const int threads = 256;
+    const int64_t words = (int64_t)K * N / 8;
+    hipLaunchKernelGGL(pack_weights_kernel, dim3(blocks_for(words, threads)), dim3(threads), 0,
+                       stream, q, K, N, w_packed);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(permute_scales_kernel, dim3(blocks_for((int64_t)G * N, threads)),
+                       dim3(threads), 0, stream, s, N, G, 0, s_packed);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack(const uint32_t *w_packed, const uint16_t *s_packed, int K, int N,
+                         int G, uint8_t *q, uint16_t *s, hipStream_t stream)
+{
+    const int threads = 256;
+    const int64_t words = (int64_t)K * N / 8;
+    hipLaunchKernelGGL(unpack_weights_kernel, dim3(blocks_for(words, threads)), dim3(threads), 0,
+                       stream, w_packed, K, N, q);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(permute_scales_kernel, dim3(blocks_for((int64_t)G * N, threads)),
+                       dim3(threads), 0, stream, s_packed, N, G, 1, s);
+    return hipGetLastError();
+}
+
+}  // namespace marlin

@@ -1,0 +1,93 @@
+"""Tensor helpers over the C ABI (PyTorch supplies device memory and streams).
+
+No arithmetic of the method happens here: these functions allocate outputs,
+check dtypes and devices, and call the ``marlin_*`` entry points on the
+current HIP stream.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _binding as B
+
+
+def _group(K: int, group) -> int:
+    return -1 if group is None or group == -1 or group == K else int(group)
+
+
+def _cur_stream(t: torch.Tensor):
+    return torch.cuda.current_stream(t.device)
+
+
+def pack(q: torch.Tensor, s: torch.Tensor, group=128):
+    """Pack codes q (uint8 [K, N]) and scales s (fp16 [G, N]) on the GPU.
+
+    Returns (w_packed uint8 [K*N/2], s_packed fp16 [G*N]).
+    """
+    if not (q.is_cuda and s.is_cuda):
+        raise ValueError("pack: q and s must be device tensors")
+    if q.dtype != torch.uint8 or s.dtype != torch.float16:
+        raise TypeError("pack: q must be uint8, s float16")
+    K, N = q.shape
+    g = _group(K, group)
+    wb = B.marlin_packed_weight_bytes(K, N)
+    sb = B.marlin_packed_scale_bytes(K, N, g)
+    if wb == 0 or sb == 0:
+        raise B.MarlinError("pack", 2)
+    q = q.contiguous()
+    s = s.contiguous()
+    wp = torch.empty(wb, dtype=torch.uint8, device=q.device)
+    sp = torch.empty(sb // 2, dtype=torch.float16, device=q.device)
+    B.marlin_pack_weights(q, s, K, N, g, wp, sp, _cur_stream(q))
+    return wp, sp
+
+
+def unpack(wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128):
+    """Inverse of ``pack``: returns (q uint8 [K, N], s fp16 [G, N])."""
+    g = _group(K, group)
+    G = 1 if g == -1 else K // g
+    q = torch.empty((K, N), dtype=torch.uint8, device=wp.device)
+    s = torch.empty((G, N), dtype=torch.float16, device=wp.device)
+    B.marlin_unpack_weights(wp, sp, K, N, g, q, s, _cur_stream(wp))
+    return q, s
+
+
+class Workspace:
+    """A zero-filled device workspace, grown on demand (never shrunk).
+
+    One workspace serves any number of GEMMs issued in order on one stream;
+    each call leaves the counters at zero.
+    """
+
+    def __init__(self, device=None, nbytes: int = 0):
+        self.device = torch.device(device or "cuda")
+        self.buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+
+    def ensure(self, nbytes: int) -> torch.Tensor:
+        if self.buf.numel() < nbytes:
+            self.buf = torch.zeros(nbytes, dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+_default_ws: dict = {}
+
+
+def gemm(A: torch.Tensor, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128,
+         out: torch.Tensor | None = None, workspace: Workspace | None = None) -> torch.Tensor:
+    """C = A * dequant(W) with packed W; A fp16 [M, K] -> C fp16 [M, N]."""
+    if A.dtype != torch.float16 or not A.is_cuda:
+        raise TypeError("gemm: A must be a float16 device tensor")
+    A = A.contiguous()
+    M = A.shape[0]
+    if A.shape[1] != K:
+        raise ValueError("gemm: A has %d columns, expected K=%d" % (A.shape[1], K))
+    g = _group(K, group)
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=A.device)
+    need = B.marlin_workspace_bytes(M, N, K, g)
+    if workspace is None:
+        key = (A.device, torch.cuda.current_stream(A.device).cuda_stream)
+        workspace = _default_ws.setdefault(key, Workspace(A.device))
+    buf = workspace.ensure(need)
+    B.marlin_gemm(A, wp, sp, out, buf, buf.numel(), M, N, K, g, _cur_stream(A))
+    return out

@@ -1,0 +1,84 @@
+"""Byte and FLOP accounting of the W4A16 GEMM, and MI355X peaks.
+
+Algorithmic work per call (what the method must move or compute; workspace
+traffic is implementation overhead and not counted):
+
+* FLOPs: 2*M*N*K (Section 3.4, "Bound By Weight Loading": exactly M*K*N
+  multiply-accumulates of 2 FLOPs each);
+* bytes: the paper's 16MK + 4KN + 16MN bits (fp16 A and C, 4-bit B) plus the
+  group scales, 2 bytes per scale, ceil(K/g)*N of them (the 0.125 bit per
+  weight that Section 5.1 includes in its ideal 3.87x at g = 128);
+* weight-stream bytes: K*N/2 + 2*ceil(K/g)*N.
+
+The fp16 comparator (a plain fp16 GEMM of the same shape) moves
+2KN + 2MK + 2MN bytes.  The roofline time of either is
+max(bytes / HBM bandwidth, FLOPs / MFMA peak).
+"""
+from __future__ import annotations
+
+# MI355X published peaks (dense): HBM3E bandwidth and fp16 MFMA throughput.
+HBM_BYTES_PER_S = 8.0e12
+FP16_MFMA_FLOPS = 2.5e15
+CU_COUNT = 256
+CLOCK_HZ = 2.4e9
+
+
+def num_groups(K: int, g) -> int:
+    if g is None or g == -1 or g >= K:
+        return 1
+    return -(-K // g)
+
+
+def flops(M: int, N: int, K: int) -> float:
+    return 2.0 * M * N * K
+
+
+def paper_memory_bits(M: int, N: int, K: int) -> int:
+    """The paper's count of bits touched, without scales: 16MK + 4KN + 16MN."""
+    return 16 * M * K + 4 * K * N + 16 * M * N
+
+
+def weight_bytes(N: int, K: int, g, bits: int = 4) -> float:
+    return K * N * bits / 8.0 + 2.0 * num_groups(K, g) * N
+
+
+def w4a16_bytes(M: int, N: int, K: int, g) -> float:
+    return paper_memory_bits(M, N, K) / 8.0 + 2.0 * num_groups(K, g) * N
+
+
+def fp16_bytes(M: int, N: int, K: int) -> float:
+    return 2.0 * K * N + 2.0 * M * K + 2.0 * M * N
+
+
+def t_roof(nbytes: float, nflops: float, bw: float = HBM_BYTES_PER_S,
+           peak: float = FP16_MFMA_FLOPS) -> float:
+    return max(nbytes / bw, nflops / peak)
+
+
+def w4a16_t_roof(M, N, K, g, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS) -> float:
+    return t_roof(w4a16_bytes(M, N, K, g), flops(M, N, K), bw, peak)
+
+
+def fp16_t_roof(M, N, K, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS) -> float:
+    return t_roof(fp16_bytes(M, N, K), flops(M, N, K), bw, peak)
+
+
+def bound(M, N, K, g, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS) -> str:
+    return "hbm" if w4a16_bytes(M, N, K, g) / bw >= flops(M, N, K) / peak else "mfma"
+
+
+def ideal_weight_speedup(bits: int = 4, g: int = 128, scale_bits: int = 16) -> float:
+    """fp16 weight bits over quantised weight bits including scale storage."""
+    return 16.0 / (bits + scale_bits / g)
+
+
+def b_opt(flop_per_byte: float, bits: int = 4) -> float:
+    """Batch size at which a weight-load-bound matmul turns compute-bound:
+    2 FLOPs per weight per input row against bits/8 bytes per weight."""
+    return flop_per_byte * (bits / 8.0) / 2.0
+
+
+def ridge_m(g: int = 128, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS, bits: int = 4) -> float:
+    """M at which weight bytes / bw equals 2MNK / peak (A and C ignored)."""
+    per_weight = bits / 8.0 + 2.0 / g
+    return (peak / bw) * per_weight / 2.0

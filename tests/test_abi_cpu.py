@@ -1,0 +1,123 @@
+"""The C-ABI library loads, exports every entry point of include/marlin.h, and
+rejects bad arguments with the documented status before any HIP call.
+
+Nothing here launches work: every call either returns from host-side
+validation or touches no device memory, so these run without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2408_11743_amd as pkg
+from paper_2408_11743_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "marlin.h")
+
+OK, NULLP, SHAPE, GROUP, ALIGN, WS = 0, 1, 2, 3, 4, 5
+FAKE = 0x10000  # aligned, never dereferenced: every call below fails validation first
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(marlin_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return pkg.lib()
+
+
+def test_exports_every_header_symbol(L):
+    names = header_functions()
+    assert "marlin_gemm" in names and "marlin_pack_weights" in names
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in B.SIGNATURES, "binding lacks %s" % n
+
+
+def test_layout_version(L):
+    assert L.marlin_layout_version() == B.LAYOUT_VERSION == 1
+
+
+def test_status_strings(L):
+    for code, name in B.STATUS.items():
+        assert L.marlin_status_string(code).decode() == name
+    assert L.marlin_status_string(99).decode() == "MARLIN_ERR_UNKNOWN"
+
+
+def test_size_queries(L):
+    assert L.marlin_packed_weight_bytes(4096, 4096) == 4096 * 4096 // 2
+    assert L.marlin_packed_scale_bytes(4096, 4096, 128) == 32 * 4096 * 2
+    assert L.marlin_packed_scale_bytes(4096, 4096, -1) == 4096 * 2
+    assert L.marlin_packed_scale_bytes(4096, 4096, 4096) == 4096 * 2
+    assert L.marlin_packed_scale_bytes(4096, 4096, 256) == 16 * 4096 * 2
+    for bad in [(4000, 4096), (4096, 4000), (0, 64), (128, 0), (64, 64)]:
+        assert L.marlin_packed_weight_bytes(*bad) == 0
+    assert L.marlin_packed_scale_bytes(4096, 4096, 64) == 0
+    assert L.marlin_packed_scale_bytes(4096, 4096, 384) == 0  # does not divide K
+    ws = L.marlin_workspace_bytes(16, 4096, 4096, 128)
+    assert ws > 0
+    assert L.marlin_workspace_bytes(16, 4096, 4096, 100) == 0
+    # the larger pass of an M > 128 call decides
+    assert L.marlin_workspace_bytes(200, 4096, 4096, 128) >= L.marlin_workspace_bytes(72, 4096, 4096, 128)
+
+
+def _gemm(L, A=FAKE, W=FAKE, S=FAKE, C=FAKE, ws=FAKE, wsb=1 << 40, M=16, N=4096, K=4096, g=128):
+    return L.marlin_gemm(A, W, S, C, ws, wsb, M, N, K, g, None)
+
+
+def test_gemm_rejects_bad_arguments(L):
+    assert _gemm(L, A=None) == NULLP
+    assert _gemm(L, W=None) == NULLP
+    assert _gemm(L, S=None) == NULLP
+    assert _gemm(L, C=None) == NULLP
+    assert _gemm(L, ws=None) == NULLP
+    assert _gemm(L, K=4000) == SHAPE
+    assert _gemm(L, N=4000) == SHAPE
+    assert _gemm(L, K=0) == SHAPE
+    assert _gemm(L, M=-1) == SHAPE
+    assert _gemm(L, M=(1 << 24) + 1) == SHAPE
+    assert _gemm(L, g=64) == GROUP
+    assert _gemm(L, g=0) == GROUP
+    assert _gemm(L, g=-2) == GROUP
+    assert _gemm(L, g=384) == GROUP
+    assert _gemm(L, A=FAKE + 2) == ALIGN
+    assert _gemm(L, W=FAKE + 8) == ALIGN
+    assert _gemm(L, S=FAKE + 4) == ALIGN
+    assert _gemm(L, C=FAKE + 1) == ALIGN
+    assert _gemm(L, ws=FAKE + 1) == ALIGN
+    need = L.marlin_workspace_bytes(16, 4096, 4096, 128)
+    assert _gemm(L, wsb=need - 1) == WS
+    assert _gemm(L, wsb=0) == WS
+    # M == 0 enqueues nothing
+    assert _gemm(L, M=0, A=None, C=None) == OK
+
+
+def test_pack_rejects_bad_arguments(L):
+    def pack(q=FAKE, s=FAKE, K=256, N=128, g=128, w=FAKE, sp=FAKE):
+        return L.marlin_pack_weights(q, s, K, N, g, w, sp, None)
+
+    def unpack(w=FAKE, sp=FAKE, K=256, N=128, g=128, q=FAKE, s=FAKE):
+        return L.marlin_unpack_weights(w, sp, K, N, g, q, s, None)
+
+    for f in (pack, unpack):
+        assert f(K=200) == SHAPE
+        assert f(N=100) == SHAPE
+        assert f(g=64) == GROUP
+        assert f(w=FAKE + 4) == ALIGN
+        assert f(sp=FAKE + 2) == ALIGN
+    assert pack(q=None) == NULLP
+    assert pack(s=None) == NULLP
+    assert pack(w=None) == NULLP
+    assert unpack(q=None) == NULLP
+    assert unpack(sp=None) == NULLP
+
+
+def test_binding_raises_named_errors(L):
+    with pytest.raises(B.MarlinError) as e:
+        B.marlin_gemm(FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, 16, 4096, 4000, 128)
+    assert e.value.status == SHAPE and "INVALID_SHAPE" in str(e.value)

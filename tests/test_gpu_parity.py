@@ -1,0 +1,268 @@
+"""GPU parity: the HIP path (through the C ABI) against the FP64 oracle.
+
+Bar (spec tolerance, elementwise): |C_gpu - C_ref| <= 2e-3 + 1e-2*|C_ref|,
+with C_ref the unrounded fp64 oracle value.  Packing and unpacking are
+bit-exact; closed-form cases (identity, zero weights, power-of-two scales,
+every code in every nibble slot) are bit-exact.
+
+Inputs are the seeded workloads of ``synth``; large shapes are compared on
+sampled outputs computed one by one by the oracle, in the same launch
+configuration the bench times (the library picks it from the shape).
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import synth  # noqa: E402
+from oracle import layout  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+ATOL, RTOL = 2e-3, 1e-2
+
+
+@pytest.fixture(scope="module")
+def mk():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2408_11743_amd as mk
+    mk.lib()
+    return mk
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def check_close(C_gpu, C_ref, what=""):
+    C = C_gpu.astype(np.float64)
+    err = np.abs(C - C_ref)
+    bound = ATOL + RTOL * np.abs(C_ref)
+    bad = err > bound
+    assert np.isfinite(C).all(), what + ": non-finite output"
+    assert not bad.any(), "%s: %d/%d outside tolerance; worst err %.3g at %s (ref %.4g gpu %.4g)" % (
+        what, bad.sum(), bad.size, err.max(), np.unravel_index(err.argmax(), err.shape),
+        C_ref.flat[err.argmax()], C.flat[err.argmax()])
+
+
+def run_gemm(mk, A, q, s, g, ws=None):
+    K, N = q.shape
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws)
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+# ---------------- packing ----------------
+
+@pytest.mark.parametrize("K,N,g", [(128, 64, 128), (256, 192, 128), (1024, 1024, 128),
+                                   (512, 256, -1), (1024, 320, 256)])
+def test_pack_matches_layout_reference(mk, K, N, g):
+    q, s = synth.weights(90, K, N, None if g == -1 else g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    torch.cuda.synchronize()
+    words = wp.cpu().numpy().view(np.uint32)
+    assert np.array_equal(words, layout.pack_weights(q))
+    assert np.array_equal(sp.cpu().numpy().view(np.uint16),
+                          layout.pack_scales(s, K, g).view(np.uint16))
+
+
+@pytest.mark.parametrize("K,N,g", [(256, 128, 128), (4096, 4096, 128), (11008, 4096, -1)])
+def test_pack_unpack_roundtrip_bitexact(mk, K, N, g):
+    rng = np.random.default_rng([91, K, N])
+    q = rng.integers(0, 256, size=(K, N), dtype=np.uint8)  # high nibble must be ignored
+    G = 1 if g == -1 else K // g
+    s_bits = rng.integers(0, 1 << 16, size=(G, N), dtype=np.uint16)  # any bits, NaNs included
+    wp, sp = mk.pack(dev(q), dev(s_bits.view(np.float16)), group=g)
+    q2, s2 = mk.unpack(wp, sp, K, N, group=g)
+    torch.cuda.synchronize()
+    assert np.array_equal(q2.cpu().numpy(), q & 0xF)
+    assert np.array_equal(s2.cpu().numpy().view(np.uint16), s_bits)
+
+
+# ---------------- GEMM against the oracle ----------------
+
+def test_tiny_config(mk):
+    # 1024 x 1024, M = 16, g = 128 (the smallest named workload)
+    q, s = synth.weights(0, 1024, 1024, 128)
+    A = synth.activations(0, 16, 1024)
+    check_close(run_gemm(mk, A, q, s, 128), oracle.gemm(A, q, s, 128), "tiny")
+
+
+@pytest.mark.parametrize("M", [1, 2, 4, 8, 16, 32, 64, 128])
+def test_llama7b_attention_all_M(mk, M):
+    q, s = synth.weights(1, 4096, 4096, 128)
+    A = synth.activations(1, M, 4096)
+    check_close(run_gemm(mk, A, q, s, 128), oracle.gemm(A, q, s, 128), "4096x4096 M=%d" % M)
+
+
+@pytest.mark.parametrize("M", [3, 17, 33, 127])
+@pytest.mark.parametrize("K,N", [(1024, 768), (384, 192)])
+def test_ragged_M_and_N(mk, M, K, N):
+    # M not a multiple of 16; N = 64 * odd exercises the narrow variants
+    q, s = synth.weights(2, K, N, 128)
+    A = synth.activations(2, M, K)
+    check_close(run_gemm(mk, A, q, s, 128), oracle.gemm(A, q, s, 128), "M=%d K=%d N=%d" % (M, K, N))
+
+
+@pytest.mark.parametrize("M", [1, 16, 32, 64, 128])
+@pytest.mark.parametrize("g", [-1, 256])
+def test_other_groups(mk, M, g):
+    K, N = 2048, 1024
+    q, s = synth.weights(3, K, N, None if g == -1 else g)
+    A = synth.activations(3, M, K)
+    check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "g=%d M=%d" % (g, M))
+
+
+@pytest.mark.parametrize("M", [130, 200, 256])
+def test_M_above_128_runs_in_passes(mk, M):
+    K, N = 1024, 512
+    q, s = synth.weights(4, K, N, 128)
+    A = synth.activations(4, M, K)
+    check_close(run_gemm(mk, A, q, s, 128), oracle.gemm(A, q, s, 128), "M=%d" % M)
+
+
+def test_M_zero(mk):
+    K, N = 256, 128
+    q, s = synth.weights(5, K, N, 128)
+    wp, sp = mk.pack(dev(q), dev(s), group=128)
+    C = mk.gemm(torch.empty((0, K), dtype=torch.float16, device="cuda"), wp, sp, K, N)
+    assert C.shape == (0, N)
+
+
+# ---------------- closed forms, bit-exact ----------------
+
+@pytest.mark.parametrize("M", [1, 16, 32, 64, 128])
+def test_identity_weights_reproduce_A(mk, M):
+    K = N = 512
+    q = (np.full((K, N), 8, dtype=np.uint8) + np.eye(K, dtype=np.uint8))
+    for g in (128, -1):
+        s = np.ones((1 if g == -1 else K // g, N), dtype=np.float16)
+        A = synth.activations(6, M, K)
+        C = run_gemm(mk, A, q, s, g)
+        assert np.array_equal(C.view(np.uint16), A.view(np.uint16)), (M, g)
+
+
+@pytest.mark.parametrize("M", [1, 32, 128])
+def test_zero_weights(mk, M):
+    K, N = 1024, 256
+    q, s = synth.weights(7, K, N, 128)
+    q[:] = 8
+    C = run_gemm(mk, synth.activations(7, M, K), q, s, 128)
+    assert np.array_equal(C, np.zeros_like(C))
+
+
+@pytest.mark.parametrize("M", [1, 16, 32, 128])
+def test_every_code_in_every_nibble_slot(mk, M):
+    # A rows are unit vectors e_k, s = 1: C[m, n] = q[k_m, n] - 8 exactly.
+    # q[k, n] = (k + 3n) mod 16 puts every code at every k mod 8 (nibble slot).
+    K, N = 128, 256
+    k_idx = np.arange(M) % K
+    A = np.zeros((M, K), dtype=np.float16)
+    A[np.arange(M), k_idx] = 1.0
+    kk, nn = np.meshgrid(np.arange(K), np.arange(N), indexing="ij")
+    q = ((kk + 3 * nn) % 16).astype(np.uint8)
+    s = np.ones((1, N), dtype=np.float16)
+    C = run_gemm(mk, A, q, s, 128)
+    assert np.array_equal(C, (q[k_idx].astype(np.float32) - 8).astype(np.float16))
+
+
+@pytest.mark.parametrize("M", [1, 32, 128])
+def test_power_of_two_scales(mk, M):
+    K, N = 1024, 512
+    q, s = synth.weights(8, K, N, 128)
+    A = synth.activations(8, M, K)
+    C1 = run_gemm(mk, A, q, s, 128).astype(np.float32)
+    C2 = run_gemm(mk, A, q, (s.astype(np.float32) * 2).astype(np.float16), 128).astype(np.float32)
+    # doubling is exact in fp32 and in the fp16 result, except where the fp16
+    # result is subnormal (below 2^-14), whose spacing is a fixed 2^-24
+    normal = np.abs(C1) >= 2.0 ** -14
+    assert np.array_equal(C2[normal], 2 * C1[normal])
+    assert (np.abs(C2 - 2 * C1)[~normal] <= 2.0 ** -24).all()
+
+
+# ---------------- reduction, determinism, workspace ----------------
+
+def test_bitwise_deterministic_and_workspace_reuse(mk):
+    K, N, M = 4096, 4096, 16
+    q, s = synth.weights(1, K, N, 128)
+    A = dev(synth.activations(1, M, K))
+    wp, sp = mk.pack(dev(q), dev(s))
+    ws = mk.Workspace("cuda")
+    outs = [mk.gemm(A, wp, sp, K, N, workspace=ws).cpu().numpy() for _ in range(3)]
+    fresh = mk.gemm(A, wp, sp, K, N, workspace=mk.Workspace("cuda")).cpu().numpy()
+    for o in outs[1:] + [fresh]:
+        assert np.array_equal(o.view(np.uint16), outs[0].view(np.uint16))
+
+
+def test_workspace_shared_across_shapes(mk):
+    ws = mk.Workspace("cuda")
+    for (K, N, M, g) in [(4096, 4096, 1, 128), (1024, 768, 33, 128), (4096, 11008, 128, 128),
+                         (11008, 4096, 16, -1), (4096, 4096, 1, 128)]:
+        q, s = synth.weights(9, K, N, None if g == -1 else g)
+        A = synth.activations(9, M, K)
+        check_close(run_gemm(mk, A, q, s, g, ws=ws), oracle.gemm(A, q, s, g), "shared ws")
+
+
+def test_two_streams_two_workspaces(mk):
+    K, N = 4096, 4096
+    q, s = synth.weights(1, K, N, 128)
+    wp, sp = mk.pack(dev(q), dev(s))
+    A1, A2 = synth.activations(10, 8, K), synth.activations(11, 64, K)
+    d1, d2 = dev(A1), dev(A2)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    w1, w2 = mk.Workspace("cuda"), mk.Workspace("cuda")
+    torch.cuda.synchronize()
+    outs1, outs2 = [], []
+    for _ in range(4):
+        with torch.cuda.stream(s1):
+            outs1.append(mk.gemm(d1, wp, sp, K, N, workspace=w1))
+        with torch.cuda.stream(s2):
+            outs2.append(mk.gemm(d2, wp, sp, K, N, workspace=w2))
+    torch.cuda.synchronize()
+    r1, r2 = oracle.gemm(A1, q, s, 128), oracle.gemm(A2, q, s, 128)
+    for o in outs1:
+        check_close(o.cpu().numpy(), r1, "stream 1")
+    for o in outs2:
+        check_close(o.cpu().numpy(), r2, "stream 2")
+
+
+def test_rows_are_independent(mk):
+    K, N, M = 2048, 1024, 32
+    q, s = synth.weights(12, K, N, 128)
+    A = synth.activations(12, M, K)
+    C = run_gemm(mk, A, q, s, 128)
+    ref = oracle.gemm(A, q, s, 128)
+    for m in (0, 5, 31):
+        Cm = run_gemm(mk, A[m:m + 1], q, s, 128)
+        check_close(Cm, ref[m:m + 1], "row %d alone" % m)
+        assert np.abs(Cm[0].astype(np.float64) - C[m]).max() <= 2 * (ATOL + RTOL * np.abs(ref[m]).max())
+
+
+# ---------------- full-size named workloads, sampled ----------------
+
+def _samples(M, N, count, seed):
+    rng = np.random.default_rng(seed)
+    mi = rng.integers(0, M, size=count)
+    ni = rng.integers(0, N, size=count)
+    # corners and tile edges
+    extra_m = np.array([0, M - 1, 0, M - 1, M // 2])
+    extra_n = np.array([0, N - 1, N - 1, 0, 63])
+    return np.concatenate([mi, extra_m]), np.concatenate([ni, extra_n])
+
+
+@pytest.mark.parametrize("wid,K,N,g", [(2, 4096, 11008, 128), (2, 11008, 4096, 128),
+                                       (2, 4096, 11008, -1), (2, 11008, 4096, -1),
+                                       (3, 8192, 28672, 128), (3, 28672, 8192, 128)])
+def test_full_size_layers_sampled(mk, wid, K, N, g):
+    q, s = synth.weights(wid, K, N, None if g == -1 else g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    ws = mk.Workspace("cuda")
+    for M in (1, 16, 32, 128):
+        A = synth.activations(wid, M, K)
+        C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws).cpu().numpy()
+        mi, ni = _samples(M, N, 1500, [wid, K, N, M])
+        ref = oracle.gemm_sampled(A, q, s, g, mi, ni)
+        check_close(C[mi, ni], ref, "K=%d N=%d g=%d M=%d sampled" % (K, N, g, M))

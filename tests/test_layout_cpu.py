@@ -1,0 +1,99 @@
+"""Host-side checks of the packed layouts and of the paper's dequantisation
+recipe (no GPU).
+
+The layout reference in oracle/layout.py is checked against the header's
+description by construction tests (each packed word is rebuilt from the
+definition for single positions); the dequantisation recipe of Section 3.4
+("Dequantization and Tensor Cores") is checked on every code in every nibble
+slot with numpy's own fp16 arithmetic.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import layout
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_constants.json")))
+
+
+def test_roundtrip_random():
+    rng = np.random.default_rng(3)
+    for K, N in [(128, 64), (256, 128), (384, 192)]:
+        q = rng.integers(0, 16, size=(K, N), dtype=np.uint8)
+        w = layout.pack_weights(q)
+        assert w.dtype == np.uint32 and w.size == K * N // 8
+        assert np.array_equal(layout.unpack_weights(w, K, N), q)
+        for g in (128, -1):
+            G = 1 if g == -1 else K // g
+            s = rng.standard_normal((G, N)).astype(np.float16)
+            sp = layout.pack_scales(s, K, g)
+            assert np.array_equal(layout.unpack_scales(sp, K, N, g).view(np.uint16), s.view(np.uint16))
+
+
+def test_single_positions_follow_header():
+    # a lone code 0xF at (k, n) must land in word (((c*KU+ku)*4+nb)*64+l)*4+t,
+    # nibble (j>>1)+4(j&1), with c=n//64, nb=(n%64)//16, l%16=n%16,
+    # ku=k//128, t=(k%128)//32, l//16=(k%32)//8, j=k%8
+    K, N = 256, 128
+    for (k, n) in [(0, 0), (7, 0), (8, 1), (31, 15), (32, 16), (127, 63), (128, 64), (255, 127), (77, 90)]:
+        q = np.zeros((K, N), dtype=np.uint8)
+        q[k, n] = 0xF
+        w = layout.pack_weights(q)
+        c, nb, lo = n // 64, (n % 64) // 16, n % 16
+        ku, t, hi, j = k // 128, (k % 128) // 32, (k % 32) // 8, k % 8
+        l = hi * 16 + lo
+        idx = (((c * (K // 128) + ku) * 4 + nb) * 64 + l) * 4 + t
+        nib = (j >> 1) + 4 * (j & 1)
+        assert np.flatnonzero(w).tolist() == [idx]
+        assert w[idx] == 0xF << (4 * nib)
+
+
+def test_scale_positions_follow_header():
+    K, N, g = 256, 128, 128
+    G = 2
+    s = np.arange(G * N, dtype=np.float16).reshape(G, N)
+    sp = layout.pack_scales(s, K, g)
+    for (r, n) in [(0, 0), (1, 127), (0, 21), (1, 64)]:
+        c, rem = n // 64, n % 64
+        nb, lg, i = rem // 16, (rem % 16) // 4, rem % 4
+        assert sp[(((c * G + r) * 4 + lg) * 4 + nb) * 4 + i] == s[r, n]
+
+
+def _fp16(bits):
+    return np.array(bits, dtype=np.uint16).view(np.float16)
+
+
+def test_paper_or_bits_give_1024():
+    # the OR pattern 0110010 in the top 7 bits of an fp16 is the number 1024,
+    # whose mantissa LSB has weight 1 (Section 3.4)
+    top7 = int(GOLD["dequant_or_bits"]["value"], 2)
+    assert top7 == 50
+    base = top7 << 9
+    assert base == 0x6400 and float(_fp16(base)) == 1024.0
+    assert float(_fp16(base | 1)) - 1024.0 == 1.0
+
+
+@pytest.mark.parametrize("slot", range(8))
+def test_dequant_recipe_every_code_every_slot(slot):
+    # low nibble of each 16-bit half: (x & 0x000F000F) | 0x64006400 = 1024 + q,
+    # minus 1032 (the zero point 8 folded into the subtrahend) = q - 8;
+    # high nibble: (x & 0x00F000F0) | 0x64006400 = 1024 + 16q, then
+    # fma(., 1/16, -72) = q - 8.  Shifting by 8 reaches the other two nibbles.
+    zp = GOLD["zero_point"]["value"]
+    for code in range(16):
+        x = np.uint32(code << (4 * slot))
+        half = slot // 4          # which 16-bit half holds the code
+        sub = slot % 4            # nibble within that half
+        y = x >> np.uint32(8) if sub >= 2 else x
+        if sub % 2 == 0:
+            bits = (y & np.uint32(0x000F000F)) | np.uint32(0x64006400)
+            h = np.array([bits], dtype=np.uint32).view(np.float16)
+            val = (h - np.float16(1024 + zp))[half]
+        else:
+            bits = (y & np.uint32(0x00F000F0)) | np.uint32(0x64006400)
+            h = np.array([bits], dtype=np.uint32).view(np.float16)
+            val = (h[half].astype(np.float32) * np.float32(1 / 16) - np.float32(64 + zp))
+            val = np.float16(val)  # one rounding, as a fused multiply-add
+        assert float(val) == code - zp, (slot, code, float(val))
