@@ -40,6 +40,7 @@ M_SWEEP = [1, 2, 4, 8, 16, 32, 64, 128]
 WID = 1
 ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies (Infinity Cache is 256 MB)
 GRAPHS = 16
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a16_gemm_4096x4096_msweep_traffic.json")
 
 
 def log(msg):
@@ -54,7 +55,24 @@ def parse():
     ap.add_argument("--per-m-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fp16", action="store_true")
+    ap.add_argument("--calibration-copy-mb", type=int, default=0,
+                    help="run plain device-to-device copies of this many MB (outside the timed "
+                         "region) so hardware byte counters can be scaled against a known size")
     return ap.parse_args()
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed counter summary, or None when
+    the kernel source has changed since the counters were taken."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        src = os.path.join(ROOT, "paper_2408_11743_amd", "csrc", "gemm.hip")
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["gemm_hip_sha256"]:
+            return None
+        return rec["step_avg_hbm_bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def main():
@@ -87,6 +105,16 @@ def main():
     sps = [sp0] + [sp0.clone() for _ in range(nrot - 1)]
     log("weights %dx%d g=%d: %d B packed per copy, %d copies (%.2f GB)" %
         (K, N, g, wbytes, nrot, nrot * wbytes / 1e9))
+
+    if args.calibration_copy_mb:
+        nb = args.calibration_copy_mb << 20
+        src = torch.ones(nb // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration: 3 device copies of %d MiB" % args.calibration_copy_mb)
+        del src, dst
 
     acts = {M: torch.from_numpy(synth.activations(WID, M, K)).to(dev) for M in M_SWEEP}
     outs = {M: torch.empty((M, N), dtype=torch.float16, device=dev) for M in M_SWEEP}
@@ -230,9 +258,12 @@ def main():
         ok = True
         for M in M_SWEEP:
             A_np = acts[M].cpu().numpy()
-            c0 = time.perf_counter()
-            ref = oracle.gemm(A_np, q, s, g)
-            tot += time.perf_counter() - c0
+            runs = []
+            for _ in range(3):
+                c0 = time.perf_counter()
+                ref = oracle.gemm(A_np, q, s, g)
+                runs.append(time.perf_counter() - c0)
+            tot += float(np.median(runs))
             launch(M, 0, torch.cuda.current_stream())
             torch.cuda.synchronize()
             got = outs[M].cpu().numpy().astype(np.float64)
@@ -241,7 +272,8 @@ def main():
             worst = max(worst, float(err.max()))
         cpu = {"value": round(step_flops / tot / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
                "kind": "oracle", "seconds": round(tot, 3),
-               "sample": "the whole step: fp64 oracle at every M of the sweep, 4096x4096 g=128"}
+               "sample": "the whole step (fp64 oracle at every M of the sweep, 4096x4096 g=128), "
+                         "median of 3 runs per M"}
         parity = {"ok": ok, "max_abs_err": worst}
         log("oracle: %.2f s for one step on %d threads; GPU parity %s (max err %.3g)" %
             (tot, threads, ok, worst))
@@ -267,9 +299,12 @@ def main():
         "weight_GBps": round(step_wbytes / (ms_per_step * 1e-3) / 1e9, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved_gbs, 1),
                      "peak": R.HBM_BYTES_PER_S / 1e9, "unit": "GB/s",
-                     "frac": round(achieved_gbs * 1e9 / R.HBM_BYTES_PER_S, 4), "traffic": None,
+                     "frac": round(achieved_gbs * 1e9 / R.HBM_BYTES_PER_S, 4),
+                     "traffic": measured_traffic(),
+                     "traffic_unit": "HBM bytes per launch (step average)",
+                     "algorithmic_bytes_per_launch": round(step_bytes / len(M_SWEEP)),
                      "avg_launch_us": round(avg_launch_us, 3),
-                     "kernel": "w4a16_gemm_kernel (all M variants of the step)"},
+                     "kernel": "w4a16_stream_kernel (M <= 32) and w4a16_lds_kernel (M = 64, 128)"},
         "roof_frac_step": round(sum(R.w4a16_t_roof(M, N, K, g) for M in M_SWEEP) /
                                 (ms_per_step * 1e-3), 4),
         "min_roof_frac_M_le_16": min(r["roof_frac"] for r in small),

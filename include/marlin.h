@@ -23,7 +23,7 @@
  *  - The caller owns all buffers.  Outputs must not alias inputs.
  *  - Shapes: K % 128 == 0, N % 64 == 0, K >= 128, N >= 64, M >= 0
  *    (M == 0 enqueues nothing and returns MARLIN_OK).  K, N <= 2^20,
- *    M <= 2^24.
+ *    K * N < 2^32 (packed weights below 2 GiB), M <= 2^24.
  *  - Group size `group`: -1 or K (one scale per column), or a multiple of
  *    128 that divides K (e.g. 128).  G = K / group scale rows (1 per column
  *    for per-channel scales).
@@ -129,10 +129,12 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  *   w_packed   device, packed weights (marlin_pack_weights layout).
  *   s_packed   device, packed scales (marlin_pack_weights layout, same group).
  *   C          device, fp16 [M][N] row-major, written (every element).
- *   workspace  device, >= marlin_workspace_bytes(M, N, K, group) bytes.  It
- *              must be zero-filled once before its first use; every call
- *              leaves its counters at zero again, so it can be reused by
- *              later calls on the same stream without clearing.  Calls that
+ *   workspace  device, >= marlin_workspace_bytes(M, N, K, group) bytes.  Its
+ *              first 256 KiB (arrival counters) must be zero before its
+ *              first use (zero-fill the whole buffer once); every call
+ *              leaves the counters at zero again, so one workspace serves
+ *              any sequence of calls, of any shapes, issued in order on one
+ *              stream, as long as it is large enough for each.  Calls that
  *              may overlap (different streams) need separate workspaces.
  *
  * Accumulation is fp32.  Group scales: for up to 32 rows of A per pass,

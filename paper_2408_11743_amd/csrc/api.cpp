@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cstdlib>
+#include <cstring>
 #include <mutex>
 
 #include "marlin.h"
@@ -27,7 +29,8 @@ int64_t scale_rows(int64_t K, int64_t group)
 
 bool shape_ok(int64_t K, int64_t N)
 {
-    return K >= 128 && N >= 64 && K % 128 == 0 && N % 64 == 0 && K <= (1 << 20) && N <= (1 << 20);
+    return K >= 128 && N >= 64 && K % 128 == 0 && N % 64 == 0 && K <= (1 << 20) && N <= (1 << 20) &&
+           (uint64_t)K * (uint64_t)N < ((uint64_t)1 << 32);
 }
 
 marlin_status_t check_weights(int64_t K, int64_t N, int64_t group)
@@ -54,34 +57,77 @@ int device_cu_count(int device)
     return cus;
 }
 
+// Tuning override, read once: MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>" forces
+// the column-tile width and the work-group count of the register-streaming
+// kernel (sweeps only; the heuristic below is the default).
+struct ForcedConfig {
+    int nb = 0;
+    int grid = 0;
+};
+
+static ForcedConfig read_forced()
+{
+    ForcedConfig f;
+    const char *e = getenv("MARLIN_FORCE_CONFIG");
+    if (!e) return f;
+    const char *q = strstr(e, "nb=");
+    if (q) f.nb = atoi(q + 3);
+    q = strstr(e, "grid=");
+    if (q) f.grid = atoi(q + 5);
+    if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
+    if (f.grid < 0) f.grid = 0;
+    return f;
+}
+
+static const ForcedConfig &forced()
+{
+    static const ForcedConfig f = read_forced();
+    return f;
+}
+
 // Kernel choice by rows of A per pass:
-//   M <= 16: register-streaming kernel, mb = 1, 4 waves splitting K, 1 per CU;
-//   M <= 32: register-streaming kernel, mb = 2, 4 waves splitting K, 1 per CU;
+//   M <= 32: register-streaming kernel, mb = 1 (M <= 16) or 2, kStreamWaves
+//            waves splitting K, kStreamOcc work-groups per CU, column tiles of
+//            16 * nb columns;
 //   M <= 64 / 128: LDS-pipeline kernel, mb = 4 / 8, 4 waves splitting N, 1 per
-//   CU (narrower nw when N is not a multiple of 256 or 128).
+//            CU (narrower nw when N is not a multiple of 256 or 128).
+// The tile width nb is 4 (64 columns: the activation fragments of a 128-row
+// block serve four weight blocks) except on small layers (K * N <= 2^24),
+// where 32-column tiles halve the K range each work-group covers; nb = 1 or 2
+// also when N is not a multiple of 64 * nb (measured on MI355X, see the
+// design notes).
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
 GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
 {
     (void)group_units;
     GemmConfig cfg;
-    const int tiles64 = N / 64;
+    const int KU = K / 128;
+    const int tiles16 = N / 16;
+    const int ncu = cus < kMaxCus ? cus : kMaxCus;
     int per_cu;
     if (M <= 32) {
         cfg.kind = kKindStream;
         cfg.mb = (M <= 16) ? 1 : 2;
         cfg.nw = 1;
-        cfg.kw = 4;
-        per_cu = 1;
+        cfg.kw = kStreamWaves;
+        per_cu = kStreamOcc;
+        const bool small = (int64_t)K * N <= ((int64_t)1 << 24);
+        cfg.nb = (!small && tiles16 % 4 == 0) ? 4 : (tiles16 % 2 == 0 ? 2 : 1);
+        if (forced().nb && tiles16 % forced().nb == 0) cfg.nb = forced().nb;
     } else {
         cfg.kind = kKindLds;
         cfg.mb = (M <= 64) ? 4 : 8;
+        cfg.nb = 4;
         cfg.kw = 1;
-        cfg.nw = (tiles64 % 4 == 0) ? 4 : (tiles64 % 2 == 0) ? 2 : 1;
+        cfg.nw = (tiles16 % 16 == 0) ? 4 : (tiles16 % 8 == 0) ? 2 : 1;
         per_cu = 1;
     }
-    const int64_t units = (int64_t)(N / (64 * cfg.nw)) * (K / 128);
-    int64_t grid = (int64_t)(cus < kMaxCus ? cus : kMaxCus) * per_cu;
+    const int64_t cols = (cfg.kind == kKindStream) ? tiles16 / cfg.nb : tiles16 / (4 * cfg.nw);
+    const int64_t units = cols * KU;
+    int64_t grid = (int64_t)ncu * per_cu;
+    if (cfg.kind == kKindStream && forced().grid) grid = forced().grid;
+    if (grid > (int64_t)kMaxCus * kMaxPerCu) grid = (int64_t)kMaxCus * kMaxPerCu;
     if (grid > units) grid = units;  // every work-group must own at least one unit
     if (grid < 1) grid = 1;
     cfg.grid = (int)grid;
@@ -90,11 +136,15 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
 
 int slot_floats(const GemmConfig &cfg);
 
+// The workspace starts with a fixed region of arrival counters, one per
+// column tile, big enough for the finest tiling (16 columns) of the largest N.
+// It never moves, whatever the shape, so any sequence of calls on one
+// workspace finds every counter it uses at zero; the fp32 partial slots
+// follow it.
 size_t workspace_bytes_for(const GemmConfig &cfg, int N)
 {
-    const size_t cols = (size_t)N / (64 * cfg.nw);
-    const size_t counter_bytes = ((cols * 4 + 255) / 256) * 256;
-    return counter_bytes + (size_t)cfg.grid * 2 * (size_t)slot_floats(cfg) * sizeof(float);
+    (void)N;
+    return kCounterRegionBytes + (size_t)cfg.grid * 2 * (size_t)slot_floats(cfg) * sizeof(float);
 }
 
 namespace {
@@ -206,8 +256,7 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
     for (int64_t m0 = 0; m0 < M; m0 += 128) {
         const int mp = (M - m0) < 128 ? (int)(M - m0) : 128;
         const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus);
-        const size_t cols = (size_t)N / (64 * cfg.nw);
-        const size_t counter_bytes = ((cols * 4 + 255) / 256) * 256;
+        const size_t counter_bytes = kCounterRegionBytes;
         GemmProblem p;
         p.A = A + m0 * K;
         p.W = (const uint32_t *)w_packed;
@@ -220,6 +269,17 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         p.K = (int)K;
         p.G = (int)G;
         p.group_units = gu;
+        p.gshift = -1;
+        p.gmagic = 0;
+        if (gu > 0) {
+            if ((gu & (gu - 1)) == 0) {
+                int sh = 0;
+                while ((1 << sh) < gu) ++sh;
+                p.gshift = sh;
+            } else {
+                p.gmagic = (uint32_t)(((uint64_t)1 << 32) / (uint64_t)gu + 1);
+            }
+        }
         const hipError_t e = launch_gemm(cfg, p, stream);
         if (e != hipSuccess) return MARLIN_ERR_HIP;
     }

@@ -46,6 +46,8 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kLdsBytes = 160 * 1024;
 constexpr int kAuxNonTemporal = 2;  // cache-policy bit: non-temporal (streamed once)
+// Word 3 of a gfx9 buffer descriptor for raw (untyped) dword access.
+constexpr int kBufferFlags = 0x00020000;
 
 // s_waitcnt immediate for gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4]<<14.
 template <int V>
@@ -72,28 +74,37 @@ __device__ __forceinline__ void lds_barrier()
 
 __device__ __forceinline__ half2_t as_h2(uint32_t x) { return __builtin_bit_cast(half2_t, x); }
 
-// (x & m) | o in one VALU instruction (the compiler otherwise splits it when
-// it hoists the masks).
-__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t o)
+// Masks of the int4 -> fp16 conversion.  They are made opaque once per
+// kernel (an empty asm that "redefines" them in vector registers) so that
+// (x & m) | o selects the single v_and_or_b32 with register operands instead
+// of an and/or pair with literal constants.
+struct DequantConsts {
+    uint32_t lo, hi, ex;
+};
+
+__device__ __forceinline__ DequantConsts dequant_consts()
 {
-    uint32_t r;
-    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(m), "v"(o));
-    return r;
+    DequantConsts k{0x000F000Fu, 0x00F000F0u, 0x64006400u};
+    asm volatile("" : "+v"(k.lo), "+v"(k.hi), "+v"(k.ex));
+    return k;
 }
 
 // Eight codes of one packed word -> the eight fp16 values q - 8 in element
-// order j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).
-__device__ __forceinline__ half8_t dequant8(uint32_t x)
+// order j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).  Low nibbles
+// of each 16-bit half land in the low mantissa bits of 1024.0 (0x6400):
+// 1024 + q, minus 1032 gives q - 8 exactly.  The next nibble lands 4 bits
+// higher: 1024 + 16q, and (1024 + 16q) / 16 - 72 = q - 8 in one fma.  A shift
+// by 8 brings the other two nibbles of each half into the same positions.
+__device__ __forceinline__ half8_t dequant8(uint32_t x, const DequantConsts &k)
 {
-    const uint32_t kLo = 0x000F000Fu, kHi = 0x00F000F0u, kExp = 0x64006400u;
     const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
     const half2_t mul = {(_Float16)0.0625f, (_Float16)0.0625f};
     const half2_t add = {(_Float16)-72.0f, (_Float16)-72.0f};
     const uint32_t y = x >> 8;
-    const half2_t r0 = as_h2(and_or(x, kLo, kExp)) - sub;
-    const half2_t r1 = __builtin_elementwise_fma(as_h2(and_or(x, kHi, kExp)), mul, add);
-    const half2_t r2 = as_h2(and_or(y, kLo, kExp)) - sub;
-    const half2_t r3 = __builtin_elementwise_fma(as_h2(and_or(y, kHi, kExp)), mul, add);
+    const half2_t r0 = as_h2((x & k.lo) | k.ex) - sub;
+    const half2_t r1 = __builtin_elementwise_fma(as_h2((x & k.hi) | k.ex), mul, add);
+    const half2_t r2 = as_h2((y & k.lo) | k.ex) - sub;
+    const half2_t r3 = __builtin_elementwise_fma(as_h2((y & k.hi) | k.ex), mul, add);
     return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
 }
 
@@ -172,6 +183,14 @@ __device__ __forceinline__ void cursor_next(Cursor &cu, int KU)
         cu.done = rem <= 0;
         cu.ku_end = rem < KU ? (int)rem : KU;
     }
+}
+
+// Scale row of 128-row block ku: ku / group_units, by a shift when the group
+// is a power-of-two number of blocks, else by a multiply with the rounded-up
+// reciprocal 2^32 / group_units (exact for ku, group_units < 2^16).
+__device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)
+{
+    return p.gshift >= 0 ? (ku >> p.gshift) : (int)__umulhi((uint32_t)ku, p.gmagic);
 }
 
 __device__ __forceinline__ int64_t range_start(int w, int64_t total, int grid)
@@ -269,198 +288,261 @@ __device__ __forceinline__ void publish_and_reduce(const GemmProblem &p, const i
 // ---------------------------------------------------------------------------
 // Kernel 1 (decode batches, M <= 32): register streaming.
 //
-// Every wave of a work-group takes its own 128-row block of a stage (waves
-// split K), so no weight or activation byte is shared between waves: each
-// lane loads exactly its MFMA operands (16-byte non-temporal loads of the
-// pre-shuffled weights, 16-byte loads of the activation rows, which hit L2)
-// straight into a D-deep ring of registers.  The loop is unrolled over the
-// ring so register slots are static and the compiler's vmcnt waits keep D-1
-// stages in flight.  Waves meet only at the end of a column segment, where
-// their fp32 tiles are summed in LDS (Algorithm 1's reduction across waves
-// that share an output tile).
-template <int MB, int KW, int D, bool PER_CHANNEL>
-__global__ void __launch_bounds__(64 * KW, 1) w4a16_stream_kernel(GemmProblem p)
+// A work-group owns a column tile of 16*NB columns (NB 16-column blocks) over
+// a range of 128-row blocks of K (the striped partition); its KW waves take
+// consecutive 128-row blocks of each stage (waves split K), so no weight or
+// activation byte is shared between waves: each lane loads exactly its MFMA
+// operands (16-byte non-temporal buffer loads of the pre-shuffled weights,
+// 16-byte loads of the activation rows, which hit L2) straight into a D-deep
+// ring of registers.  The loop is unrolled over the ring so register slots
+// are static and the compiler's vmcnt waits keep D-1 stages in flight.  Waves
+// meet only at the end of a column segment, where their fp32 tiles are summed
+// in LDS (Algorithm 1's reduction across waves that share an output tile).
+// Narrow tiles (NB = 1) give enough whole columns to occupy every compute unit
+// without splitting K across work-groups on small layers.
+template <int MB, int NB, int KW, int D, int OCC, bool PER_CHANNEL>
+__global__ void __launch_bounds__(64 * KW, OCC) w4a16_stream_kernel(GemmProblem p)
 {
-    constexpr int kBlocks = 4 * MB;
-    constexpr int kOwn = kBlocks / KW;
-    static_assert(kBlocks % KW == 0, "output blocks must split evenly over waves");
+    constexpr int kBlocks = NB * MB;               // 16x16 output blocks per wave
+    constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
+    constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
     __shared__ float4_t red[KW * kBlocks * 64];
     __shared__ int flags[2];
 
     const int lane = threadIdx.x & 63;
-    const int kw = threadIdx.x >> 6;
+    const DequantConsts dq = dequant_consts();
+    // wave index as a scalar: all cursor and address arithmetic below is uniform
+    const int kw = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lg = lane >> 4;
     const int KU = p.K >> 7;
-    const int cols = p.N >> 6;
-    const int64_t total = (int64_t)cols * KU;
+    const int cols = p.N / (16 * NB);
+    const int total = cols * KU;  // < 2^31 (host checks K * N)
     const int grid = gridDim.x;
     const int wg = blockIdx.x;
-    const int64_t u0 = range_start(wg, total, grid);
-    const int64_t u1 = range_start(wg + 1, total, grid);
-    const int first_col = (int)(u0 / KU);
+    const int u0 = (int)range_start(wg, total, grid);
+    const int u1 = (int)range_start(wg + 1, total, grid);
+    const int first_col = u0 / KU;
 
     // Stages of this work-group: each segment (its part of one column) takes
     // ceil(length / KW) stages.
     int n_st = 0;
-    for (int64_t u = u0; u < u1;) {
-        const int64_t c = u / KU;
-        const int64_t e = (c + 1) * KU < u1 ? (c + 1) * KU : u1;
-        n_st += (int)((e - u + KW - 1) / KW);
+    for (int u = u0; u < u1;) {
+        const int e = (u / KU + 1) * KU < u1 ? (u / KU + 1) * KU : u1;
+        n_st += (e - u + KW - 1) / KW;
         u = e;
     }
 
-    Cursor ld, cp;
-    cursor_init(ld, u0, u1, KU);
+    // Stage cursors (wave-uniform): column tile c, first 128-row block ku of
+    // the stage, segment [begin, end) within the column.
+    struct Cur {
+        int c, ku, begin, end;
+    };
+    auto cur_init = [&](Cur &q) {
+        q.c = first_col;
+        q.ku = u0 - q.c * KU;
+        q.begin = q.ku;
+        q.end = (u1 - q.c * KU) < KU ? (u1 - q.c * KU) : KU;
+    };
+    auto cur_next = [&](Cur &q) {
+        q.ku += KW;
+        if (q.ku >= q.end) {
+            q.c += 1;
+            q.ku = 0;
+            q.begin = 0;
+            q.end = (u1 - q.c * KU) < KU ? (u1 - q.c * KU) : KU;
+        }
+    };
+    Cur ld, cp;
+    cur_init(ld);
     cp = ld;
 
-    u32x4_t wr[D][4];
-    half8_t ar[D][4 * MB];
-    half8_t sr[D][2];
-
-    // Every stage issues the same loads, unconditionally (past the end of the
-    // range they all read one fixed line), so the compiler's vmcnt waits see
-    // a static pattern and keep D - 1 stages in flight.
-    auto issue = [&](int j, const Cursor &cu) {
-        const bool valid = !cu.done;
-        int ku = cu.ku + kw;
-        if (ku >= cu.ku_end) ku = cu.ku;  // idle wave: any valid block, result unused
-        const int c = cu.c;
-        const u32x4_t *wsrc = (const u32x4_t *)p.W + ((int64_t)(c * KU + ku) * 4) * 64 + lane;
-        const int wstep = valid ? 64 : 0;
-        if (!valid) wsrc = (const u32x4_t *)p.W;
+    // Loads are buffer loads: a fixed per-lane byte offset in one VGPR, the
+    // per-stage offset in a scalar register, so the stream costs no vector
+    // address arithmetic.  Past the end of the range a stage uses an empty
+    // descriptor: its loads are out of range, touch no memory and return 0,
+    // which keeps the pattern of loads per stage static.  Activation rows are
+    // loaded only by lanes whose row exists (the other lanes' MFMA columns are
+    // never stored).
+    const uint32_t w_lane = lane * 16;
+    const int arow = lane & 15;
+    uint32_t a_lane[MB];
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) wr[j][nb] = __builtin_nontemporal_load(wsrc + nb * wstep);
-        const int astep = valid ? 32 : 0;
+    for (int mb = 0; mb < MB; ++mb) a_lane[mb] = (uint32_t)((mb * 16 + arow) * p.K + 8 * lg) * 2;
+    const uint32_t s_lane = lg * 32;
+    const int w_bytes = (int)((uint32_t)p.K * (uint32_t)(p.N / 2));
+    const int a_bytes = p.M * p.K * 2;
+    const int s_bytes = p.G * p.N * 2;
+
+    u32x4_t wr[D][NB];
+    half8_t ar[D][4 * MB];
+    half8_t sr[D][kSLoads];
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+#pragma unroll
+        for (int i = 0; i < 4 * MB; ++i) ar[j][i] = half8_t{};
+
+    auto issue = [&](int j, const Cur &cu, bool valid) {
+        int ku = cu.ku + kw;
+        ku = ku < cu.end ? ku : cu.ku;  // idle wave: any valid block, result unused
+        const int nbg = cu.c * NB;      // first global 16-column block of the tile
+        const __amdgpu_buffer_rsrc_t rw =
+            __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, valid ? w_bytes : 0, kBufferFlags);
+        const int w_off = (((nbg >> 2) * KU + ku) * 4 + (nbg & 3)) << 10;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+            wr[j][b] = __builtin_bit_cast(
+                u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, w_off, kAuxNonTemporal));
+        const __amdgpu_buffer_rsrc_t ra =
+            __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, valid ? a_bytes : 0, kBufferFlags);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
-            int row = mb * 16 + (lane & 15);
-            row = row < p.M ? row : p.M - 1;
-            const uint16_t *arow = p.A + (int64_t)row * p.K + ku * 128 + 8 * lg;
-            if (!valid) arow = p.A;
+            if (mb * 16 + arow < p.M) {
 #pragma unroll
-            for (int t = 0; t < 4; ++t) ar[j][mb * 4 + t] = *(const half8_t *)(arow + t * astep);
+                for (int t = 0; t < 4; ++t)
+                    ar[j][mb * 4 + t] = __builtin_bit_cast(
+                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(ra, a_lane[mb] + t * 64, ku << 8, 0));
+            }
         }
         if constexpr (!PER_CHANNEL) {
-            const uint16_t *ssrc = p.S + ((int64_t)c * p.G + ku / p.group_units) * 64 + lg * 16;
-            if (!valid) ssrc = p.S;
-            sr[j][0] = *(const half8_t *)ssrc;
-            sr[j][1] = *(const half8_t *)(ssrc + (valid ? 8 : 0));
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, valid ? s_bytes : 0, kBufferFlags);
+            const int s_off = (((nbg >> 2) * p.G + scale_row_of(ku, p)) << 7) + (nbg & 3) * 8;
+#pragma unroll
+            for (int i = 0; i < kSLoads; ++i)
+                sr[j][i] = __builtin_bit_cast(
+                    half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
         }
     };
 
-    float4_t acc[4][MB];
+    float4_t acc[NB][MB];
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
+        for (int mb = 0; mb < MB; ++mb) acc[b][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
 
+    // MFMA order: k-step outer, column block inner, so consecutive MFMAs are
+    // independent; group scales fold in after the stage's last MFMA.
     auto compute = [&](int j) {
         if constexpr (!PER_CHANNEL) {
-            float sc[16];
+            float4_t tmp[NB][MB];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) { sc[i] = (float)sr[j][0][i]; sc[8 + i] = (float)sr[j][1][i]; }
+            for (int t = 0; t < 4; ++t)
 #pragma unroll
-            for (int nb = 0; nb < 4; ++nb) {
-                float4_t tmp[MB];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const half8_t b = dequant8(wr[j][nb][t]);
+                for (int b = 0; b < NB; ++b) {
+                    const half8_t w = dequant8(wr[j][b][t], dq);
 #pragma unroll
                     for (int mb = 0; mb < MB; ++mb)
-                        tmp[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                            b, ar[j][mb * 4 + t], t == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : tmp[mb], 0, 0, 0);
+                        tmp[b][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                            w, ar[j][mb * 4 + t], t == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : tmp[b][mb], 0, 0, 0);
                 }
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                // scales of block b: halves 4b .. 4b+3 of this lane's run
+                const half8_t sv = sr[j][b >> 1];
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[nb][mb][i] += tmp[mb][i] * sc[nb * 4 + i];
+                    for (int i = 0; i < 4; ++i) acc[b][mb][i] += tmp[b][mb][i] * (float)sv[(b & 1) * 4 + i];
             }
         } else {
 #pragma unroll
             for (int t = 0; t < 4; ++t)
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
-                    const half8_t b = dequant8(wr[j][nb][t]);
+                for (int b = 0; b < NB; ++b) {
+                    const half8_t w = dequant8(wr[j][b][t], dq);
 #pragma unroll
                     for (int mb = 0; mb < MB; ++mb)
-                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(b, ar[j][mb * 4 + t], acc[nb][mb], 0, 0, 0);
+                        acc[b][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w, ar[j][mb * 4 + t], acc[b][mb], 0, 0, 0);
                 }
         }
     };
 
-    // block b = nb*MB + mb; wave kw owns b = kw + j*KW after the LDS reduction
+    // block index blk = b*MB + mb; wave kw owns blk = kw + j*KW (< kBlocks)
     auto own = [&](int j) { return kw + j * KW; };
     auto store_c = [&](int c, const float4_t *out) {
 #pragma unroll
         for (int j = 0; j < kOwn; ++j) {
-            const int b = kw + j * KW;
-            const int nb = b / MB, mb = b % MB;
-            const int m = mb * 16 + (lane & 15);
+            const int blk = kw + j * KW;
+            if (blk >= kBlocks) break;
+            const int b = blk / MB, mb = blk % MB;
+            const int m = mb * 16 + arow;
             if (m < p.M) {
+                const int nbg = c * NB + b;
                 float4_t v = out[j];
                 if constexpr (PER_CHANNEL) {
-                    const half4_t s4 = *(const half4_t *)(p.S + (int64_t)c * 64 + lg * 16 + nb * 4);
+                    const half4_t s4 = *(const half4_t *)(p.S + (int64_t)(nbg >> 2) * 64 + lg * 16 + (nbg & 3) * 4);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) v[i] *= (float)s4[i];
                 }
                 const half4_t h = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
-                *(half4_t *)(p.C + (int64_t)m * p.N + c * 64 + nb * 16 + lg * 4) = h;
+                *(half4_t *)(p.C + (int64_t)m * p.N + nbg * 16 + lg * 4) = h;
             }
         }
     };
 
     int pcol[2] = {-1, -1};
     const int slot_floats = kBlocks * 256;
-    auto finish_segment = [&](const Cursor &cu) {
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) red[(kw * kBlocks + nb * MB + mb) * 64 + lane] = acc[nb][mb];
-        lds_barrier();
+    auto finish_segment = [&](const Cur &cu) {
         float4_t out[kOwn];
+        if constexpr (KW > 1) {
 #pragma unroll
-        for (int j = 0; j < kOwn; ++j) {
-            const int b = own(j);
-            float4_t s = red[b * 64 + lane];
+            for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int k2 = 1; k2 < KW; ++k2) s += red[(k2 * kBlocks + b) * 64 + lane];
-            out[j] = s;
+                for (int mb = 0; mb < MB; ++mb) red[(kw * kBlocks + b * MB + mb) * 64 + lane] = acc[b][mb];
+            lds_barrier();
+#pragma unroll
+            for (int j = 0; j < kOwn; ++j) {
+                const int blk = own(j);
+                if (blk < kBlocks) {
+                    float4_t s = red[blk * 64 + lane];
+#pragma unroll
+                    for (int k2 = 1; k2 < KW; ++k2) s += red[(k2 * kBlocks + blk) * 64 + lane];
+                    out[j] = s;
+                }
+            }
+            lds_barrier();
+        } else {
+#pragma unroll
+            for (int j = 0; j < kOwn; ++j) out[j] = acc[j / MB][j % MB];
         }
-        lds_barrier();
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
-        if (cu.seg_begin == 0 && cu.ku_end == KU) {
+            for (int mb = 0; mb < MB; ++mb) acc[b][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
+        if (cu.begin == 0 && cu.end == KU) {
             store_c(cu.c, out);
         } else {
             const int which = (cu.c == first_col) ? 0 : 1;
             pcol[which] = cu.c;
             float *slot = p.partials + ((int64_t)wg * 2 + which) * slot_floats;
 #pragma unroll
-            for (int j = 0; j < kOwn; ++j) store_partial(slot, own(j), lane, out[j]);
+            for (int j = 0; j < kOwn; ++j)
+                if (own(j) < kBlocks) store_partial(slot, own(j), lane, out[j]);
         }
     };
 
 #pragma unroll
     for (int j = 0; j < D; ++j) {
-        issue(j, ld);
-        if (!ld.done) cursor_next<KW>(ld, KU);
+        issue(j, ld, j < n_st);
+        cur_next(ld);
     }
     const int iters = (n_st + D - 1) / D;
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int j = 0; j < D; ++j) {
-            if (it * D + j < n_st) {
-                if (cp.ku + kw < cp.ku_end) compute(j);
-                if (cp.ku + KW >= cp.ku_end) finish_segment(cp);
-                cursor_next<KW>(cp, KU);
+            const int st = it * D + j;
+            if (st < n_st) {
+                if (cp.ku + kw < cp.end) compute(j);
+                if (cp.ku + KW >= cp.end) finish_segment(cp);
+                cur_next(cp);
             }
-            issue(j, ld);
-            if (!ld.done) cursor_next<KW>(ld, KU);
+            issue(j, ld, st + D < n_st);
+            cur_next(ld);
         }
     }
-    publish_and_reduce<kOwn>(p, pcol, flags, wg, KU, total, grid, slot_floats, lane, own, store_c);
+    auto own_valid = [&](int j) { return own(j) < kBlocks ? own(j) : 0; };
+    publish_and_reduce<kOwn>(p, pcol, flags, wg, KU, (int64_t)total, grid, slot_floats, lane, own_valid,
+                             store_c);
 }
 
 // ---------------------------------------------------------------------------
@@ -475,6 +557,7 @@ __global__ void __launch_bounds__(64 * NW * KW, 1)
     __shared__ __attribute__((aligned(1024))) uint8_t smem[Gm::kSmemBytes];
 
     const int lane = threadIdx.x & 63;
+    const DequantConsts dq = dequant_consts();
     const int wave = threadIdx.x >> 6;
     const int nw = (NW == 1) ? 0 : wave % NW;
     const int kw = (KW == 1) ? 0 : wave / NW;
@@ -519,7 +602,7 @@ __global__ void __launch_bounds__(64 * NW * KW, 1)
                                              LDS_PTR(base + (kw * Gm::kAFrags + f) * 1024), 16, 0, 0);
         }
         if constexpr (!PER_CHANNEL) {
-            const int r = ku / p.group_units;
+            const int r = scale_row_of(ku, p);
             const uint16_t *ssrc = p.S + ((int64_t)c64 * p.G + r) * 64 + (lane & 31) * 2;
             if (lane < 32)
                 __builtin_amdgcn_global_load_lds((const void *)ssrc,
@@ -655,7 +738,7 @@ __global__ void __launch_bounds__(64 * NW * KW, 1)
                     float4_t tmp[MB];
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
-                        const half8_t b = dequant8(wv[t]);
+                        const half8_t b = dequant8(wv[t], dq);
 #pragma unroll
                         for (int mb = 0; mb < MB; ++mb)
                             tmp[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
@@ -689,7 +772,7 @@ __global__ void __launch_bounds__(64 * NW * KW, 1)
                     for (int mb = 0; mb < MB; ++mb) a[mb] = abase[(mb * 4 + t) * 64 + lane];
 #pragma unroll
                     for (int nb = 0; nb < 4; ++nb) {
-                        half8_t b = dequant8(wv[nb][t]);
+                        half8_t b = dequant8(wv[nb][t], dq);
                         if constexpr (!PER_CHANNEL) b = scale8(b, s2[nb]);
 #pragma unroll
                         for (int mb = 0; mb < MB; ++mb)
@@ -728,23 +811,35 @@ hipError_t launch_variant(const GemmConfig &cfg, const GemmProblem &p, hipStream
 
 }  // namespace
 
-int slot_floats(const GemmConfig &cfg) { return cfg.nw * 4 * cfg.mb * 256; }
+int slot_floats(const GemmConfig &cfg)
+{
+    return cfg.kind == kKindStream ? cfg.nb * cfg.mb * 256 : cfg.nw * 4 * cfg.mb * 256;
+}
 
-template <int MB, int KW, int D>
+template <int MB, int NB>
 hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
+    constexpr int KW = kStreamWaves, OCC = kStreamOcc;
+    constexpr int D = (MB == 1) ? (NB == 4 ? 3 : NB == 2 ? 4 : 6) : (NB == 4 ? 2 : 4);
     GemmProblem arg = p;
     void *args[] = {&arg};
-    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, KW, D, true>
-                                          : (const void *)&w4a16_stream_kernel<MB, KW, D, false>;
+    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, KW, D, OCC, true>
+                                          : (const void *)&w4a16_stream_kernel<MB, NB, KW, D, OCC, false>;
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * KW), args, 0, stream);
 }
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     if (cfg.kind == kKindStream) {
-        if (cfg.mb == 1 && cfg.kw == 4) return launch_stream<1, 4, kStreamDepthMB1>(cfg, p, stream);
-        if (cfg.mb == 2 && cfg.kw == 4) return launch_stream<2, 4, kStreamDepthMB2>(cfg, p, stream);
+        switch (cfg.mb * 10 + cfg.nb) {
+        case 11: return launch_stream<1, 1>(cfg, p, stream);
+        case 12: return launch_stream<1, 2>(cfg, p, stream);
+        case 14: return launch_stream<1, 4>(cfg, p, stream);
+        case 21: return launch_stream<2, 1>(cfg, p, stream);
+        case 22: return launch_stream<2, 2>(cfg, p, stream);
+        case 24: return launch_stream<2, 4>(cfg, p, stream);
+        default: return hipErrorInvalidValue;
+        }
         return hipErrorInvalidValue;
     }
     const int key = cfg.mb * 100 + cfg.nw * 10 + cfg.kw;

@@ -15,12 +15,13 @@ namespace marlin {
 //   grid: work-groups (Stream-K workers)
 constexpr int kKindStream = 0;  // register-streaming kernel (M <= 32)
 constexpr int kKindLds = 1;     // LDS-pipeline kernel (M > 32)
-constexpr int kStreamDepthMB1 = 6;
-constexpr int kStreamDepthMB2 = 4;
+constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
+constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
 struct GemmConfig {
     int kind;
     int mb;
+    int nb;  // register-streaming kernel: 16-column blocks per column tile (1, 2 or 4)
     int nw;
     int kw;
     int grid;
@@ -38,11 +39,17 @@ struct GemmProblem {
     int K;
     int G;                // scale rows
     int group_units;      // 128-row blocks per scale group; 0 = per-channel
+    int gshift;           // log2(group_units) if a power of two, else -1
+    uint32_t gmagic;      // ceil(2^32 / group_units) when gshift < 0
 };
 
 // Upper bound on compute units used (MI355X has 256).  Workspace sizes are
 // computed with this bound, never with the device's.
 constexpr int kMaxCus = 256;
+constexpr int kMaxPerCu = 2;  // work-groups per compute unit, at most
+// Arrival counters at the start of every workspace: one per 16-column tile of
+// the largest N (2^20).
+constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4;
 
 // Device facts cached per device.
 int device_cu_count(int device);

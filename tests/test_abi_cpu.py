@@ -55,7 +55,7 @@ def test_size_queries(L):
     assert L.marlin_packed_scale_bytes(4096, 4096, -1) == 4096 * 2
     assert L.marlin_packed_scale_bytes(4096, 4096, 4096) == 4096 * 2
     assert L.marlin_packed_scale_bytes(4096, 4096, 256) == 16 * 4096 * 2
-    for bad in [(4000, 4096), (4096, 4000), (0, 64), (128, 0), (64, 64)]:
+    for bad in [(4000, 4096), (4096, 4000), (0, 64), (128, 0), (64, 64), (1 << 17, 1 << 15)]:
         assert L.marlin_packed_weight_bytes(*bad) == 0
     assert L.marlin_packed_scale_bytes(4096, 4096, 64) == 0
     assert L.marlin_packed_scale_bytes(4096, 4096, 384) == 0  # does not divide K
