@@ -79,8 +79,8 @@ def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the GEMM would shard by columns or rows with an RCCL all-reduce; "
-              "see the design notes). Run with --gpus 1.", file=sys.stderr)
+              "(the GEMM would shard by columns, or by rows with an RCCL "
+              "all-reduce of C). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -304,7 +304,7 @@ def main():
                      "traffic_unit": "HBM bytes per launch (step average)",
                      "algorithmic_bytes_per_launch": round(step_bytes / len(M_SWEEP)),
                      "avg_launch_us": round(avg_launch_us, 3),
-                     "kernel": "w4a16_stream_kernel (M <= 32) and w4a16_lds_kernel (M = 64, 128)"},
+                     "kernel": "w4a16_stream_kernel"},
         "roof_frac_step": round(sum(R.w4a16_t_roof(M, N, K, g) for M in M_SWEEP) /
                                 (ms_per_step * 1e-3), 4),
         "min_roof_frac_M_le_16": min(r["roof_frac"] for r in small),

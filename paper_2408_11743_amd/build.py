@@ -18,7 +18,11 @@ ARCH = "gfx950"
 
 # Packed fp32 instructions are disabled for all device code: plain float code
 # is compiled to scalar-per-lane fp32 instructions.
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# MFMA results are kept in ordinary vector registers (the kernels have
+# registers to spare at one wave per SIMD), so the fp32 fold after each
+# stage reads them without accumulator-register moves.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def hipcc() -> str:

@@ -57,9 +57,9 @@ int device_cu_count(int device)
     return cus;
 }
 
-// Tuning override, read once: MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>" forces
-// the column-tile width and the work-group count of the register-streaming
-// kernel (sweeps only; the heuristic below is the default).
+// Tuning override, read once: MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>"
+// forces the column-tile width and the work-group count (sweeps only; the
+// heuristic below is the default).
 struct ForcedConfig {
     int nb = 0;
     int grid = 0;
@@ -85,17 +85,13 @@ static const ForcedConfig &forced()
     return f;
 }
 
-// Kernel choice by rows of A per pass:
-//   M <= 32: register-streaming kernel, mb = 1 (M <= 16) or 2, kStreamWaves
-//            waves splitting K, kStreamOcc work-groups per CU, column tiles of
-//            16 * nb columns;
-//   M <= 64 / 128: LDS-pipeline kernel, mb = 4 / 8, 4 waves splitting N, 1 per
-//            CU (narrower nw when N is not a multiple of 256 or 128).
-// The tile width nb is 4 (64 columns: the activation fragments of a 128-row
-// block serve four weight blocks) except on small layers (K * N <= 2^24),
-// where 32-column tiles halve the K range each work-group covers; nb = 1 or 2
-// also when N is not a multiple of 64 * nb (measured on MI355X, see the
-// design notes).
+// Configuration by rows of A per pass: mb = ceil(M / 16) rounded up to 1, 2,
+// 4 or 8; kStreamWaves waves splitting K, kStreamOcc work-groups per CU.
+// The column tile is 64 columns (nb = 4: the activation fragments of a
+// 128-row block serve four weight blocks) except on small layers
+// (K * N <= 2^24), where 32-column tiles halve the K range each work-group
+// covers; nb = 1 or 2 also when N is not a multiple of 64 * nb (choices
+// measured on MI355X).
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
 GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
@@ -105,28 +101,15 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     const int KU = K / 128;
     const int tiles16 = N / 16;
     const int ncu = cus < kMaxCus ? cus : kMaxCus;
-    int per_cu;
-    if (M <= 32) {
-        cfg.kind = kKindStream;
-        cfg.mb = (M <= 16) ? 1 : 2;
-        cfg.nw = 1;
-        cfg.kw = kStreamWaves;
-        per_cu = kStreamOcc;
-        const bool small = (int64_t)K * N <= ((int64_t)1 << 24);
-        cfg.nb = (!small && tiles16 % 4 == 0) ? 4 : (tiles16 % 2 == 0 ? 2 : 1);
-        if (forced().nb && tiles16 % forced().nb == 0) cfg.nb = forced().nb;
-    } else {
-        cfg.kind = kKindLds;
-        cfg.mb = (M <= 64) ? 4 : 8;
-        cfg.nb = 4;
-        cfg.kw = 1;
-        cfg.nw = (tiles16 % 16 == 0) ? 4 : (tiles16 % 8 == 0) ? 2 : 1;
-        per_cu = 1;
-    }
-    const int64_t cols = (cfg.kind == kKindStream) ? tiles16 / cfg.nb : tiles16 / (4 * cfg.nw);
-    const int64_t units = cols * KU;
-    int64_t grid = (int64_t)ncu * per_cu;
-    if (cfg.kind == kKindStream && forced().grid) grid = forced().grid;
+    cfg.mb = (M <= 16) ? 1 : (M <= 32) ? 2 : (M <= 64) ? 4 : 8;
+    const bool small = (int64_t)K * N <= ((int64_t)1 << 24);
+    cfg.nb = (!small && tiles16 % 4 == 0) ? 4 : (tiles16 % 2 == 0 ? 2 : 1);
+    if (cfg.mb >= 4 && cfg.nb == 1) cfg.nb = 2;
+    if (cfg.mb == 8) cfg.nb = 2;  // register budget: 8 row blocks x 64 columns spill
+    if (forced().nb && tiles16 % forced().nb == 0 && !(cfg.mb >= 4 && forced().nb == 1)) cfg.nb = forced().nb;
+    const int64_t units = (int64_t)(tiles16 / cfg.nb) * KU;
+    int64_t grid = (int64_t)ncu * kStreamOcc;
+    if (forced().grid) grid = forced().grid;
     if (grid > (int64_t)kMaxCus * kMaxPerCu) grid = (int64_t)kMaxCus * kMaxPerCu;
     if (grid > units) grid = units;  // every work-group must own at least one unit
     if (grid < 1) grid = 1;
@@ -268,18 +251,14 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         p.N = (int)N;
         p.K = (int)K;
         p.G = (int)G;
+        p.KU = (int)(K / 128);
+        p.units = (int)(N / (16 * cfg.nb)) * p.KU;
+        p.per_wg = p.units / cfg.grid;
+        p.extra = p.units % cfg.grid;
         p.group_units = gu;
-        p.gshift = -1;
-        p.gmagic = 0;
-        if (gu > 0) {
-            if ((gu & (gu - 1)) == 0) {
-                int sh = 0;
-                while ((1 << sh) < gu) ++sh;
-                p.gshift = sh;
-            } else {
-                p.gmagic = (uint32_t)(((uint64_t)1 << 32) / (uint64_t)gu + 1);
-            }
-        }
+        // Exact for every block index below 2^13 (K <= 2^20): with
+        // e = gmagic * gu - 2^26 < gu <= 2^13, ku * e < 2^26.
+        p.gmagic = gu > 0 ? (uint32_t)((((uint64_t)1 << 26) + (uint64_t)gu - 1) / (uint64_t)gu) : 0u;
         const hipError_t e = launch_gemm(cfg, p, stream);
         if (e != hipSuccess) return MARLIN_ERR_HIP;
     }

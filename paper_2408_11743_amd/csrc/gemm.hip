@@ -1,34 +1,38 @@
 // W4A16 GEMM for gfx950: C[M,N] = A[M,K] * (s * (q - 8)), fp32 accumulation.
 //
-// Design (the paper's Section 3.4 ideas, re-derived for CDNA4):
+// Design (the ideas of the paper's Section 3.4, re-derived for CDNA4):
 //  * Transposed product, as the paper does for its sparse kernel (Section 4):
 //    each v_mfma_f32_16x16x32_f16 multiplies a 16(n) x 32(k) block of W^T
 //    (first operand) by a 32(k) x 16(m) block of A^T.  A lane's first operand
 //    is 8 consecutive k of one column n: exactly one packed 32-bit word of
 //    codes, so one 16-byte load feeds four MFMA steps ("Maximizing Loading
 //    Bandwidth", "Dequantization and Tensor Cores").
-//  * Weights and activations reach LDS through gfx950's direct-to-LDS loads
-//    (global_load_lds_dwordx4), the CDNA counterpart of cp.async, with the
-//    non-temporal bit on the weight stream (the paper's evict_first).  P stages
-//    are in flight; the kernel waits on vmcnt per stage with static counts
-//    ("Memory Load Pipelining").
-//  * int4 -> fp16 by bit operations: mask the code into the low mantissa bits
-//    of the fp16 number 1024 (0x6400) and subtract 1032 exactly; codes in the
-//    next nibble become 1024 + 16q and are fixed by one fma (x/16 - 72).  Two
-//    codes per 32-bit register at a time ("Dequantization and Tensor Cores").
-//  * Group scales multiply each 128-row fp32 partial product (one group or
-//    part of one); per-channel scales multiply the final sum once
-//    ("Groups and Instruction Ordering").
-//  * Waves of a work-group split N (sharing the activation tile in LDS) or K
-//    (each with its own tile, reduced in LDS at the end: Algorithm 1's layout).
+//  * int4 -> fp16 by bit operations only.  A code masked into the low bits of
+//    a zero-exponent fp16 number IS the fp16 value q * 2^-24 (a subnormal,
+//    which the matrix cores consume exactly); the code one nibble higher is
+//    16 q * 2^-24.  So one AND yields two operands, and a word of eight codes
+//    costs one shift and four ANDs.  The factor 16 of the upper nibbles is
+//    moved to the activations (their elements 2, 3, 6, 7 are multiplied by
+//    1/16, exact for normal fp16), the zero point to one extra MFMA per
+//    k-step against the codes 8 (shared by all column blocks, subtracted),
+//    and 2^24 into the final conversion.  This is the magic-number idea of
+//    the "Dequantization and Tensor Cores" paragraph with the magic number 0:
+//    no subtraction is needed per weight at all.
+//  * Group scales multiply each 128-row fp32 partial product once, fused
+//    with the bias add (v_fma_mix_f32 reads the fp16 scale directly);
+//    per-channel scales multiply the final sum ("Groups and Instruction
+//    Ordering").
+//  * The four waves of a work-group take consecutive 128-row blocks of one
+//    column tile per stage and meet in LDS when a tile segment ends
+//    (Algorithm 1's reduction over waves that share an output tile).
 //  * Stream-K style striped partitioning over a persistent grid: work-group w
 //    owns the contiguous range [w*T/grid, (w+1)*T/grid) of (column tile,
 //    128-row block) units, column-major, wrapping into the next column
-//    ("Striped Partitioning").  Columns split across work-groups are combined
-//    through fp32 partial slots in the workspace; the last work-group to
-//    arrive (an agent-scope acq_rel counter) sums the slots in a fixed order
-//    and writes C, then resets the counter.  No work-group ever waits on
-//    another, so no co-residency is assumed.
+//    ("Striped Partitioning").  A column tile shared by several work-groups
+//    is combined through fp32 partial slots in the workspace; whichever
+//    work-group completes the tile's arrival count sums the slots in
+//    work-group order (bitwise reproducible) and writes C.  No work-group
+//    ever waits for another, so no co-residency is assumed.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -42,19 +46,15 @@ typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-#define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
-
-constexpr int kLdsBytes = 160 * 1024;
 constexpr int kAuxNonTemporal = 2;  // cache-policy bit: non-temporal (streamed once)
 // Word 3 of a gfx9 buffer descriptor for raw (untyped) dword access.
 constexpr int kBufferFlags = 0x00020000;
+constexpr float kTwo24 = 16777216.0f;  // undoes the 2^-24 of the subnormal operands
 
 // s_waitcnt immediate for gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4]<<14.
-template <int V>
-__device__ __forceinline__ void wait_vmcnt()
+__device__ __forceinline__ void wait_vmcnt0()
 {
-    static_assert(V >= 0 && V < 64, "vmcnt out of range");
-    __builtin_amdgcn_s_waitcnt((V & 15) | (7 << 4) | (15 << 8) | ((V >> 4) << 14));
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8) | (0 << 14));
     asm volatile("" ::: "memory");
 }
 
@@ -73,149 +73,75 @@ __device__ __forceinline__ void lds_barrier()
 }
 
 __device__ __forceinline__ half2_t as_h2(uint32_t x) { return __builtin_bit_cast(half2_t, x); }
+__device__ __forceinline__ uint32_t as_u32(half2_t x) { return __builtin_bit_cast(uint32_t, x); }
 
-// Masks of the int4 -> fp16 conversion.  They are made opaque once per
-// kernel (an empty asm that "redefines" them in vector registers) so that
-// (x & m) | o selects the single v_and_or_b32 with register operands instead
-// of an and/or pair with literal constants.
-struct DequantConsts {
-    uint32_t lo, hi, ex;
-};
-
-__device__ __forceinline__ DequantConsts dequant_consts()
+// Eight codes of one packed word -> eight MFMA operands in element order
+// j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).  Elements 0, 1, 4, 5
+// are q * 2^-24, elements 2, 3, 6, 7 are 16 q * 2^-24.
+__device__ __forceinline__ half8_t dequant_sub(uint32_t x)
 {
-    DequantConsts k{0x000F000Fu, 0x00F000F0u, 0x64006400u};
-    asm volatile("" : "+v"(k.lo), "+v"(k.hi), "+v"(k.ex));
-    return k;
-}
-
-// Eight codes of one packed word -> the eight fp16 values q - 8 in element
-// order j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).  Low nibbles
-// of each 16-bit half land in the low mantissa bits of 1024.0 (0x6400):
-// 1024 + q, minus 1032 gives q - 8 exactly.  The next nibble lands 4 bits
-// higher: 1024 + 16q, and (1024 + 16q) / 16 - 72 = q - 8 in one fma.  A shift
-// by 8 brings the other two nibbles of each half into the same positions.
-__device__ __forceinline__ half8_t dequant8(uint32_t x, const DequantConsts &k)
-{
-    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
-    const half2_t mul = {(_Float16)0.0625f, (_Float16)0.0625f};
-    const half2_t add = {(_Float16)-72.0f, (_Float16)-72.0f};
     const uint32_t y = x >> 8;
-    const half2_t r0 = as_h2((x & k.lo) | k.ex) - sub;
-    const half2_t r1 = __builtin_elementwise_fma(as_h2((x & k.hi) | k.ex), mul, add);
-    const half2_t r2 = as_h2((y & k.lo) | k.ex) - sub;
-    const half2_t r3 = __builtin_elementwise_fma(as_h2((y & k.hi) | k.ex), mul, add);
-    return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
+    return __builtin_bit_cast(half8_t, u32x4_t{x & 0x000F000Fu, x & 0x00F000F0u, y & 0x000F000Fu,
+                                               y & 0x00F000F0u});
 }
 
-// Multiply eight fp16 weights by one fp16 scale (four packed multiplies).
-__device__ __forceinline__ half8_t scale8(half8_t b, half2_t s)
+// Activation operand matching dequant_sub: elements 2, 3, 6, 7 times 1/16.
+__device__ __forceinline__ half8_t prescale(half8_t a)
 {
-    half2_t r0 = half2_t{b[0], b[1]} * s, r1 = half2_t{b[2], b[3]} * s;
-    half2_t r2 = half2_t{b[4], b[5]} * s, r3 = half2_t{b[6], b[7]} * s;
-    return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
+    const u32x4_t u = __builtin_bit_cast(u32x4_t, a);
+    const half2_t r = {(_Float16)0.0625f, (_Float16)0.0625f};
+    return __builtin_bit_cast(half8_t, u32x4_t{u[0], as_u32(as_h2(u[1]) * r), u[2], as_u32(as_h2(u[3]) * r)});
 }
 
-template <int MB, int NW, int KW, bool PER_CHANNEL>
-struct Geo {
-    static constexpr int kWaves = NW * KW;
-    static constexpr int kThreads = 64 * kWaves;
-    static constexpr int kAFrags = 4 * MB;                 // 1 KiB fragments per kw per stage
-    static constexpr int kAFragsPerWave = kAFrags / NW;
-    static constexpr int kABytes = KW * kAFrags * 1024;
-    static constexpr int kWBytes = KW * NW * 4 * 1024;
-    static constexpr int kSBytes = PER_CHANNEL ? 0 : KW * NW * 128;
-    static constexpr int kStageBytes = kABytes + kWBytes + kSBytes;
-    static constexpr int kBlocks = 4 * MB;                 // 16x16 output blocks per wave
-    static constexpr int kOwnBlocks = kBlocks / KW;        // blocks a wave owns after reduction
-    static constexpr int kRedBytes = (KW > 1) ? KW * NW * kBlocks * 1024 : 0;
-    static constexpr int kFlagBytes = 64;
-    static constexpr int kLoadsPerStage = 4 + kAFragsPerWave + (PER_CHANNEL ? 0 : 1);
-    // Stages: as many as fit in LDS, at most 4, and few enough that the loads
-    // issued after a stage stay within the 6-bit vmcnt counter.
-    static constexpr int kStagesFit = (kLdsBytes - kRedBytes - kFlagBytes) / kStageBytes;
-    static constexpr int kStagesCnt = 2 + 63 / kLoadsPerStage;
-    static constexpr int P0 = kStagesFit < kStagesCnt ? kStagesFit : kStagesCnt;
-    static constexpr int P = P0 > 4 ? 4 : P0;
-    static constexpr int kSmemBytes = P * kStageBytes + kRedBytes + kFlagBytes;
-    static constexpr int kSlotFloats = NW * kBlocks * 256;  // one partial tile, register layout
-    // Group scales: fp32 fold of each 128-row product for small M (cheapest
-    // in VALU there); fp16 scaling of the weights for larger M (no extra
-    // accumulators).
-    static constexpr bool kFold = !PER_CHANNEL && MB <= 2;
-    static_assert(kAFrags % NW == 0, "A fragments must split evenly over N-waves");
-    static_assert(kBlocks % KW == 0, "output blocks must split evenly over K-waves");
-    static_assert(P >= 2, "at least two pipeline stages must fit in LDS");
-    static_assert((P - 2) * kLoadsPerStage < 64, "vmcnt range");
-};
-
-// Position of a work-group in its range of units.  A stage covers up to KW
-// consecutive 128-row blocks of one column tile.
-struct Cursor {
-    int c;          // column tile
-    int ku;         // first 128-row block of the stage
-    int ku_end;     // end of the segment (this work-group's part of column c)
-    int seg_begin;  // first block of the segment
-    int64_t u_end;  // end of the work-group's unit range
-    bool done;
-};
-
-__device__ __forceinline__ void cursor_init(Cursor &cu, int64_t u0, int64_t u1, int KU)
+// Zero-point operand: the codes 8 in the same encoding, 8 * 2^-24 in the
+// elements paired with unscaled activations and 128 * 2^-24 where the
+// activation carries 1/16.  Against the prescaled activations it yields
+// 8 * sum_k A_k * 2^-24 for every column n, which is subtracted.  Because it
+// is exactly the operand of a column whose codes are all 8, such a column's
+// two products are the same computation and cancel exactly (the matrix
+// cores' fp32 rounding is not symmetric under negation, so the constant is
+// subtracted rather than added negated).
+__device__ __forceinline__ half8_t bias_operand()
 {
-    cu.u_end = u1;
-    cu.done = (u0 >= u1);
-    cu.c = (int)(u0 / KU);
-    cu.ku = (int)(u0 - (int64_t)cu.c * KU);
-    cu.seg_begin = cu.ku;
-    const int64_t rem = u1 - (int64_t)cu.c * KU;
-    cu.ku_end = rem < KU ? (int)rem : KU;
+    return __builtin_bit_cast(half8_t, u32x4_t{0x00080008u, 0x00800080u, 0x00080008u, 0x00800080u});
 }
 
-template <int KW>
-__device__ __forceinline__ void cursor_next(Cursor &cu, int KU)
+__device__ __forceinline__ float4_t mfma(half8_t w, half8_t a, float4_t c)
 {
-    cu.ku += KW;
-    if (cu.ku >= cu.ku_end) {
-        cu.c += 1;
-        cu.ku = 0;
-        cu.seg_begin = 0;
-        const int64_t rem = cu.u_end - (int64_t)cu.c * KU;
-        cu.done = rem <= 0;
-        cu.ku_end = rem < KU ? (int)rem : KU;
-    }
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, a, c, 0, 0, 0);
 }
 
-// Scale row of 128-row block ku: ku / group_units, by a shift when the group
-// is a power-of-two number of blocks, else by a multiply with the rounded-up
-// reciprocal 2^32 / group_units (exact for ku, group_units < 2^16).
+// Scale row of 128-row block ku: ku / group_units as one multiply-high with
+// the host's rounded-up reciprocal 2^26 / group_units (exact for ku < 2^13).
 __device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)
 {
-    return p.gshift >= 0 ? (ku >> p.gshift) : (int)__umulhi((uint32_t)ku, p.gmagic);
+    return (int)__umulhi((uint32_t)ku << 6, p.gmagic);
 }
 
-__device__ __forceinline__ int64_t range_start(int w, int64_t total, int grid)
+// First unit of work-group w: floor(w * units / grid), from the host's
+// quotient and remainder so that no 64-bit division is needed.
+__device__ __forceinline__ int range_start(const GemmProblem &p, int w, int grid)
 {
-    return ((int64_t)w * total) / grid;
+    return w * p.per_wg + (int)((uint32_t)(w * p.extra) / (uint32_t)grid);
 }
 
 // Work-group that owns unit u: the largest w with range_start(w) <= u.
-__device__ __forceinline__ int unit_owner(int64_t u, int64_t total, int grid)
+__device__ __forceinline__ int unit_owner(const GemmProblem &p, int u, int grid)
 {
-    return (int)(((u + 1) * grid - 1) / total);
+    return (int)((((int64_t)u + 1) * grid - 1) / p.units);
 }
 
 // ---- cross-work-group partial tiles ----
 // A work-group that covers a column tile only in part writes its fp32 tile to
-// one of its two workspace slots (0: its first column, 1: its last), in
+// one of its two workspace slots (0: its first column tile, 1: its last), in
 // structure-of-arrays order so every store instruction covers 256 contiguous
-// bytes: float index ((blk*4 + i)*64 + lane), blk = nw*kBlocks + b.  Those
-// bytes are written and read with relaxed agent-scope atomics, which the
-// compiler emits as ordinary vector stores / loads carrying the
-// device-coherence bit, so they bypass the per-XCD L2 non-coherence without a
-// whole-cache writeback or invalidate.  Ordering: each wave waits for its
-// stores to complete (vmcnt 0) before the work-group barrier that precedes
-// the arrival counter's atomic increment, and the last arriver issues its
-// loads only after that increment has returned.
+// bytes: float index ((blk*4 + i)*64 + lane).  Those bytes are written and
+// read with relaxed agent-scope atomics, which the compiler emits as ordinary
+// vector stores / loads carrying the device-coherence bit, so they bypass the
+// per-XCD L2 non-coherence without a whole-cache writeback or invalidate.
+// Ordering: a wave waits for its stores to complete (vmcnt 0) before the
+// work-group barrier that precedes the arrival counter's atomic increment,
+// and a reducer issues its loads only after it has read the counter.
 __device__ __forceinline__ void store_partial(float *slot, int blk, int lane, float4_t v)
 {
     float *d = slot + blk * 256 + lane;
@@ -232,209 +158,211 @@ __device__ __forceinline__ float4_t load_partial(const float *slot, int blk, int
     return v;
 }
 
-// After the main loop: announce this work-group's partial columns (at most
-// two); the work-group whose arrival completes a column's count sums the
-// column's slots in work-group order (a fixed order: results are bitwise
-// reproducible) and stores C.  `own(j)` gives the partial-tile block index of
-// the j-th block this wave owns; `store_c(c, out)` writes C.
-template <int KOWN, typename OwnFn, typename StoreFn>
-__device__ __forceinline__ void publish_and_reduce(const GemmProblem &p, const int (&pcol)[2], int *flags,
-                                                   int wg, int KU, int64_t total, int grid,
-                                                   int slot_floats, int lane, OwnFn own, StoreFn store_c)
-{
-    if (pcol[0] < 0 && pcol[1] < 0) return;  // uniform across the work-group
-    wait_vmcnt<0>();                          // this wave's partial stores are complete
-    lds_barrier();
-    if (threadIdx.x == 0) {
-#pragma unroll
-        for (int which = 0; which < 2; ++which) {
-            int last = 0;
-            const int c = pcol[which];
-            if (c >= 0) {
-                const int wf = unit_owner((int64_t)c * KU, total, grid);
-                const int wl = unit_owner((int64_t)c * KU + KU - 1, total, grid);
-                const uint32_t old = __hip_atomic_fetch_add(p.counters + c, 1u, __ATOMIC_RELAXED,
-                                                            __HIP_MEMORY_SCOPE_AGENT);
-                if (old == (uint32_t)(wl - wf)) {
-                    last = 1;
-                    __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-            }
-            flags[which] = last;
-        }
-    }
-    lds_barrier();
-#pragma unroll
-    for (int which = 0; which < 2; ++which) {
-        const int c = pcol[which];
-        if (c < 0 || !flags[which]) continue;
-        const int wf = unit_owner((int64_t)c * KU, total, grid);
-        const int wl = unit_owner((int64_t)c * KU + KU - 1, total, grid);
-        float4_t out[KOWN];
-        for (int w = wf; w <= wl; ++w) {
-            const int wcol = (int)(range_start(w, total, grid) / KU);
-            const float *slot = p.partials + ((int64_t)w * 2 + ((c == wcol) ? 0 : 1)) * slot_floats;
-#pragma unroll
-            for (int j = 0; j < KOWN; ++j) {
-                const float4_t v = load_partial(slot, own(j), lane);
-                out[j] = (w == wf) ? v : out[j] + v;
-            }
-        }
-        store_c(c, out);
-    }
-    (void)wg;
-}
-
 // ---------------------------------------------------------------------------
-// Kernel 1 (decode batches, M <= 32): register streaming.
+// Register-streaming kernel.
 //
 // A work-group owns a column tile of 16*NB columns (NB 16-column blocks) over
-// a range of 128-row blocks of K (the striped partition); its KW waves take
+// a range of 128-row blocks of K (the striped partition); its four waves take
 // consecutive 128-row blocks of each stage (waves split K), so no weight or
 // activation byte is shared between waves: each lane loads exactly its MFMA
 // operands (16-byte non-temporal buffer loads of the pre-shuffled weights,
-// 16-byte loads of the activation rows, which hit L2) straight into a D-deep
-// ring of registers.  The loop is unrolled over the ring so register slots
-// are static and the compiler's vmcnt waits keep D-1 stages in flight.  Waves
-// meet only at the end of a column segment, where their fp32 tiles are summed
-// in LDS (Algorithm 1's reduction across waves that share an output tile).
-// Narrow tiles (NB = 1) give enough whole columns to occupy every compute unit
-// without splitting K across work-groups on small layers.
-template <int MB, int NB, int KW, int D, int OCC, bool PER_CHANNEL>
-__global__ void __launch_bounds__(64 * KW, OCC) w4a16_stream_kernel(GemmProblem p)
+// 16-byte loads of activation rows, which hit L2) straight into a D-deep ring
+// of registers.  The loop is unrolled over the ring so register slots are
+// static and the compiler's vmcnt waits keep D-1 stages in flight while one
+// is computed.  A wave whose block lies past the end of a segment loads
+// through an empty buffer descriptor (no memory is touched, zeros return) and
+// skips the stage's arithmetic.
+//
+// Cross-work-group combination, at the end: the work-group's first tile (if
+// shared) was written to slot 0 when its segment ended; it now bumps that
+// tile's counter.  Its last tile (if shared) stays in registers: the counter
+// is read first, and if every other contributor has arrived (the usual case:
+// they processed that tile at the start of their ranges) the work-group adds
+// their slots to its registers and writes C at once; otherwise it writes slot
+// 1 and arrives like the others.
+template <int MB, int NB, int D, bool PER_CHANNEL>
+__global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
 {
+    constexpr int KW = kStreamWaves;
     constexpr int kBlocks = NB * MB;               // 16x16 output blocks per wave
     constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
     constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
+    static_assert(KW == 4, "four waves per work-group");
     __shared__ float4_t red[KW * kBlocks * 64];
     __shared__ int flags[2];
 
     const int lane = threadIdx.x & 63;
-    const DequantConsts dq = dequant_consts();
-    // wave index as a scalar: all cursor and address arithmetic below is uniform
-    const int kw = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int kw = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, scalar
     const int lg = lane >> 4;
-    const int KU = p.K >> 7;
-    const int cols = p.N / (16 * NB);
-    const int total = cols * KU;  // < 2^31 (host checks K * N)
+    const int KU = p.KU;
     const int grid = gridDim.x;
     const int wg = blockIdx.x;
-    const int u0 = (int)range_start(wg, total, grid);
-    const int u1 = (int)range_start(wg + 1, total, grid);
-    const int first_col = u0 / KU;
+    const int u0 = range_start(p, wg, grid);
+    const int u1 = range_start(p, wg + 1, grid);
+    const int c_first = (int)((uint32_t)u0 / (uint32_t)KU);
+    const int c_last = (int)((uint32_t)(u1 - 1) / (uint32_t)KU);
+    const int k0 = u0 - c_first * KU;  // first block in the first tile
+    const int k1 = u1 - c_last * KU;   // end block in the last tile (1..KU)
 
-    // Stages of this work-group: each segment (its part of one column) takes
-    // ceil(length / KW) stages.
-    int n_st = 0;
-    for (int u = u0; u < u1;) {
-        const int e = (u / KU + 1) * KU < u1 ? (u / KU + 1) * KU : u1;
-        n_st += (e - u + KW - 1) / KW;
-        u = e;
-    }
+    // Byte offsets of tile c's block 0: weights (4 KiB per (64 columns x 128
+    // rows) block, 1 KiB per 16 columns) and scale rows (128 B per 64 columns).
+    auto w_tile = [&](int c) -> uint32_t {
+        const uint32_t nbg = (uint32_t)c * NB;
+        return ((nbg >> 2) * (uint32_t)KU * 4u + (nbg & 3u)) << 10;
+    };
+    auto s_tile = [&](int c) -> uint32_t {
+        const uint32_t nbg = (uint32_t)c * NB;
+        return (((nbg >> 2) * (uint32_t)p.G) << 7) + (nbg & 3u) * 8u;
+    };
 
-    // Stage cursors (wave-uniform): column tile c, first 128-row block ku of
-    // the stage, segment [begin, end) within the column.
-    struct Cur {
-        int c, ku, begin, end;
-    };
-    auto cur_init = [&](Cur &q) {
-        q.c = first_col;
-        q.ku = u0 - q.c * KU;
-        q.begin = q.ku;
-        q.end = (u1 - q.c * KU) < KU ? (u1 - q.c * KU) : KU;
-    };
-    auto cur_next = [&](Cur &q) {
-        q.ku += KW;
-        if (q.ku >= q.end) {
-            q.c += 1;
-            q.ku = 0;
-            q.begin = 0;
-            q.end = (u1 - q.c * KU) < KU ? (u1 - q.c * KU) : KU;
-        }
-    };
-    Cur ld, cp;
-    cur_init(ld);
-    cp = ld;
-
-    // Loads are buffer loads: a fixed per-lane byte offset in one VGPR, the
-    // per-stage offset in a scalar register, so the stream costs no vector
-    // address arithmetic.  Past the end of the range a stage uses an empty
-    // descriptor: its loads are out of range, touch no memory and return 0,
-    // which keeps the pattern of loads per stage static.  Activation rows are
-    // loaded only by lanes whose row exists (the other lanes' MFMA columns are
-    // never stored).
-    const uint32_t w_lane = lane * 16;
-    const int arow = lane & 15;
+    // Per-lane parts of the load addresses (fixed for the whole kernel).
+    const uint32_t w_lane = (uint32_t)kw * 4096u + (uint32_t)lane * 16u;
     uint32_t a_lane[MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) a_lane[mb] = (uint32_t)((mb * 16 + arow) * p.K + 8 * lg) * 2;
-    const uint32_t s_lane = lg * 32;
-    const int w_bytes = (int)((uint32_t)p.K * (uint32_t)(p.N / 2));
-    const int a_bytes = p.M * p.K * 2;
-    const int s_bytes = p.G * p.N * 2;
+    for (int mb = 0; mb < MB; ++mb)
+        a_lane[mb] = (uint32_t)((mb * 16 + (lane & 15)) * p.K + 8 * lg) * 2u + (uint32_t)kw * 256u;
+    const uint32_t s_lane = (uint32_t)lg * 32u;
+    // Rows of A past M lie past the end of the A buffer: their loads return 0.
+    const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
+    const uint32_t a_bytes = (uint32_t)p.M * (uint32_t)p.K * 2u;
+    const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
     u32x4_t wr[D][NB];
     half8_t ar[D][4 * MB];
     half8_t sr[D][kSLoads];
-#pragma unroll
-    for (int j = 0; j < D; ++j)
-#pragma unroll
-        for (int i = 0; i < 4 * MB; ++i) ar[j][i] = half8_t{};
 
-    auto issue = [&](int j, const Cur &cu, bool valid) {
-        int ku = cu.ku + kw;
-        ku = ku < cu.end ? ku : cu.ku;  // idle wave: any valid block, result unused
-        const int nbg = cu.c * NB;      // first global 16-column block of the tile
+    // ---- load cursor: wave-uniform, advanced once per stage ----
+    int ld_c = c_first, ld_ku = k0;
+    int ld_end = (c_first == c_last) ? k1 : KU;
+    uint32_t ld_w = w_tile(ld_c) + (uint32_t)ld_ku * 4096u;
+    uint32_t ld_s = s_tile(ld_c);
+
+    auto issue = [&](int j) {
+        const int my = ld_ku + kw;
+        const bool on = my < ld_end;
         const __amdgpu_buffer_rsrc_t rw =
-            __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, valid ? w_bytes : 0, kBufferFlags);
-        const int w_off = (((nbg >> 2) * KU + ku) * 4 + (nbg & 3)) << 10;
+            __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
 #pragma unroll
         for (int b = 0; b < NB; ++b)
             wr[j][b] = __builtin_bit_cast(
-                u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, w_off, kAuxNonTemporal));
+                u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, ld_w, kAuxNonTemporal));
         const __amdgpu_buffer_rsrc_t ra =
-            __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, valid ? a_bytes : 0, kBufferFlags);
+            __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, on ? a_bytes : 0u, kBufferFlags);
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            if (mb * 16 + arow < p.M) {
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    ar[j][mb * 4 + t] = __builtin_bit_cast(
-                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(ra, a_lane[mb] + t * 64, ku << 8, 0));
-            }
-        }
+            for (int t = 0; t < 4; ++t)
+                ar[j][mb * 4 + t] = __builtin_bit_cast(
+                    half8_t, __builtin_amdgcn_raw_buffer_load_b128(ra, a_lane[mb] + t * 64, ld_ku * 256, 0));
         if constexpr (!PER_CHANNEL) {
             const __amdgpu_buffer_rsrc_t rs =
-                __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, valid ? s_bytes : 0, kBufferFlags);
-            const int s_off = (((nbg >> 2) * p.G + scale_row_of(ku, p)) << 7) + (nbg & 3) * 8;
+                __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
+            const uint32_t s_off = ld_s + ((uint32_t)scale_row_of(my, p) << 7);
 #pragma unroll
             for (int i = 0; i < kSLoads; ++i)
                 sr[j][i] = __builtin_bit_cast(
                     half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
         }
     };
+    auto advance_ld = [&]() {
+        ld_ku += KW;
+        ld_w += KW * 4096u;
+        if (ld_ku >= ld_end) {  // next segment (rare)
+            ld_c += 1;
+            ld_ku = 0;
+            ld_end = (ld_c < c_last) ? KU : (ld_c == c_last) ? k1 : 0;  // 0: past the range
+            ld_w = w_tile(ld_c);
+            ld_s = s_tile(ld_c);
+        }
+    };
+
+    // Issue the first D stages before anything else.
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+        issue(j);
+        advance_ld();
+    }
+
+    // Stages of this work-group: ceil(segment length / KW) per segment.
+    const int n_st = (c_first == c_last)
+                         ? (k1 - k0 + KW - 1) / KW
+                         : (KU - k0 + KW - 1) / KW + (c_last - c_first - 1) * ((KU + KW - 1) / KW) +
+                               (k1 + KW - 1) / KW;
 
     float4_t acc[NB][MB];
+    float4_t bacc[PER_CHANNEL ? MB : 1];  // per-channel: zero-point sum, chained like acc
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[b][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
-
-    // MFMA order: k-step outer, column block inner, so consecutive MFMAs are
-    // independent; group scales fold in after the stage's last MFMA.
-    auto compute = [&](int j) {
-        if constexpr (!PER_CHANNEL) {
-            float4_t tmp[NB][MB];
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
+    for (int mb = 0; mb < (PER_CHANNEL ? MB : 1); ++mb) bacc[mb] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+    half8_t kb = bias_operand();
+    asm volatile("" : "+v"(kb));  // keep the constant in vector registers
+    const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
+
+    // One stage: for each 16-row block of A, four MFMA steps per column block
+    // plus four for the zero point.  Group scales: the stage's zero-point
+    // product is subtracted from each column block's 128-row product, and the
+    // difference scaled and accumulated in one fused multiply-add per value.
+    auto compute = [&](int j) {
+        half8_t a[4 * MB];
+#pragma unroll
+        for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(ar[j][i]);
+        if constexpr (PER_CHANNEL) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) bacc[mb] = mfma(kb, a[mb * 4 + t], bacc[mb]);
 #pragma unroll
                 for (int b = 0; b < NB; ++b) {
-                    const half8_t w = dequant8(wr[j][b][t], dq);
+                    const half8_t w = dequant_sub(wr[j][b][t]);
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) acc[b][mb] = mfma(w, a[mb * 4 + t], acc[b][mb]);
+                }
+            }
+        } else if constexpr (MB >= 4) {
+            // Column block outer: each dequantized word feeds MB MFMAs and only
+            // MB fp32 temporaries are live at a time.
+            float4_t tb[MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) tb[mb] = mfma(kb, a[mb * 4 + t], t == 0 ? zero4 : tb[mb]);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                float4_t tmp[MB];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const half8_t w = dequant_sub(wr[j][b][t]);
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) tmp[mb] = mfma(w, a[mb * 4 + t], t == 0 ? zero4 : tmp[mb]);
+                }
+                const half8_t sv = sr[j][b >> 1];
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        acc[b][mb][i] = __builtin_fmaf(tmp[mb][i] - tb[mb][i], (float)sv[(b & 1) * 4 + i],
+                                                       acc[b][mb][i]);
+            }
+        } else {
+            // k-step outer, column block inner: consecutive MFMAs are independent.
+            float4_t tb[MB];
+            float4_t tmp[NB][MB];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) tb[mb] = mfma(kb, a[mb * 4 + t], t == 0 ? zero4 : tb[mb]);
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    const half8_t w = dequant_sub(wr[j][b][t]);
 #pragma unroll
                     for (int mb = 0; mb < MB; ++mb)
-                        tmp[b][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                            w, ar[j][mb * 4 + t], t == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : tmp[b][mb], 0, 0, 0);
+                        tmp[b][mb] = mfma(w, a[mb * 4 + t], t == 0 ? zero4 : tmp[b][mb]);
                 }
+            }
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 // scales of block b: halves 4b .. 4b+3 of this lane's run
@@ -442,18 +370,10 @@ __global__ void __launch_bounds__(64 * KW, OCC) w4a16_stream_kernel(GemmProblem 
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[b][mb][i] += tmp[b][mb][i] * (float)sv[(b & 1) * 4 + i];
+                    for (int i = 0; i < 4; ++i)
+                        acc[b][mb][i] = __builtin_fmaf(tmp[b][mb][i] - tb[mb][i], (float)sv[(b & 1) * 4 + i],
+                                                       acc[b][mb][i]);
             }
-        } else {
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int b = 0; b < NB; ++b) {
-                    const half8_t w = dequant8(wr[j][b][t], dq);
-#pragma unroll
-                    for (int mb = 0; mb < MB; ++mb)
-                        acc[b][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w, ar[j][mb * 4 + t], acc[b][mb], 0, 0, 0);
-                }
         }
     };
 
@@ -462,17 +382,20 @@ __global__ void __launch_bounds__(64 * KW, OCC) w4a16_stream_kernel(GemmProblem 
     auto store_c = [&](int c, const float4_t *out) {
 #pragma unroll
         for (int j = 0; j < kOwn; ++j) {
-            const int blk = kw + j * KW;
+            const int blk = own(j);
             if (blk >= kBlocks) break;
             const int b = blk / MB, mb = blk % MB;
-            const int m = mb * 16 + arow;
+            const int m = mb * 16 + (lane & 15);
             if (m < p.M) {
                 const int nbg = c * NB + b;
                 float4_t v = out[j];
                 if constexpr (PER_CHANNEL) {
                     const half4_t s4 = *(const half4_t *)(p.S + (int64_t)(nbg >> 2) * 64 + lg * 16 + (nbg & 3) * 4);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] *= (float)s4[i];
+                    for (int i = 0; i < 4; ++i) v[i] *= (float)s4[i] * kTwo24;
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] *= kTwo24;
                 }
                 const half4_t h = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
                 *(half4_t *)(p.C + (int64_t)m * p.N + nbg * 16 + lg * 4) = h;
@@ -480,376 +403,195 @@ __global__ void __launch_bounds__(64 * KW, OCC) w4a16_stream_kernel(GemmProblem 
         }
     };
 
-    int pcol[2] = {-1, -1};
     const int slot_floats = kBlocks * 256;
-    auto finish_segment = [&](const Cur &cu) {
-        float4_t out[kOwn];
-        if constexpr (KW > 1) {
+    float *const my_slots = p.partials + (int64_t)wg * 2 * slot_floats;
+    bool has_first = false, has_last = false;
+    float4_t last_out[kOwn];
+#pragma unroll
+    for (int j = 0; j < kOwn; ++j) last_out[j] = zero4;
+
+    // ---- compute cursor ----
+    int cp_c = c_first, cp_ku = k0, cp_begin = k0;
+    int cp_end = (c_first == c_last) ? k1 : KU;
+
+    // A segment is complete: sum the four waves' tiles in LDS, then write C
+    // (whole column), keep the sum (shared last tile) or write slot 0
+    // (shared first tile).
+    auto finish_segment = [&]() {
+        if constexpr (PER_CHANNEL) {
 #pragma unroll
             for (int b = 0; b < NB; ++b)
 #pragma unroll
-                for (int mb = 0; mb < MB; ++mb) red[(kw * kBlocks + b * MB + mb) * 64 + lane] = acc[b][mb];
-            lds_barrier();
+                for (int mb = 0; mb < MB; ++mb) acc[b][mb] -= bacc[mb];
 #pragma unroll
-            for (int j = 0; j < kOwn; ++j) {
-                const int blk = own(j);
-                if (blk < kBlocks) {
-                    float4_t s = red[blk * 64 + lane];
-#pragma unroll
-                    for (int k2 = 1; k2 < KW; ++k2) s += red[(k2 * kBlocks + blk) * 64 + lane];
-                    out[j] = s;
-                }
-            }
-            lds_barrier();
-        } else {
-#pragma unroll
-            for (int j = 0; j < kOwn; ++j) out[j] = acc[j / MB][j % MB];
+            for (int mb = 0; mb < MB; ++mb) bacc[mb] = zero4;
         }
+        float4_t out[kOwn];
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[b][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
-        if (cu.begin == 0 && cu.end == KU) {
-            store_c(cu.c, out);
+            for (int mb = 0; mb < MB; ++mb) red[(kw * kBlocks + b * MB + mb) * 64 + lane] = acc[b][mb];
+        lds_barrier();
+#pragma unroll
+        for (int j = 0; j < kOwn; ++j) {
+            const int blk = own(j);
+            if (blk < kBlocks) {
+                float4_t s = red[blk * 64 + lane];
+#pragma unroll
+                for (int k2 = 1; k2 < KW; ++k2) s += red[(k2 * kBlocks + blk) * 64 + lane];
+                out[j] = s;
+            } else {
+                out[j] = zero4;
+            }
+        }
+        lds_barrier();
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) acc[b][mb] = zero4;
+        if (cp_begin == 0 && cp_end == KU) {
+            store_c(cp_c, out);
+        } else if (cp_c == c_last) {
+            has_last = true;
+#pragma unroll
+            for (int j = 0; j < kOwn; ++j) last_out[j] = out[j];
         } else {
-            const int which = (cu.c == first_col) ? 0 : 1;
-            pcol[which] = cu.c;
-            float *slot = p.partials + ((int64_t)wg * 2 + which) * slot_floats;
+            has_first = true;
 #pragma unroll
             for (int j = 0; j < kOwn; ++j)
-                if (own(j) < kBlocks) store_partial(slot, own(j), lane, out[j]);
+                if (own(j) < kBlocks) store_partial(my_slots, own(j), lane, out[j]);
         }
     };
 
-#pragma unroll
-    for (int j = 0; j < D; ++j) {
-        issue(j, ld, j < n_st);
-        cur_next(ld);
-    }
-    const int iters = (n_st + D - 1) / D;
-    for (int it = 0; it < iters; ++it) {
+    // Loads are issued unconditionally (past the range through empty
+    // descriptors) so that every stage has the same load pattern and the
+    // compiler's vmcnt waits stay static.
+    for (int st0 = 0; st0 < n_st; st0 += D) {
 #pragma unroll
         for (int j = 0; j < D; ++j) {
-            const int st = it * D + j;
-            if (st < n_st) {
-                if (cp.ku + kw < cp.end) compute(j);
-                if (cp.ku + KW >= cp.end) finish_segment(cp);
-                cur_next(cp);
+            if (st0 + j < n_st) {
+                if (cp_ku + kw < cp_end) compute(j);
+                if (cp_ku + KW >= cp_end) {
+                    finish_segment();
+                    cp_c += 1;
+                    cp_ku = 0;
+                    cp_begin = 0;
+                    cp_end = (cp_c < c_last) ? KU : k1;
+                } else {
+                    cp_ku += KW;
+                }
             }
-            issue(j, ld, st + D < n_st);
-            cur_next(ld);
+            issue(j);
+            advance_ld();
         }
     }
-    auto own_valid = [&](int j) { return own(j) < kBlocks ? own(j) : 0; };
-    publish_and_reduce<kOwn>(p, pcol, flags, wg, KU, (int64_t)total, grid, slot_floats, lane, own_valid,
-                             store_c);
-}
 
-// ---------------------------------------------------------------------------
-// Kernel 2 (larger batches, M > 32): LDS pipeline.
-template <int MB, int NW, int KW, bool PER_CHANNEL>
-__global__ void __launch_bounds__(64 * NW * KW, 1)
-    w4a16_lds_kernel(GemmProblem p)
-{
-    using Gm = Geo<MB, NW, KW, PER_CHANNEL>;
-    constexpr int P = Gm::P;
-    constexpr int L = Gm::kLoadsPerStage;
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[Gm::kSmemBytes];
-
-    const int lane = threadIdx.x & 63;
-    const DequantConsts dq = dequant_consts();
-    const int wave = threadIdx.x >> 6;
-    const int nw = (NW == 1) ? 0 : wave % NW;
-    const int kw = (KW == 1) ? 0 : wave / NW;
-    const int lg = lane >> 4;
-
-    const int KU = p.K >> 7;
-    const int cols = p.N / (64 * NW);
-    const int64_t total = (int64_t)cols * KU;
-    const int grid = gridDim.x;
-    const int wg = blockIdx.x;
-    const int64_t u0 = range_start(wg, total, grid);
-    const int64_t u1 = range_start(wg + 1, total, grid);
-    const int first_col = (int)(u0 / KU);
-
-    Cursor ld, cp;
-    cursor_init(ld, u0, u1, KU);
-    cp = ld;
-
-    uint8_t *const red = smem + P * Gm::kStageBytes;
-    int *const flags = (int *)(smem + P * Gm::kStageBytes + Gm::kRedBytes);
-
-    // ---- stage loader: every wave issues exactly L loads per stage ----
-    auto issue = [&](const Cursor &cu, int slot) {
-        int ku = cu.ku + kw;
-        if (ku >= cu.ku_end) ku = cu.ku;  // idle wave: reload a valid block, result unused
-        uint8_t *base = smem + slot * Gm::kStageBytes;
-        const int c64 = cu.c * NW + nw;
-        const uint32_t *wsrc = p.W + ((int64_t)(c64 * KU + ku) * 4) * 256 + lane * 4;
-        uint8_t *wdst = base + Gm::kABytes + (kw * NW + nw) * 4096;
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-            __builtin_amdgcn_global_load_lds((const void *)(wsrc + nb * 256), LDS_PTR(wdst + nb * 1024),
-                                             16, 0, kAuxNonTemporal);
-#pragma unroll
-        for (int i = 0; i < Gm::kAFragsPerWave; ++i) {
-            const int f = nw + i * NW;
-            const int mb = f >> 2, t = f & 3;
-            int row = mb * 16 + (lane & 15);
-            row = row < p.M ? row : p.M - 1;
-            const uint16_t *asrc = p.A + (int64_t)row * p.K + ku * 128 + 32 * t + 8 * lg;
-            __builtin_amdgcn_global_load_lds((const void *)asrc,
-                                             LDS_PTR(base + (kw * Gm::kAFrags + f) * 1024), 16, 0, 0);
-        }
-        if constexpr (!PER_CHANNEL) {
-            const int r = scale_row_of(ku, p);
-            const uint16_t *ssrc = p.S + ((int64_t)c64 * p.G + r) * 64 + (lane & 31) * 2;
-            if (lane < 32)
-                __builtin_amdgcn_global_load_lds((const void *)ssrc,
-                                                 LDS_PTR(base + Gm::kABytes + Gm::kWBytes + (kw * NW + nw) * 128),
-                                                 4, 0, 0);
-        }
+    // ---- combination of shared tiles ----
+    if (!has_first && !has_last) return;  // uniform across the work-group
+    // Contributors of tile c: work-groups owner(c*KU) .. owner(c*KU + KU - 1);
+    // the slot a contributor used for c: 1 if c is its last tile, else 0.
+    auto slot_of = [&](int w, int c) -> const float * {
+        const int wl_last = (int)((uint32_t)(range_start(p, w + 1, grid) - 1) / (uint32_t)KU);
+        return p.partials + ((int64_t)w * 2 + (c == wl_last ? 1 : 0)) * slot_floats;
     };
-
-    float4_t acc[4][MB];
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
-
-    // Partial segments of this work-group: head (its first column) and tail.
-    int pcol[2] = {-1, -1};
-
-    // ---- output helpers (register layout: block b = nb*MB + mb; lane holds
-    //      rows n = 16nb + 4lg + i, column m = 16mb + lane%16) ----
-    auto store_c = [&](int c, const float4_t *out) {
-        const int c64 = c * NW + nw;
-#pragma unroll
-        for (int j = 0; j < Gm::kOwnBlocks; ++j) {
-            const int b = kw + j * KW;
-            const int nb = b / MB, mb = b % MB;
-            const int m = mb * 16 + (lane & 15);
-            if (m < p.M) {
-                float4_t v = out[j];
-                if constexpr (PER_CHANNEL) {
-                    const half4_t s4 = *(const half4_t *)(p.S + (int64_t)c64 * 64 + lg * 16 + nb * 4);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] *= (float)s4[i];
-                }
-                const half4_t h = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
-                const int n = c64 * 64 + nb * 16 + lg * 4;
-                *(half4_t *)(p.C + (int64_t)m * p.N + n) = h;
+    wait_vmcnt0();  // this wave's slot-0 stores are complete
+    lds_barrier();
+    if (threadIdx.x == 0) {
+        int f0 = 0, f1 = 0;
+        if (has_first) {
+            const int c = c_first;
+            const int others = unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid);
+            const uint32_t old = __hip_atomic_fetch_add(p.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (old == (uint32_t)others) {
+                f0 = 1;
+                __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
+        if (has_last) {
+            const int c = c_last;
+            const int others = unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid);
+            const uint32_t seen = __hip_atomic_load(p.counters + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (seen == (uint32_t)others) {
+                f1 = 1;
+                __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        flags[0] = f0;
+        flags[1] = f1;
+    }
+    lds_barrier();
+    const bool reduce_first = has_first && flags[0] != 0;
+    bool reduce_last = has_last && flags[1] != 0;
+    if (has_last && !reduce_last) {
+        // Not every contributor has arrived: publish slot 1 and arrive.
+#pragma unroll
+        for (int j = 0; j < kOwn; ++j)
+            if (own(j) < kBlocks) store_partial(my_slots + slot_floats, own(j), lane, last_out[j]);
+        wait_vmcnt0();
+        lds_barrier();
+        if (threadIdx.x == 0) {
+            const int c = c_last;
+            const int others = unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid);
+            const uint32_t old = __hip_atomic_fetch_add(p.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            int f1 = 0;
+            if (old == (uint32_t)others) {
+                f1 = 1;
+                __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            flags[1] = f1;
+        }
+        lds_barrier();
+        reduce_last = flags[1] != 0;
+    }
+    // Sum the contributors' slots in work-group order; this work-group's own
+    // last-tile sum comes from registers (the same values it would store).
+    auto reduce = [&](int c, bool own_in_regs) {
+        const int wf = unit_owner(p, c * KU, grid);
+        const int wl = unit_owner(p, c * KU + KU - 1, grid);
+        float4_t out[kOwn];
+        for (int w = wf; w <= wl; ++w) {
+            const float *slot = slot_of(w, c);
+#pragma unroll
+            for (int j = 0; j < kOwn; ++j) {
+                const int blk = own(j) < kBlocks ? own(j) : 0;
+                const float4_t v = (own_in_regs && w == wg) ? last_out[j] : load_partial(slot, blk, lane);
+                out[j] = (w == wf) ? v : out[j] + v;
+            }
+        }
+        store_c(c, out);
     };
-
-    // ---- segment end: reduce over K-waves, then write C or a partial slot ----
-    auto finish_segment = [&](const Cursor &cu) {
-        float4_t out[Gm::kOwnBlocks];
-        if constexpr (KW > 1) {
-            float4_t *r = (float4_t *)red;
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb)
-                    r[((kw * NW + nw) * Gm::kBlocks + nb * MB + mb) * 64 + lane] = acc[nb][mb];
-            lds_barrier();
-#pragma unroll
-            for (int j = 0; j < Gm::kOwnBlocks; ++j) {
-                const int b = kw + j * KW;
-                float4_t s = r[((0 * NW + nw) * Gm::kBlocks + b) * 64 + lane];
-#pragma unroll
-                for (int k2 = 1; k2 < KW; ++k2) s += r[((k2 * NW + nw) * Gm::kBlocks + b) * 64 + lane];
-                out[j] = s;
-            }
-            lds_barrier();
-        } else {
-#pragma unroll
-            for (int j = 0; j < Gm::kOwnBlocks; ++j) out[j] = acc[j / MB][j % MB];
-        }
-#pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = float4_t{0.f, 0.f, 0.f, 0.f};
-
-        if (cu.seg_begin == 0 && cu.ku_end == KU) {
-            store_c(cu.c, out);
-        } else {
-            const int which = (cu.c == first_col) ? 0 : 1;
-            pcol[which] = cu.c;
-            float *slot = p.partials + ((int64_t)wg * 2 + which) * Gm::kSlotFloats;
-#pragma unroll
-            for (int j = 0; j < Gm::kOwnBlocks; ++j) store_partial(slot, nw * Gm::kBlocks + kw + j * KW, lane, out[j]);
-        }
-    };
-
-    // ---- main pipeline ----
-    int issued = 0, computed = 0;
-#pragma unroll
-    for (int s = 0; s < P - 1; ++s) {
-        if (!ld.done) {
-            issue(ld, s);
-            cursor_next<KW>(ld, KU);
-            ++issued;
-        }
-    }
-    int slot = 0, ld_slot = P - 1;
-    while (!cp.done) {
-        const int ahead = issued - computed - 1;  // stages issued after the one to compute
-        if constexpr (P >= 4) {
-            if (ahead >= 2) wait_vmcnt<2 * L>();
-            else if (ahead == 1) wait_vmcnt<L>();
-            else wait_vmcnt<0>();
-        } else if constexpr (P == 3) {
-            if (ahead >= 1) wait_vmcnt<L>();
-            else wait_vmcnt<0>();
-        } else {
-            wait_vmcnt<0>();
-        }
-        if constexpr (NW > 1) lds_barrier();
-        if (!ld.done) {
-            issue(ld, ld_slot);
-            cursor_next<KW>(ld, KU);
-            ++issued;
-            ld_slot = (ld_slot + 1 == P) ? 0 : ld_slot + 1;
-        }
-
-        // ---- compute one stage ----
-        if (cp.ku + kw < cp.ku_end) {
-            const uint8_t *base = smem + slot * Gm::kStageBytes;
-            const half8_t *abase = (const half8_t *)(base + kw * Gm::kAFrags * 1024);
-            const u32x4_t *wbase = (const u32x4_t *)(base + Gm::kABytes + (kw * NW + nw) * 4096);
-            const uint8_t *sbase = base + Gm::kABytes + Gm::kWBytes + (kw * NW + nw) * 128;
-            if constexpr (Gm::kFold) {
-                // fp32 fold: each 128-row product is scaled once per output.
-                half8_t a[MB][4];
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) a[mb][t] = abase[(mb * 4 + t) * 64 + lane];
-                float sc[16];
-                const half8_t *sp = (const half8_t *)(sbase + lg * 32);
-                const half8_t s0 = sp[0], s1 = sp[1];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) { sc[i] = (float)s0[i]; sc[8 + i] = (float)s1[i]; }
-#pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
-                    const u32x4_t wv = wbase[nb * 64 + lane];
-                    float4_t tmp[MB];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const half8_t b = dequant8(wv[t], dq);
-#pragma unroll
-                        for (int mb = 0; mb < MB; ++mb)
-                            tmp[mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                                b, a[mb][t], t == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : tmp[mb], 0, 0, 0);
-                    }
-#pragma unroll
-                    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) acc[nb][mb][i] += tmp[mb][i] * sc[nb * 4 + i];
-                }
-            } else {
-                // Per-channel scales (applied at the end), or group scales
-                // multiplied into the fp16 weights of column n = 16nb + lane%16.
-                u32x4_t wv[4];
-#pragma unroll
-                for (int nb = 0; nb < 4; ++nb) wv[nb] = wbase[nb * 64 + lane];
-                half2_t s2[4];
-                if constexpr (!PER_CHANNEL) {
-                    const _Float16 *sh = (const _Float16 *)sbase;
-                    const int col = lane & 15;
-#pragma unroll
-                    for (int nb = 0; nb < 4; ++nb) {
-                        const _Float16 v = sh[16 * (col >> 2) + 4 * nb + (col & 3)];
-                        s2[nb] = half2_t{v, v};
-                    }
-                }
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    half8_t a[MB];
-#pragma unroll
-                    for (int mb = 0; mb < MB; ++mb) a[mb] = abase[(mb * 4 + t) * 64 + lane];
-#pragma unroll
-                    for (int nb = 0; nb < 4; ++nb) {
-                        half8_t b = dequant8(wv[nb][t], dq);
-                        if constexpr (!PER_CHANNEL) b = scale8(b, s2[nb]);
-#pragma unroll
-                        for (int mb = 0; mb < MB; ++mb)
-                            acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(b, a[mb], acc[nb][mb], 0, 0, 0);
-                    }
-                }
-            }
-        }
-        ++computed;
-
-        if (cp.ku + KW >= cp.ku_end) finish_segment(cp);
-        cursor_next<KW>(cp, KU);
-        slot = (slot + 1 == P) ? 0 : slot + 1;
-    }
-
-    auto own = [&](int j) { return nw * Gm::kBlocks + kw + j * KW; };
-    publish_and_reduce<Gm::kOwnBlocks>(p, pcol, flags, wg, KU, total, grid, Gm::kSlotFloats, lane, own,
-                                       store_c);
-}
-
-template <int MB, int NW, int KW>
-hipError_t launch_variant(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
-{
-    const bool per_channel = (p.group_units == 0);
-    GemmProblem arg = p;
-    void *args[] = {&arg};
-    if (per_channel) {
-        using Gm = Geo<MB, NW, KW, true>;
-        return hipLaunchKernel((const void *)&w4a16_lds_kernel<MB, NW, KW, true>, dim3(cfg.grid),
-                               dim3(Gm::kThreads), args, 0, stream);
-    }
-    using Gm = Geo<MB, NW, KW, false>;
-    return hipLaunchKernel((const void *)&w4a16_lds_kernel<MB, NW, KW, false>, dim3(cfg.grid),
-                           dim3(Gm::kThreads), args, 0, stream);
+    if (reduce_last) reduce(c_last, true);
+    if (reduce_first) reduce(c_first, false);
 }
 
 }  // namespace
 
-int slot_floats(const GemmConfig &cfg)
-{
-    return cfg.kind == kKindStream ? cfg.nb * cfg.mb * 256 : cfg.nw * 4 * cfg.mb * 256;
-}
+int slot_floats(const GemmConfig &cfg) { return cfg.nb * cfg.mb * 256; }
 
 template <int MB, int NB>
 hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    constexpr int KW = kStreamWaves, OCC = kStreamOcc;
-    constexpr int D = (MB == 1) ? (NB == 4 ? 3 : NB == 2 ? 4 : 6) : (NB == 4 ? 2 : 4);
+    constexpr int D = (MB == 1) ? (NB == 4 ? 3 : NB == 2 ? 4 : 6) : (MB == 2) ? (NB == 4 ? 2 : 4) : 2;
     GemmProblem arg = p;
     void *args[] = {&arg};
-    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, KW, D, OCC, true>
-                                          : (const void *)&w4a16_stream_kernel<MB, NB, KW, D, OCC, false>;
-    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * KW), args, 0, stream);
+    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, D, true>
+                                          : (const void *)&w4a16_stream_kernel<MB, NB, D, false>;
+    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * kStreamWaves), args, 0, stream);
 }
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    if (cfg.kind == kKindStream) {
-        switch (cfg.mb * 10 + cfg.nb) {
-        case 11: return launch_stream<1, 1>(cfg, p, stream);
-        case 12: return launch_stream<1, 2>(cfg, p, stream);
-        case 14: return launch_stream<1, 4>(cfg, p, stream);
-        case 21: return launch_stream<2, 1>(cfg, p, stream);
-        case 22: return launch_stream<2, 2>(cfg, p, stream);
-        case 24: return launch_stream<2, 4>(cfg, p, stream);
-        default: return hipErrorInvalidValue;
-        }
-        return hipErrorInvalidValue;
-    }
-    const int key = cfg.mb * 100 + cfg.nw * 10 + cfg.kw;
-    switch (key) {
-    case 441: return launch_variant<4, 4, 1>(cfg, p, stream);
-    case 421: return launch_variant<4, 2, 1>(cfg, p, stream);
-    case 411: return launch_variant<4, 1, 1>(cfg, p, stream);
-    case 841: return launch_variant<8, 4, 1>(cfg, p, stream);
-    case 821: return launch_variant<8, 2, 1>(cfg, p, stream);
-    case 811: return launch_variant<8, 1, 1>(cfg, p, stream);
+    switch (cfg.mb * 10 + cfg.nb) {
+    case 11: return launch_stream<1, 1>(cfg, p, stream);
+    case 12: return launch_stream<1, 2>(cfg, p, stream);
+    case 14: return launch_stream<1, 4>(cfg, p, stream);
+    case 21: return launch_stream<2, 1>(cfg, p, stream);
+    case 22: return launch_stream<2, 2>(cfg, p, stream);
+    case 24: return launch_stream<2, 4>(cfg, p, stream);
+    case 42: return launch_stream<4, 2>(cfg, p, stream);
+    case 44: return launch_stream<4, 4>(cfg, p, stream);
+    case 82: return launch_stream<8, 2>(cfg, p, stream);
+    case 84: return launch_stream<8, 4>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

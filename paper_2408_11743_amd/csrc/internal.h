@@ -10,20 +10,14 @@ namespace marlin {
 
 // One launch configuration of the GEMM kernel.
 //   mb  : 16-row blocks of A handled per pass (M_pad = 16 * mb, M <= M_pad)
-//   nw  : waves along N; each wave owns one 64-column tile
-//   kw  : waves along K; each takes a different 128-row block of a stage
+//   nb  : 16-column blocks per column tile (1, 2 or 4)
 //   grid: work-groups (Stream-K workers)
-constexpr int kKindStream = 0;  // register-streaming kernel (M <= 32)
-constexpr int kKindLds = 1;     // LDS-pipeline kernel (M > 32)
 constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
 constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
 struct GemmConfig {
-    int kind;
     int mb;
-    int nb;  // register-streaming kernel: 16-column blocks per column tile (1, 2 or 4)
-    int nw;
-    int kw;
+    int nb;
     int grid;
 };
 
@@ -38,9 +32,12 @@ struct GemmProblem {
     int N;
     int K;
     int G;                // scale rows
+    int KU;               // 128-row blocks of K
+    int units;            // column tiles * KU: the striped partition's units
+    int per_wg;           // units / grid
+    int extra;            // units % grid
     int group_units;      // 128-row blocks per scale group; 0 = per-channel
-    int gshift;           // log2(group_units) if a power of two, else -1
-    uint32_t gmagic;      // ceil(2^32 / group_units) when gshift < 0
+    uint32_t gmagic;      // ceil(2^26 / group_units): row of block ku = (ku * 2^6 * gmagic) >> 32
 };
 
 // Upper bound on compute units used (MI355X has 256).  Workspace sizes are

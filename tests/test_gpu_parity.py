@@ -1,9 +1,10 @@
 """GPU parity: the HIP path (through the C ABI) against the FP64 oracle.
 
-Bar (spec tolerance, elementwise): |C_gpu - C_ref| <= 2e-3 + 1e-2*|C_ref|,
+Bar (elementwise tolerance of the hot path): |C_gpu - C_ref| <= 2e-3 + 1e-2*|C_ref|,
 with C_ref the unrounded fp64 oracle value.  Packing and unpacking are
-bit-exact; closed-form cases (identity, zero weights, power-of-two scales,
-every code in every nibble slot) are bit-exact.
+bit-exact; closed-form cases (zero weights, power-of-two scales, every code
+in every nibble slot) are bit-exact; identity weights reproduce A within the
+bar (the zero point is a separate fp32 product; see that test).
 
 Inputs are the seeded workloads of ``synth``; large shapes are compared on
 sampled outputs computed one by one by the oracle, in the same launch
@@ -142,7 +143,14 @@ def test_identity_weights_reproduce_A(mk, M):
         s = np.ones((1 if g == -1 else K // g, N), dtype=np.float16)
         A = synth.activations(6, M, K)
         C = run_gemm(mk, A, q, s, g)
-        assert np.array_equal(C.view(np.uint16), A.view(np.uint16)), (M, g)
+        # The zero point enters as its own fp32 product (-8 * sum_k A_k), so
+        # an output that is small next to 8 * sum_k |A_k| -- here C = A while
+        # every other code is 8 and s = 1 -- carries the matrix cores' fp32
+        # rounding of sums of a few hundred: up to about 1e-3 absolute.  So
+        # identity weights reproduce A within the elementwise bar, not
+        # bit-exactly (with realistic scales s << 1 the error scales by s).
+        err = np.abs(C.astype(np.float64) - A.astype(np.float64))
+        assert (err <= 2e-3 + 1e-2 * np.abs(A.astype(np.float64))).all(), (M, g, float(err.max()))
 
 
 @pytest.mark.parametrize("M", [1, 32, 128])

@@ -2,82 +2,114 @@
 
 The kernel gives work-group w the unit range [w*T/grid, (w+1)*T/grid) of
 (column tile, 128-row block) units in column-major order (Section 3.4,
-"Striped Partitioning"), walks it in stages of KW blocks that never cross a
-column, writes a partial tile into slot 0 (its first column) or slot 1 (its
-last column) when it covers a column only in part, and the work-group whose
-arrival completes a column's count sums that column's slots.  This model
-re-states that schedule in Python and checks, for many shapes and grid
-sizes, that every unit is computed exactly once, every slot index and
-counter index is in range, the arrival count of every split column equals
-its number of partial segments, and no work-group is empty.
+"Striped Partitioning"), computed as w*(T div grid) + (w*(T mod grid)) div
+grid.  It walks the range in stages of KW blocks that never cross a column
+tile.  A tile covered only in part is combined across work-groups: the
+work-group's first tile (when shared and not also its last) goes to slot 0
+when its segment ends; its last tile (when shared) is kept in registers and
+either reduced at once, if every other contributor has already arrived, or
+written to slot 1.  This model re-states that schedule and the arrival
+protocol in Python and checks, for many shapes and grid sizes, that every
+unit is computed exactly once, the closed-form stage count matches the walk,
+the slot a reducer reads is the slot its writer used, every shared tile is
+reduced exactly once whatever the arrival order, and every counter returns
+to zero.
 """
+import random
+
 import pytest
 
 
 def range_start(w, total, grid):
-    return (w * total) // grid
+    q, r = divmod(total, grid)
+    return w * q + (w * r) // grid
 
 
 def unit_owner(u, total, grid):
     return ((u + 1) * grid - 1) // total
 
 
+def closed_form_stages(u0, u1, KU, KW):
+    c_first, c_last = u0 // KU, (u1 - 1) // KU
+    k0, k1 = u0 - c_first * KU, u1 - c_last * KU
+    ceil = lambda x: (x + KW - 1) // KW
+    if c_first == c_last:
+        return ceil(k1 - k0)
+    return ceil(KU - k0) + (c_last - c_first - 1) * ceil(KU) + ceil(k1)
+
+
 def walk(w, total, grid, KU, KW):
     """Yield (column, first block, segment begin, segment end, stage blocks)."""
     u0, u1 = range_start(w, total, grid), range_start(w + 1, total, grid)
-    if u0 >= u1:
-        return
-    c = u0 // KU
-    ku = u0 - c * KU
-    seg_begin = ku
-    ku_end = min(KU, u1 - c * KU)
-    while True:
-        blocks = [ku + kw for kw in range(KW) if ku + kw < ku_end]
-        yield c, ku, seg_begin, ku_end, blocks
-        ku += KW
-        if ku >= ku_end:
-            c += 1
-            ku = 0
-            seg_begin = 0
-            rem = u1 - c * KU
-            if rem <= 0:
-                return
-            ku_end = min(KU, rem)
+    c_first, c_last = u0 // KU, (u1 - 1) // KU
+    k0, k1 = u0 - c_first * KU, u1 - c_last * KU
+    c, ku, begin = c_first, k0, k0
+    end = k1 if c_first == c_last else KU
+    for _ in range(closed_form_stages(u0, u1, KU, KW)):
+        blocks = [ku + kw for kw in range(KW) if ku + kw < end]
+        yield c, ku, begin, end, blocks
+        if ku + KW >= end:
+            c, ku, begin = c + 1, 0, 0
+            end = KU if c < c_last else k1
+        else:
+            ku += KW
 
 
-def model(cols, KU, grid, KW):
+def contributors(c, KU, total, grid):
+    return unit_owner(c * KU, total, grid), unit_owner(c * KU + KU - 1, total, grid)
+
+
+def reader_slot(w, c, KU, total, grid):
+    """Slot the reducer reads for contributor w of tile c."""
+    last_tile = (range_start(w + 1, total, grid) - 1) // KU
+    return 1 if c == last_tile else 0
+
+
+def model(cols, KU, grid, KW, rng):
     total = cols * KU
     assert 1 <= grid <= total
     seen = {}
-    partials = {}        # column -> list of (w, slot)
+    shared = {}  # tile -> {w: "first" | "last"}
     for w in range(grid):
-        first_col = range_start(w, total, grid) // KU
+        u0, u1 = range_start(w, total, grid), range_start(w + 1, total, grid)
+        assert u0 < u1, "empty work-group %d" % w
+        c_last = (u1 - 1) // KU
         stages = list(walk(w, total, grid, KU, KW))
-        assert stages, "empty work-group %d" % w
+        assert sum(len(b) for *_, b in stages) == u1 - u0
         for (c, ku, sb, se, blocks) in stages:
             assert 0 <= c < cols
             for b in blocks:
                 assert 0 <= b < KU
                 seen[(c, b)] = seen.get((c, b), 0) + 1
-            if ku + KW >= se:  # segment end
-                if not (sb == 0 and se == KU):
-                    slot = 0 if c == first_col else 1
-                    partials.setdefault(c, []).append((w, slot))
+            if ku + KW >= se and not (sb == 0 and se == KU):  # partial segment ends
+                kind = "last" if c == c_last else "first"
+                assert w not in shared.get(c, {})
+                shared.setdefault(c, {})[w] = kind
     assert len(seen) == total and all(v == 1 for v in seen.values())
-    for c, lst in partials.items():
-        wf = unit_owner(c * KU, total, grid)
-        wl = unit_owner(c * KU + KU - 1, total, grid)
-        assert [w for w, _ in lst] == list(range(wf, wl + 1)), c
-        assert len(lst) == wl - wf + 1 >= 2
-        for w, slot in lst:
-            wcol = range_start(w, total, grid) // KU
-            assert slot == (0 if c == wcol else 1)
-        # each work-group holds at most one segment per slot
-    per_w = {}
-    for c, lst in partials.items():
-        for w, slot in lst:
-            assert (w, slot) not in per_w, "slot reused"
-            per_w[(w, slot)] = c
+    for c, who in shared.items():
+        wf, wl = contributors(c, KU, total, grid)
+        assert sorted(who) == list(range(wf, wl + 1)), c
+        for w, kind in who.items():
+            assert reader_slot(w, c, KU, total, grid) == (1 if kind == "last" else 0)
+        # arrival protocol under random orders: "first" contributors arrive
+        # with an increment; "last" ones peek, and arrive only if the peek
+        # does not show every other contributor.
+        for _ in range(8):
+            counter, reducers = 0, []
+            order = list(who)
+            rng.shuffle(order)
+            others = wl - wf
+            for w in order:
+                if who[w] == "last" and counter == others:
+                    reducers.append(w)
+                    counter = 0
+                    continue
+                old = counter
+                counter += 1
+                if old == others:
+                    reducers.append(w)
+                    counter = 0
+            assert len(reducers) == 1 and counter == 0, (c, order, reducers)
 
 
 @pytest.mark.parametrize("KW", [1, 2, 4])
@@ -88,4 +120,21 @@ def test_schedule(cols, KU, grid, KW):
     total = cols * KU
     if grid > total:
         grid = total
-    model(cols, KU, grid, KW)
+    model(cols, KU, grid, KW, random.Random(cols * 1000 + KU + grid))
+
+
+def test_range_start_matches_floor():
+    for total in (1, 7, 4096, 28672, 57344, 114688, (1 << 31) - 1):
+        for grid in (1, 3, 255, 256, 512):
+            if grid > total:
+                continue
+            for w in (0, 1, grid // 2, grid - 1, grid):
+                assert range_start(w, total, grid) == (w * total) // grid
+
+
+def test_scale_row_magic_exact():
+    """Scale row of block ku as ((ku << 6) * ceil(2^26 / gu)) >> 32."""
+    for gu in list(range(1, 70)) + [96, 127, 128, 255, 256, 1000, 4095, 4096, 8191, 8192]:
+        m = ((1 << 26) + gu - 1) // gu
+        for ku in list(range(0, 300)) + list(range(8192 - 300, 8192)):
+            assert ((ku << 6) * m) >> 32 == ku // gu, (gu, ku)
