@@ -57,12 +57,13 @@ int device_cu_count(int device)
     return cus;
 }
 
-// Tuning override, read once: MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>"
-// forces the column-tile width and the work-group count (sweeps only; the
-// heuristic below is the default).
+// Tuning override, read once: MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>"
+// forces the column-tile width, the work-group count and the partition
+// (sweeps only; the heuristic below is the default).
 struct ForcedConfig {
     int nb = 0;
     int grid = 0;
+    int whole = -1;
 };
 
 static ForcedConfig read_forced()
@@ -74,6 +75,8 @@ static ForcedConfig read_forced()
     if (q) f.nb = atoi(q + 3);
     q = strstr(e, "grid=");
     if (q) f.grid = atoi(q + 5);
+    q = strstr(e, "whole=");
+    if (q) f.whole = atoi(q + 6) ? 1 : 0;
     if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
@@ -86,14 +89,36 @@ static const ForcedConfig &forced()
 }
 
 // Configuration by rows of A per pass: mb = ceil(M / 16) rounded up to 1, 2,
-// 4 or 8; kStreamWaves waves splitting K, kStreamOcc work-groups per CU.
-// The column tile is 64 columns (nb = 4: the activation fragments of a
-// 128-row block serve four weight blocks) except on small layers
-// (K * N <= 2^24), where 32-column tiles halve the K range each work-group
-// covers; nb = 1 or 2 also when N is not a multiple of 64 * nb (choices
-// measured on MI355X).
+// 4 or 8; kStreamWaves waves splitting K, kStreamOcc work-groups per CU;
+// activation rows through LDS for M <= 8.
+//
+// Column tile width (nb 16-column blocks) and partition come from a cost
+// model fitted to MI355X measurements: a work-group streams its weights at a
+// rate that depends on the tile width and the rows of A (narrow tiles and
+// more rows cost more instructions per weight byte), whole tiles per
+// work-group cost ceil(tiles / grid) tiles (idle CUs allowed), and Stream-K
+// costs the average share plus the combination of shared tiles at the end
+// (device-coherent round trips, longer with more contributors per tile).
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
+namespace {
+// Bytes per microsecond one work-group streams, by rows class and nb = 4, 2, 1.
+double wg_rate(int mb, int ar, int nb)
+{
+    static const double r[6][3] = {
+        {26e3, 22e3, 13.6e3},  // M <= 4 (activation rows in LDS)
+        {23e3, 18.4e3, 12.2e3},  // M <= 8 (activation rows in LDS)
+        {17.8e3, 12.7e3, 7.5e3},  // M <= 16
+        {11.8e3, 7.6e3, 4.2e3},  // M <= 32
+        {6e3, 4e3, 0.0},         // M <= 64
+        {0.0, 2.5e3, 0.0},       // M <= 128 (64-column tiles spill registers)
+    };
+    const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : (mb == 2) ? 3 : (mb == 4) ? 4 : 5;
+    const int col = (nb == 4) ? 0 : (nb == 2) ? 1 : 2;
+    return r[row][col];
+}
+}  // namespace
+
 GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
 {
     (void)group_units;
@@ -102,18 +127,45 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     const int tiles16 = N / 16;
     const int ncu = cus < kMaxCus ? cus : kMaxCus;
     cfg.mb = (M <= 16) ? 1 : (M <= 32) ? 2 : (M <= 64) ? 4 : 8;
-    const bool small = (int64_t)K * N <= ((int64_t)1 << 24);
-    cfg.nb = (!small && tiles16 % 4 == 0) ? 4 : (tiles16 % 2 == 0 ? 2 : 1);
-    if (cfg.mb >= 4 && cfg.nb == 1) cfg.nb = 2;
-    if (cfg.mb == 8) cfg.nb = 2;  // register budget: 8 row blocks x 64 columns spill
-    if (forced().nb && tiles16 % forced().nb == 0 && !(cfg.mb >= 4 && forced().nb == 1)) cfg.nb = forced().nb;
-    const int64_t units = (int64_t)(tiles16 / cfg.nb) * KU;
+    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : 0;
     int64_t grid = (int64_t)ncu * kStreamOcc;
     if (forced().grid) grid = forced().grid;
     if (grid > (int64_t)kMaxCus * kMaxPerCu) grid = (int64_t)kMaxCus * kMaxPerCu;
-    if (grid > units) grid = units;  // every work-group must own at least one unit
-    if (grid < 1) grid = 1;
-    cfg.grid = (int)grid;
+
+    double best = 1e30;
+    cfg.nb = 0;
+    cfg.whole = 0;
+    int64_t best_grid = grid;
+    for (int nb = 4; nb >= 1; nb >>= 1) {
+        const double rate = wg_rate(cfg.mb, cfg.ar, nb);
+        if (tiles16 % nb != 0 || rate <= 0.0) continue;
+        if (forced().nb && nb != forced().nb) continue;
+        const int64_t tiles = tiles16 / nb;
+        const double tile_us = (double)nb * 8.0 * K / rate;  // 16*nb columns x K rows x 0.5 byte
+        if (forced().whole != 0) {
+            const int64_t g = tiles < grid ? tiles : grid;
+            const double t = (double)((tiles + g - 1) / g) * tile_us;
+            if (t < best) { best = t; cfg.nb = nb; cfg.whole = 1; best_grid = g; }
+        }
+        if (forced().whole != 1) {
+            const int64_t units = tiles * KU;
+            const int64_t g = grid < units ? grid : units;
+            const double per = (double)units / (double)g;  // units per work-group
+            const bool split = (units % g) != 0 || (units / g) % KU != 0;
+            const double contributors = split ? 1.0 + (double)KU / per : 1.0;
+            const double tail = split ? 3.5 + 0.5 * (contributors - 2.0) : 0.0;
+            const double t = per * tile_us / KU + tail;
+            if (t < best) { best = t; cfg.nb = nb; cfg.whole = 0; best_grid = g; }
+        }
+    }
+    if (cfg.nb == 0) {  // only when an override excludes every choice
+        cfg.nb = (tiles16 % 2 == 0) ? 2 : 1;
+        cfg.whole = 0;
+        const int64_t units = (int64_t)(tiles16 / cfg.nb) * KU;
+        best_grid = grid < units ? grid : units;
+    }
+    if (best_grid < 1) best_grid = 1;
+    cfg.grid = (int)best_grid;
     return cfg;
 }
 
@@ -253,8 +305,9 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         p.G = (int)G;
         p.KU = (int)(K / 128);
         p.units = (int)(N / (16 * cfg.nb)) * p.KU;
-        p.per_wg = p.units / cfg.grid;
-        p.extra = p.units % cfg.grid;
+        p.gran = cfg.whole ? p.KU : 1;
+        p.per_wg = (p.units / p.gran) / cfg.grid;
+        p.extra = (p.units / p.gran) % cfg.grid;
         p.group_units = gu;
         // Exact for every block index below 2^13 (K <= 2^20): with
         // e = gmagic * gu - 2^26 < gu <= 2^13, ku * e < 2^26.

@@ -118,11 +118,12 @@ __device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)
     return (int)__umulhi((uint32_t)ku << 6, p.gmagic);
 }
 
-// First unit of work-group w: floor(w * units / grid), from the host's
-// quotient and remainder so that no 64-bit division is needed.
+// First unit of work-group w: gran * floor(w * (units / gran) / grid), from
+// the host's quotient and remainder so that no 64-bit division is needed.
+// gran = KU hands out whole column tiles; gran = 1 splits tiles (Stream-K).
 __device__ __forceinline__ int range_start(const GemmProblem &p, int w, int grid)
 {
-    return w * p.per_wg + (int)((uint32_t)(w * p.extra) / (uint32_t)grid);
+    return (w * p.per_wg + (int)((uint32_t)(w * p.extra) / (uint32_t)grid)) * p.gran;
 }
 
 // Work-group that owns unit u: the largest w with range_start(w) <= u.
@@ -180,15 +181,25 @@ __device__ __forceinline__ float4_t load_partial(const float *slot, int blk, int
 // they processed that tile at the start of their ranges) the work-group adds
 // their slots to its registers and writes C at once; otherwise it writes slot
 // 1 and arrives like the others.
-template <int MB, int NB, int D, bool PER_CHANNEL>
+template <int MB, int NB, int D, int AR, bool PER_CHANNEL>
 __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
 {
     constexpr int KW = kStreamWaves;
     constexpr int kBlocks = NB * MB;               // 16x16 output blocks per wave
     constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
     constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
+    constexpr int kSL = PER_CHANNEL ? 0 : kSLoads;
+    // Activation rows through LDS (AR > 0, one 16-row block only): 4*AR rows
+    // of the stage's 128-row block land in a per-wave LDS ring by AR
+    // direct-to-LDS loads instead of 4 register loads of 16 padded rows.
+    constexpr int kARows = 4 * AR;
+    constexpr int kAStage = kARows * 256;            // bytes per wave and stage
+    constexpr int kLoads = AR + NB + kSL;            // vector-memory ops per stage (AR > 0)
     static_assert(KW == 4, "four waves per work-group");
+    static_assert(AR == 0 || MB == 1, "LDS activation rows need a single row block");
+    static_assert(AR == 0 || (D - 1) * kLoads + NB + kSL < 64, "vmcnt range");
     __shared__ float4_t red[KW * kBlocks * 64];
+    __shared__ __attribute__((aligned(16))) uint8_t a_lds[AR > 0 ? KW * D * kAStage + 256 : 16];
     __shared__ int flags[2];
 
     const int lane = threadIdx.x & 63;
@@ -222,13 +233,41 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     for (int mb = 0; mb < MB; ++mb)
         a_lane[mb] = (uint32_t)((mb * 16 + (lane & 15)) * p.K + 8 * lg) * 2u + (uint32_t)kw * 256u;
     const uint32_t s_lane = (uint32_t)lg * 32u;
+    // Direct-to-LDS activation loads: load i, lane l fetches row r = 4i + l/16,
+    // 16-byte chunk (l % 16) ^ r of the block (an XOR swizzle, so that the
+    // MFMA-operand reads of 16 rows hit 16 different bank groups).
+    // The MFMA operands are read back with ds_read_b128 at per-lane LDS
+    // addresses fixed for each ring slot; lanes of rows past the 4*AR loaded
+    // ones read a zero row (the 256 bytes after the ring) instead.
+    uint32_t a_dma[AR > 0 ? AR : 1];
+    uint32_t a_rd[AR > 0 ? D : 1][4];
+    if constexpr (AR > 0) {
+#pragma unroll
+        for (int i = 0; i < AR; ++i) {
+            const int r = 4 * i + lg;
+            a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ r) * 8)) * 2u + (uint32_t)kw * 256u;
+        }
+        const int am = lane & 15;
+        const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
+        const uint32_t zero_row = lds0 + KW * D * kAStage;
+        if (threadIdx.x < 16) *(u32x4_t *)(a_lds + KW * D * kAStage + threadIdx.x * 16) = u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < D; ++j)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const uint32_t chunk = (uint32_t)(((4 * t + lg) ^ am) << 4);
+                a_rd[j][t] = (am < kARows) ? lds0 + (uint32_t)((kw * D + j) * kAStage + am * 256) + chunk
+                                           : zero_row + chunk;
+            }
+        __syncthreads();  // zero row written before any wave reads it
+    }
     // Rows of A past M lie past the end of the A buffer: their loads return 0.
     const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
     const uint32_t a_bytes = (uint32_t)p.M * (uint32_t)p.K * 2u;
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
     u32x4_t wr[D][NB];
-    half8_t ar[D][4 * MB];
+    half8_t ar[AR > 0 ? 1 : D][4 * MB];
     half8_t sr[D][kSLoads];
 
     // ---- load cursor: wave-uniform, advanced once per stage ----
@@ -240,6 +279,15 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     auto issue = [&](int j) {
         const int my = ld_ku + kw;
         const bool on = my < ld_end;
+        if constexpr (AR > 0) {  // first, so a stage's LDS rows are its oldest loads
+            const __amdgpu_buffer_rsrc_t rd =
+                __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, on ? a_bytes : 0u, kBufferFlags);
+#pragma unroll
+            for (int i = 0; i < AR; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rd, (__attribute__((address_space(3))) void *)(a_lds + (kw * D + j) * kAStage + i * 1024), 16,
+                    (int)a_dma[i], ld_ku * 256, 0, 0);
+        }
         const __amdgpu_buffer_rsrc_t rw =
             __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
 #pragma unroll
@@ -248,20 +296,31 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
                 u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, ld_w, kAuxNonTemporal));
         const __amdgpu_buffer_rsrc_t ra =
             __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, on ? a_bytes : 0u, kBufferFlags);
+        if constexpr (AR == 0) {
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+            for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                ar[j][mb * 4 + t] = __builtin_bit_cast(
-                    half8_t, __builtin_amdgcn_raw_buffer_load_b128(ra, a_lane[mb] + t * 64, ld_ku * 256, 0));
+                for (int t = 0; t < 4; ++t)
+                    ar[j][mb * 4 + t] = __builtin_bit_cast(
+                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(ra, a_lane[mb] + t * 64, ld_ku * 256, 0));
+        }
         if constexpr (!PER_CHANNEL) {
             const __amdgpu_buffer_rsrc_t rs =
                 __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
             const uint32_t s_off = ld_s + ((uint32_t)scale_row_of(my, p) << 7);
+            if constexpr (NB == 1) {
+                // four scales: an 8-byte load (a 16-byte one would leave half
+                // of its destination dead, and the compiler would wait for the
+                // load before reusing those registers)
+                const uint64_t v = __builtin_bit_cast(
+                    uint64_t, __builtin_amdgcn_raw_buffer_load_b64(rs, s_lane, s_off, 0));
+                sr[j][0] = __builtin_bit_cast(half8_t, u32x4_t{(uint32_t)v, (uint32_t)(v >> 32), 0u, 0u});
+            } else {
 #pragma unroll
-            for (int i = 0; i < kSLoads; ++i)
-                sr[j][i] = __builtin_bit_cast(
-                    half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
+                for (int i = 0; i < kSLoads; ++i)
+                    sr[j][i] = __builtin_bit_cast(
+                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
+            }
         }
     };
     auto advance_ld = [&]() {
@@ -308,8 +367,28 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // difference scaled and accumulated in one fused multiply-add per value.
     auto compute = [&](int j) {
         half8_t a[4 * MB];
+        if constexpr (AR > 0) {
+            // Wait for this stage's direct-to-LDS rows: loads issued after
+            // them are the stage's own weight and scale loads and D-1 later
+            // stages (vector-memory ops complete in order).  The reads are
+            // written as assembly, with their own lgkmcnt wait, so that the
+            // compiler's conservative tracking of direct-to-LDS writes does
+            // not add waits for the whole ring.
+            constexpr int kAfter = (D - 1) * kLoads + NB + kSL;
+            __builtin_amdgcn_s_waitcnt((kAfter & 15) | (7 << 4) | (15 << 8) | ((kAfter >> 4) << 14));
+            asm volatile("" ::: "memory");
+            u32x4_t v[4];
 #pragma unroll
-        for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(ar[j][i]);
+            for (int t = 0; t < 4; ++t) asm volatile("ds_read_b128 %0, %1" : "=v"(v[t]) : "v"(a_rd[j][t]));
+            // The wait "redefines" the four results, so no use of them can be
+            // scheduled before the data has arrived.
+            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])::"memory");
+#pragma unroll
+            for (int t = 0; t < 4; ++t) a[t] = prescale(__builtin_bit_cast(half8_t, v[t]));
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(ar[j][i]);
+        }
         if constexpr (PER_CHANNEL) {
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
@@ -568,30 +647,44 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
 
 int slot_floats(const GemmConfig &cfg) { return cfg.nb * cfg.mb * 256; }
 
-template <int MB, int NB>
+// Ring depth: stages in flight per wave (weights in registers: NB words of
+// 16 bytes per lane per stage, so narrow tiles afford deep rings).
+template <int MB, int NB, int AR>
+constexpr int stream_depth()
+{
+    return (MB == 1) ? (NB == 4 ? 3 : NB == 2 ? 5 : 8) : (MB == 2) ? (NB == 4 ? 2 : 4) : 2;
+}
+
+template <int MB, int NB, int AR>
 hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    constexpr int D = (MB == 1) ? (NB == 4 ? 3 : NB == 2 ? 4 : 6) : (MB == 2) ? (NB == 4 ? 2 : 4) : 2;
+    constexpr int D = stream_depth<MB, NB, AR>();
     GemmProblem arg = p;
     void *args[] = {&arg};
-    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, D, true>
-                                          : (const void *)&w4a16_stream_kernel<MB, NB, D, false>;
+    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, true>
+                                          : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, false>;
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * kStreamWaves), args, 0, stream);
 }
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    switch (cfg.mb * 10 + cfg.nb) {
-    case 11: return launch_stream<1, 1>(cfg, p, stream);
-    case 12: return launch_stream<1, 2>(cfg, p, stream);
-    case 14: return launch_stream<1, 4>(cfg, p, stream);
-    case 21: return launch_stream<2, 1>(cfg, p, stream);
-    case 22: return launch_stream<2, 2>(cfg, p, stream);
-    case 24: return launch_stream<2, 4>(cfg, p, stream);
-    case 42: return launch_stream<4, 2>(cfg, p, stream);
-    case 44: return launch_stream<4, 4>(cfg, p, stream);
-    case 82: return launch_stream<8, 2>(cfg, p, stream);
-    case 84: return launch_stream<8, 4>(cfg, p, stream);
+    switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
+    case 110: return launch_stream<1, 1, 0>(cfg, p, stream);
+    case 111: return launch_stream<1, 1, 1>(cfg, p, stream);
+    case 112: return launch_stream<1, 1, 2>(cfg, p, stream);
+    case 120: return launch_stream<1, 2, 0>(cfg, p, stream);
+    case 121: return launch_stream<1, 2, 1>(cfg, p, stream);
+    case 122: return launch_stream<1, 2, 2>(cfg, p, stream);
+    case 140: return launch_stream<1, 4, 0>(cfg, p, stream);
+    case 141: return launch_stream<1, 4, 1>(cfg, p, stream);
+    case 142: return launch_stream<1, 4, 2>(cfg, p, stream);
+    case 210: return launch_stream<2, 1, 0>(cfg, p, stream);
+    case 220: return launch_stream<2, 2, 0>(cfg, p, stream);
+    case 240: return launch_stream<2, 4, 0>(cfg, p, stream);
+    case 420: return launch_stream<4, 2, 0>(cfg, p, stream);
+    case 440: return launch_stream<4, 4, 0>(cfg, p, stream);
+    case 820: return launch_stream<8, 2, 0>(cfg, p, stream);
+    case 840: return launch_stream<8, 4, 0>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -9,15 +9,19 @@
 namespace marlin {
 
 // One launch configuration of the GEMM kernel.
-//   mb  : 16-row blocks of A handled per pass (M_pad = 16 * mb, M <= M_pad)
-//   nb  : 16-column blocks per column tile (1, 2 or 4)
-//   grid: work-groups (Stream-K workers)
+//   mb   : 16-row blocks of A handled per pass (M_pad = 16 * mb, M <= M_pad)
+//   nb   : 16-column blocks per column tile (1, 2 or 4)
+//   ar   : 0, or (mb = 1 only) the activation rows arrive in LDS, 4 * ar of them
+//   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
+//   grid : work-groups
 constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
 constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
 struct GemmConfig {
     int mb;
     int nb;
+    int ar;
+    int whole;
     int grid;
 };
 
@@ -33,9 +37,10 @@ struct GemmProblem {
     int K;
     int G;                // scale rows
     int KU;               // 128-row blocks of K
-    int units;            // column tiles * KU: the striped partition's units
-    int per_wg;           // units / grid
-    int extra;            // units % grid
+    int units;            // column tiles * KU: 128-row blocks of all column tiles
+    int gran;             // units per partition item: KU (whole tiles) or 1
+    int per_wg;           // (units / gran) / grid
+    int extra;            // (units / gran) % grid
     int group_units;      // 128-row blocks per scale group; 0 = per-channel
     uint32_t gmagic;      // ceil(2^26 / group_units): row of block ku = (ku * 2^6 * gmagic) >> 32
 };
