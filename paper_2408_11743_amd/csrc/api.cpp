@@ -106,14 +106,15 @@ namespace {
 double wg_rate(int mb, int ar, int nb)
 {
     static const double r[6][3] = {
-        {26e3, 22e3, 13.6e3},  // M <= 4 (activation rows in LDS)
-        {23e3, 18.4e3, 12.2e3},  // M <= 8 (activation rows in LDS)
-        {17.8e3, 12.7e3, 7.5e3},  // M <= 16
-        {11.8e3, 7.6e3, 4.2e3},  // M <= 32
-        {6e3, 4e3, 0.0},         // M <= 64
-        {0.0, 2.5e3, 0.0},       // M <= 128 (64-column tiles spill registers)
+        {24.5e3, 20.7e3, 13.1e3},  // M <= 4 (activation rows in LDS)
+        {22.9e3, 18.4e3, 12.1e3},  // M <= 8
+        {19.1e3, 15.1e3, 10.4e3},  // M <= 16
+        {13.9e3, 11.5e3, 6.9e3},   // M <= 32
+        {6e3, 4e3, 0.0},           // M <= 64 (activation rows in registers)
+        {0.0, 2.5e3, 0.0},         // M <= 128 (64-column tiles spill registers)
     };
     const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : (mb == 2) ? 3 : (mb == 4) ? 4 : 5;
+    (void)ar;
     const int col = (nb == 4) ? 0 : (nb == 2) ? 1 : 2;
     return r[row][col];
 }
@@ -127,7 +128,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     const int tiles16 = N / 16;
     const int ncu = cus < kMaxCus ? cus : kMaxCus;
     cfg.mb = (M <= 16) ? 1 : (M <= 32) ? 2 : (M <= 64) ? 4 : 8;
-    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : 0;
+    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : (M <= 32) ? 8 : 0;
     int64_t grid = (int64_t)ncu * kStreamOcc;
     if (forced().grid) grid = forced().grid;
     if (grid > (int64_t)kMaxCus * kMaxPerCu) grid = (int64_t)kMaxCus * kMaxPerCu;

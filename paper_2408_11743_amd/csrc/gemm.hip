@@ -189,14 +189,15 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
     constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
     constexpr int kSL = PER_CHANNEL ? 0 : kSLoads;
-    // Activation rows through LDS (AR > 0, one 16-row block only): 4*AR rows
+    // Activation rows through LDS (AR > 0, up to two 16-row blocks): 4*AR rows
     // of the stage's 128-row block land in a per-wave LDS ring by AR
-    // direct-to-LDS loads instead of 4 register loads of 16 padded rows.
+    // direct-to-LDS loads, instead of 4*MB register loads of 16*MB padded
+    // rows held in a register ring.
     constexpr int kARows = 4 * AR;
     constexpr int kAStage = kARows * 256;            // bytes per wave and stage
     constexpr int kLoads = AR + NB + kSL;            // vector-memory ops per stage (AR > 0)
     static_assert(KW == 4, "four waves per work-group");
-    static_assert(AR == 0 || MB == 1, "LDS activation rows need a single row block");
+    static_assert(AR == 0 || (MB <= 2 && kARows <= 16 * MB), "LDS activation rows: at most two row blocks");
     static_assert(AR == 0 || (D - 1) * kLoads + NB + kSL < 64, "vmcnt range");
     __shared__ float4_t red[KW * kBlocks * 64];
     __shared__ __attribute__((aligned(16))) uint8_t a_lds[AR > 0 ? KW * D * kAStage + 256 : 16];
@@ -240,25 +241,28 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // addresses fixed for each ring slot; lanes of rows past the 4*AR loaded
     // ones read a zero row (the 256 bytes after the ring) instead.
     uint32_t a_dma[AR > 0 ? AR : 1];
-    uint32_t a_rd[AR > 0 ? D : 1][4];
+    uint32_t a_rd[AR > 0 ? D : 1][AR > 0 ? MB : 1][4];
     if constexpr (AR > 0) {
 #pragma unroll
         for (int i = 0; i < AR; ++i) {
             const int r = 4 * i + lg;
-            a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ r) * 8)) * 2u + (uint32_t)kw * 256u;
+            a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u + (uint32_t)kw * 256u;
         }
-        const int am = lane & 15;
         const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
         const uint32_t zero_row = lds0 + KW * D * kAStage;
         if (threadIdx.x < 16) *(u32x4_t *)(a_lds + KW * D * kAStage + threadIdx.x * 16) = u32x4_t{0u, 0u, 0u, 0u};
 #pragma unroll
         for (int j = 0; j < D; ++j)
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const uint32_t chunk = (uint32_t)(((4 * t + lg) ^ am) << 4);
-                a_rd[j][t] = (am < kARows) ? lds0 + (uint32_t)((kw * D + j) * kAStage + am * 256) + chunk
-                                           : zero_row + chunk;
-            }
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int am = mb * 16 + (lane & 15);
+                    const uint32_t chunk = (uint32_t)(((4 * t + lg) ^ (am & 15)) << 4);
+                    a_rd[j][mb][t] = (am < kARows)
+                                         ? lds0 + (uint32_t)((kw * D + j) * kAStage + am * 256) + chunk
+                                         : zero_row + chunk;
+                }
         __syncthreads();  // zero row written before any wave reads it
     }
     // Rows of A past M lie past the end of the A buffer: their loads return 0.
@@ -377,14 +381,23 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
             constexpr int kAfter = (D - 1) * kLoads + NB + kSL;
             __builtin_amdgcn_s_waitcnt((kAfter & 15) | (7 << 4) | (15 << 8) | ((kAfter >> 4) << 14));
             asm volatile("" ::: "memory");
-            u32x4_t v[4];
+            u32x4_t v[4 * MB];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) asm volatile("ds_read_b128 %0, %1" : "=v"(v[t]) : "v"(a_rd[j][t]));
-            // The wait "redefines" the four results, so no use of them can be
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    asm volatile("ds_read_b128 %0, %1" : "=v"(v[mb * 4 + t]) : "v"(a_rd[j][mb][t]));
+            // The wait "redefines" the results, so no use of them can be
             // scheduled before the data has arrived.
-            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])::"memory");
+            if constexpr (MB == 1) {
+                asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])::"memory");
+            } else {
+                asm volatile("s_waitcnt lgkmcnt(0)"
+                             : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
+                               "+v"(v[7])::"memory");
+            }
 #pragma unroll
-            for (int t = 0; t < 4; ++t) a[t] = prescale(__builtin_bit_cast(half8_t, v[t]));
+            for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(__builtin_bit_cast(half8_t, v[i]));
         } else {
 #pragma unroll
             for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(ar[j][i]);
@@ -652,7 +665,9 @@ int slot_floats(const GemmConfig &cfg) { return cfg.nb * cfg.mb * 256; }
 template <int MB, int NB, int AR>
 constexpr int stream_depth()
 {
-    return (MB == 1) ? (NB == 4 ? 3 : NB == 2 ? 5 : 8) : (MB == 2) ? (NB == 4 ? 2 : 4) : 2;
+    if constexpr (MB == 1) return NB == 4 ? 4 : NB == 2 ? 5 : 8;
+    if constexpr (MB == 2 && AR > 0) return NB == 4 ? 3 : 4;  // LDS ring of 32 rows: 8 KiB per wave-stage
+    return 2;
 }
 
 template <int MB, int NB, int AR>
@@ -669,18 +684,18 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
-    case 110: return launch_stream<1, 1, 0>(cfg, p, stream);
     case 111: return launch_stream<1, 1, 1>(cfg, p, stream);
     case 112: return launch_stream<1, 1, 2>(cfg, p, stream);
-    case 120: return launch_stream<1, 2, 0>(cfg, p, stream);
     case 121: return launch_stream<1, 2, 1>(cfg, p, stream);
     case 122: return launch_stream<1, 2, 2>(cfg, p, stream);
-    case 140: return launch_stream<1, 4, 0>(cfg, p, stream);
     case 141: return launch_stream<1, 4, 1>(cfg, p, stream);
     case 142: return launch_stream<1, 4, 2>(cfg, p, stream);
-    case 210: return launch_stream<2, 1, 0>(cfg, p, stream);
-    case 220: return launch_stream<2, 2, 0>(cfg, p, stream);
-    case 240: return launch_stream<2, 4, 0>(cfg, p, stream);
+    case 114: return launch_stream<1, 1, 4>(cfg, p, stream);
+    case 124: return launch_stream<1, 2, 4>(cfg, p, stream);
+    case 144: return launch_stream<1, 4, 4>(cfg, p, stream);
+    case 218: return launch_stream<2, 1, 8>(cfg, p, stream);
+    case 228: return launch_stream<2, 2, 8>(cfg, p, stream);
+    case 248: return launch_stream<2, 4, 8>(cfg, p, stream);
     case 420: return launch_stream<4, 2, 0>(cfg, p, stream);
     case 440: return launch_stream<4, 4, 0>(cfg, p, stream);
     case 820: return launch_stream<8, 2, 0>(cfg, p, stream);

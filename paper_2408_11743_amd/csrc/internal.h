@@ -11,7 +11,7 @@ namespace marlin {
 // One launch configuration of the GEMM kernel.
 //   mb   : 16-row blocks of A handled per pass (M_pad = 16 * mb, M <= M_pad)
 //   nb   : 16-column blocks per column tile (1, 2 or 4)
-//   ar   : 0, or (mb = 1 only) the activation rows arrive in LDS, 4 * ar of them
+//   ar   : 0, or (mb <= 2) the activation rows arrive in LDS, 4 * ar of them
 //   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
 //   grid : work-groups
 constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
