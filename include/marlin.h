@@ -130,19 +130,17 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  *   s_packed   device, packed scales (marlin_pack_weights layout, same group).
  *   C          device, fp16 [M][N] row-major, written (every element).
  *   workspace  device, >= marlin_workspace_bytes(M, N, K, group) bytes.  Its
- *              first 256 KiB (arrival counters) must be zero before its
+ *              first 1 MiB (arrival counters) must be zero before its
  *              first use (zero-fill the whole buffer once); every call
  *              leaves the counters at zero again, so one workspace serves
  *              any sequence of calls, of any shapes, issued in order on one
  *              stream, as long as it is large enough for each.  Calls that
  *              may overlap (different streams) need separate workspaces.
  *
- * Accumulation is fp32.  Group scales: for up to 32 rows of A per pass,
- * each 128-row fp32 partial product is multiplied by its scale; for more
- * rows the scale multiplies the fp16 weights before the product (one fp16
- * rounding per weight).  Per-channel scales multiply the final fp32 sum.
- * M > 128 runs as passes of 128 rows.  Results are bitwise reproducible for
- * a given device, shape and input.
+ * Accumulation is fp32.  Group scales multiply each 128-row fp32 partial
+ * product; per-channel scales multiply the final sum once.  M > 128 runs as
+ * passes of 128 rows.  Results are bitwise reproducible for a given device,
+ * shape and input.
  * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,
  * WORKSPACE_TOO_SMALL, HIP.
  */

@@ -88,9 +88,11 @@ static const ForcedConfig &forced()
     return f;
 }
 
-// Configuration by rows of A per pass: mb = ceil(M / 16) rounded up to 1, 2,
-// 4 or 8; kStreamWaves waves splitting K, kStreamOcc work-groups per CU;
-// activation rows through LDS for M <= 8.
+// Configuration by rows of A per pass (at most 128): mb = 1 (M <= 16) or 2
+// 16-row blocks per row group; beyond 32 rows the pass is split into row
+// groups of 32 that are tiles of their own (a tile is a column tile of one
+// row group); 4 * ar activation rows per group arrive in LDS; kStreamWaves
+// waves split K, kStreamOcc work-groups per CU.
 //
 // Column tile width (nb 16-column blocks) and partition come from a cost
 // model fitted to MI355X measurements: a work-group streams its weights at a
@@ -102,18 +104,17 @@ static const ForcedConfig &forced()
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
 namespace {
-// Bytes per microsecond one work-group streams, by rows class and nb = 4, 2, 1.
+// Bytes of weights per microsecond one work-group streams, by rows of A and
+// nb = 4, 2, 1 (measured; the activation rows arrive in LDS in every class).
 double wg_rate(int mb, int ar, int nb)
 {
-    static const double r[6][3] = {
-        {24.5e3, 20.7e3, 13.1e3},  // M <= 4 (activation rows in LDS)
+    static const double r[4][3] = {
+        {24.5e3, 20.7e3, 13.1e3},  // M <= 4
         {22.9e3, 18.4e3, 12.1e3},  // M <= 8
         {19.1e3, 15.1e3, 10.4e3},  // M <= 16
-        {13.9e3, 11.5e3, 6.9e3},   // M <= 32
-        {6e3, 4e3, 0.0},           // M <= 64 (activation rows in registers)
-        {0.0, 2.5e3, 0.0},         // M <= 128 (64-column tiles spill registers)
+        {13.9e3, 11.5e3, 6.9e3},   // M <= 32 (also each row group of 32 for larger M)
     };
-    const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : (mb == 2) ? 3 : (mb == 4) ? 4 : 5;
+    const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : 3;
     (void)ar;
     const int col = (nb == 4) ? 0 : (nb == 2) ? 1 : 2;
     return r[row][col];
@@ -127,8 +128,10 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     const int KU = K / 128;
     const int tiles16 = N / 16;
     const int ncu = cus < kMaxCus ? cus : kMaxCus;
-    cfg.mb = (M <= 16) ? 1 : (M <= 32) ? 2 : (M <= 64) ? 4 : 8;
-    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : (M <= 32) ? 8 : 0;
+    cfg.mb = (M <= 16) ? 1 : 2;
+    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
+    cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32 (at most 4 per 128-row pass)
+    if (cfg.rg < 1) cfg.rg = 1;
     int64_t grid = (int64_t)ncu * kStreamOcc;
     if (forced().grid) grid = forced().grid;
     if (grid > (int64_t)kMaxCus * kMaxPerCu) grid = (int64_t)kMaxCus * kMaxPerCu;
@@ -141,7 +144,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
         const double rate = wg_rate(cfg.mb, cfg.ar, nb);
         if (tiles16 % nb != 0 || rate <= 0.0) continue;
         if (forced().nb && nb != forced().nb) continue;
-        const int64_t tiles = tiles16 / nb;
+        const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
         const double tile_us = (double)nb * 8.0 * K / rate;  // 16*nb columns x K rows x 0.5 byte
         if (forced().whole != 0) {
             const int64_t g = tiles < grid ? tiles : grid;
@@ -162,7 +165,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     if (cfg.nb == 0) {  // only when an override excludes every choice
         cfg.nb = (tiles16 % 2 == 0) ? 2 : 1;
         cfg.whole = 0;
-        const int64_t units = (int64_t)(tiles16 / cfg.nb) * KU;
+        const int64_t units = (int64_t)(tiles16 / cfg.nb) * cfg.rg * KU;
         best_grid = grid < units ? grid : units;
     }
     if (best_grid < 1) best_grid = 1;
@@ -305,7 +308,8 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         p.K = (int)K;
         p.G = (int)G;
         p.KU = (int)(K / 128);
-        p.units = (int)(N / (16 * cfg.nb)) * p.KU;
+        p.rg = cfg.rg;
+        p.units = (int)(N / (16 * cfg.nb)) * cfg.rg * p.KU;
         p.gran = cfg.whole ? p.KU : 1;
         p.per_wg = (p.units / p.gran) / cfg.grid;
         p.extra = (p.units / p.gran) % cfg.grid;

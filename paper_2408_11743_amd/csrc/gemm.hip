@@ -189,18 +189,18 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
     constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
     constexpr int kSL = PER_CHANNEL ? 0 : kSLoads;
-    // Activation rows through LDS (AR > 0, up to two 16-row blocks): 4*AR rows
-    // of the stage's 128-row block land in a per-wave LDS ring by AR
-    // direct-to-LDS loads, instead of 4*MB register loads of 16*MB padded
-    // rows held in a register ring.
+    // Activation rows through LDS (one or two 16-row blocks): the 4*AR rows of
+    // the tile's row group for the stage's 128-row block land in a per-wave
+    // LDS ring by AR direct-to-LDS loads (only real rows are fetched; the
+    // register ring holds weights and scales only).
     constexpr int kARows = 4 * AR;
     constexpr int kAStage = kARows * 256;            // bytes per wave and stage
-    constexpr int kLoads = AR + NB + kSL;            // vector-memory ops per stage (AR > 0)
+    constexpr int kLoads = AR + NB + kSL;            // vector-memory ops per stage
     static_assert(KW == 4, "four waves per work-group");
-    static_assert(AR == 0 || (MB <= 2 && kARows <= 16 * MB), "LDS activation rows: at most two row blocks");
-    static_assert(AR == 0 || (D - 1) * kLoads + NB + kSL < 64, "vmcnt range");
+    static_assert(MB <= 2 && AR >= 1 && kARows <= 16 * MB, "one or two row blocks, at least 4 rows");
+    static_assert((D - 1) * kLoads + NB + kSL < 64, "vmcnt range");
     __shared__ float4_t red[KW * kBlocks * 64];
-    __shared__ __attribute__((aligned(16))) uint8_t a_lds[AR > 0 ? KW * D * kAStage + 256 : 16];
+    __shared__ __attribute__((aligned(16))) uint8_t a_lds[KW * D * kAStage + 256];
     __shared__ int flags[2];
 
     const int lane = threadIdx.x & 63;
@@ -216,23 +216,29 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     const int k0 = u0 - c_first * KU;  // first block in the first tile
     const int k1 = u1 - c_last * KU;   // end block in the last tile (1..KU)
 
-    // Byte offsets of tile c's block 0: weights (4 KiB per (64 columns x 128
-    // rows) block, 1 KiB per 16 columns) and scale rows (128 B per 64 columns).
+    // A tile c is column tile c / rg and row group c % rg (rows 32*(c % rg)
+    // onwards when M exceeds 32; one group otherwise).  Byte offsets of tile
+    // c's block 0: weights (4 KiB per (64 columns x 128 rows) block, 1 KiB per
+    // 16 columns) and scale rows (128 B per 64 columns).
+    const uint32_t RG = (uint32_t)p.rg;
+    auto col_of = [&](int c) -> uint32_t { return RG == 1 ? (uint32_t)c : (uint32_t)c / RG; };
     auto w_tile = [&](int c) -> uint32_t {
-        const uint32_t nbg = (uint32_t)c * NB;
+        const uint32_t nbg = col_of(c) * NB;
         return ((nbg >> 2) * (uint32_t)KU * 4u + (nbg & 3u)) << 10;
     };
     auto s_tile = [&](int c) -> uint32_t {
-        const uint32_t nbg = (uint32_t)c * NB;
+        const uint32_t nbg = col_of(c) * NB;
         return (((nbg >> 2) * (uint32_t)p.G) << 7) + (nbg & 3u) * 8u;
+    };
+    // First row of tile c's row group, and the rows it has (1 .. 16*MB).
+    auto row0_of = [&](int c) -> int { return RG == 1 ? 0 : (int)((uint32_t)c - col_of(c) * RG) * 32; };
+    auto rows_of = [&](int c) -> int {
+        const int r = p.M - row0_of(c);
+        return r < 16 * MB ? r : 16 * MB;
     };
 
     // Per-lane parts of the load addresses (fixed for the whole kernel).
     const uint32_t w_lane = (uint32_t)kw * 4096u + (uint32_t)lane * 16u;
-    uint32_t a_lane[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-        a_lane[mb] = (uint32_t)((mb * 16 + (lane & 15)) * p.K + 8 * lg) * 2u + (uint32_t)kw * 256u;
     const uint32_t s_lane = (uint32_t)lg * 32u;
     // Direct-to-LDS activation loads: load i, lane l fetches row r = 4i + l/16,
     // 16-byte chunk (l % 16) ^ r of the block (an XOR swizzle, so that the
@@ -240,9 +246,9 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // The MFMA operands are read back with ds_read_b128 at per-lane LDS
     // addresses fixed for each ring slot; lanes of rows past the 4*AR loaded
     // ones read a zero row (the 256 bytes after the ring) instead.
-    uint32_t a_dma[AR > 0 ? AR : 1];
-    uint32_t a_rd[AR > 0 ? D : 1][AR > 0 ? MB : 1][4];
-    if constexpr (AR > 0) {
+    uint32_t a_dma[AR];
+    uint32_t a_rd[D][MB][4];
+    {
 #pragma unroll
         for (int i = 0; i < AR; ++i) {
             const int r = 4 * i + lg;
@@ -267,11 +273,10 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     }
     // Rows of A past M lie past the end of the A buffer: their loads return 0.
     const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
-    const uint32_t a_bytes = (uint32_t)p.M * (uint32_t)p.K * 2u;
+
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
     u32x4_t wr[D][NB];
-    half8_t ar[AR > 0 ? 1 : D][4 * MB];
     half8_t sr[D][kSLoads];
 
     // ---- load cursor: wave-uniform, advanced once per stage ----
@@ -279,13 +284,16 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     int ld_end = (c_first == c_last) ? k1 : KU;
     uint32_t ld_w = w_tile(ld_c) + (uint32_t)ld_ku * 4096u;
     uint32_t ld_s = s_tile(ld_c);
+    // The tile's activation rows as their own buffer: rows past M read 0.
+    const uint16_t *ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
+    uint32_t a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
 
     auto issue = [&](int j) {
         const int my = ld_ku + kw;
         const bool on = my < ld_end;
-        if constexpr (AR > 0) {  // first, so a stage's LDS rows are its oldest loads
+        {  // first, so a stage's LDS rows are its oldest loads
             const __amdgpu_buffer_rsrc_t rd =
-                __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, on ? a_bytes : 0u, kBufferFlags);
+                __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, on ? a_bytes : 0u, kBufferFlags);
 #pragma unroll
             for (int i = 0; i < AR; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -298,16 +306,6 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
         for (int b = 0; b < NB; ++b)
             wr[j][b] = __builtin_bit_cast(
                 u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, ld_w, kAuxNonTemporal));
-        const __amdgpu_buffer_rsrc_t ra =
-            __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, on ? a_bytes : 0u, kBufferFlags);
-        if constexpr (AR == 0) {
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    ar[j][mb * 4 + t] = __builtin_bit_cast(
-                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(ra, a_lane[mb] + t * 64, ld_ku * 256, 0));
-        }
         if constexpr (!PER_CHANNEL) {
             const __amdgpu_buffer_rsrc_t rs =
                 __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
@@ -336,6 +334,10 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
             ld_end = (ld_c < c_last) ? KU : (ld_c == c_last) ? k1 : 0;  // 0: past the range
             ld_w = w_tile(ld_c);
             ld_s = s_tile(ld_c);
+            if (RG > 1 && ld_end > 0) {
+                ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
+                a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
+            }
         }
     };
 
@@ -371,7 +373,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // difference scaled and accumulated in one fused multiply-add per value.
     auto compute = [&](int j) {
         half8_t a[4 * MB];
-        if constexpr (AR > 0) {
+        {
             // Wait for this stage's direct-to-LDS rows: loads issued after
             // them are the stage's own weight and scale loads and D-1 later
             // stages (vector-memory ops complete in order).  The reads are
@@ -398,9 +400,6 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
             }
 #pragma unroll
             for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(__builtin_bit_cast(half8_t, v[i]));
-        } else {
-#pragma unroll
-            for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(ar[j][i]);
         }
         if constexpr (PER_CHANNEL) {
 #pragma unroll
@@ -413,31 +412,6 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
 #pragma unroll
                     for (int mb = 0; mb < MB; ++mb) acc[b][mb] = mfma(w, a[mb * 4 + t], acc[b][mb]);
                 }
-            }
-        } else if constexpr (MB >= 4) {
-            // Column block outer: each dequantized word feeds MB MFMAs and only
-            // MB fp32 temporaries are live at a time.
-            float4_t tb[MB];
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                for (int t = 0; t < 4; ++t) tb[mb] = mfma(kb, a[mb * 4 + t], t == 0 ? zero4 : tb[mb]);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                float4_t tmp[MB];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const half8_t w = dequant_sub(wr[j][b][t]);
-#pragma unroll
-                    for (int mb = 0; mb < MB; ++mb) tmp[mb] = mfma(w, a[mb * 4 + t], t == 0 ? zero4 : tmp[mb]);
-                }
-                const half8_t sv = sr[j][b >> 1];
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        acc[b][mb][i] = __builtin_fmaf(tmp[mb][i] - tb[mb][i], (float)sv[(b & 1) * 4 + i],
-                                                       acc[b][mb][i]);
             }
         } else {
             // k-step outer, column block inner: consecutive MFMAs are independent.
@@ -472,14 +446,16 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // block index blk = b*MB + mb; wave kw owns blk = kw + j*KW (< kBlocks)
     auto own = [&](int j) { return kw + j * KW; };
     auto store_c = [&](int c, const float4_t *out) {
+        const int r0 = row0_of(c), rows = rows_of(c);
+        const int col = (int)col_of(c);
 #pragma unroll
         for (int j = 0; j < kOwn; ++j) {
             const int blk = own(j);
             if (blk >= kBlocks) break;
             const int b = blk / MB, mb = blk % MB;
             const int m = mb * 16 + (lane & 15);
-            if (m < p.M) {
-                const int nbg = c * NB + b;
+            if (m < rows) {
+                const int nbg = col * NB + b;
                 float4_t v = out[j];
                 if constexpr (PER_CHANNEL) {
                     const half4_t s4 = *(const half4_t *)(p.S + (int64_t)(nbg >> 2) * 64 + lg * 16 + (nbg & 3) * 4);
@@ -490,7 +466,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
                     for (int i = 0; i < 4; ++i) v[i] *= kTwo24;
                 }
                 const half4_t h = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
-                *(half4_t *)(p.C + (int64_t)m * p.N + nbg * 16 + lg * 4) = h;
+                *(half4_t *)(p.C + (int64_t)(r0 + m) * p.N + nbg * 16 + lg * 4) = h;
             }
         }
     };
@@ -666,8 +642,7 @@ template <int MB, int NB, int AR>
 constexpr int stream_depth()
 {
     if constexpr (MB == 1) return NB == 4 ? 4 : NB == 2 ? 5 : 8;
-    if constexpr (MB == 2 && AR > 0) return NB == 4 ? 3 : 4;  // LDS ring of 32 rows: 8 KiB per wave-stage
-    return 2;
+    return NB == 4 ? 3 : 4;  // LDS ring of 32 rows: 8 KiB per wave-stage
 }
 
 template <int MB, int NB, int AR>
@@ -686,20 +661,16 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
     switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
     case 111: return launch_stream<1, 1, 1>(cfg, p, stream);
     case 112: return launch_stream<1, 1, 2>(cfg, p, stream);
+    case 114: return launch_stream<1, 1, 4>(cfg, p, stream);
     case 121: return launch_stream<1, 2, 1>(cfg, p, stream);
     case 122: return launch_stream<1, 2, 2>(cfg, p, stream);
+    case 124: return launch_stream<1, 2, 4>(cfg, p, stream);
     case 141: return launch_stream<1, 4, 1>(cfg, p, stream);
     case 142: return launch_stream<1, 4, 2>(cfg, p, stream);
-    case 114: return launch_stream<1, 1, 4>(cfg, p, stream);
-    case 124: return launch_stream<1, 2, 4>(cfg, p, stream);
     case 144: return launch_stream<1, 4, 4>(cfg, p, stream);
     case 218: return launch_stream<2, 1, 8>(cfg, p, stream);
     case 228: return launch_stream<2, 2, 8>(cfg, p, stream);
     case 248: return launch_stream<2, 4, 8>(cfg, p, stream);
-    case 420: return launch_stream<4, 2, 0>(cfg, p, stream);
-    case 440: return launch_stream<4, 4, 0>(cfg, p, stream);
-    case 820: return launch_stream<8, 2, 0>(cfg, p, stream);
-    case 840: return launch_stream<8, 4, 0>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

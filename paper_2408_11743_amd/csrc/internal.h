@@ -9,7 +9,8 @@
 namespace marlin {
 
 // One launch configuration of the GEMM kernel.
-//   mb   : 16-row blocks of A handled per pass (M_pad = 16 * mb, M <= M_pad)
+//   mb   : 16-row blocks of A per row group (1 or 2)
+//   rg   : row groups of 32 rows (M > 32), each a separate set of tiles
 //   nb   : 16-column blocks per column tile (1, 2 or 4)
 //   ar   : 0, or (mb <= 2) the activation rows arrive in LDS, 4 * ar of them
 //   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
@@ -21,6 +22,7 @@ struct GemmConfig {
     int mb;
     int nb;
     int ar;
+    int rg;
     int whole;
     int grid;
 };
@@ -32,7 +34,8 @@ struct GemmProblem {
     uint16_t *C;
     float *partials;      // fp32 partial tiles, 2 slots per work-group
     uint32_t *counters;   // one arrival counter per column tile
-    int M;                // rows in this pass (1 .. 16*mb)
+    int M;                // rows in this pass (1 .. 32 * rg)
+    int rg;               // row groups (tiles = column tiles * rg)
     int N;
     int K;
     int G;                // scale rows
@@ -49,9 +52,9 @@ struct GemmProblem {
 // computed with this bound, never with the device's.
 constexpr int kMaxCus = 256;
 constexpr int kMaxPerCu = 2;  // work-groups per compute unit, at most
-// Arrival counters at the start of every workspace: one per 16-column tile of
-// the largest N (2^20).
-constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4;
+// Arrival counters at the start of every workspace: one per tile for the
+// finest tiling of the largest N (2^20 / 16 column tiles, 4 row groups).
+constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4 * 4;
 
 // Device facts cached per device.
 int device_cu_count(int device);
