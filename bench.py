@@ -204,6 +204,7 @@ def main():
             "weight_GBps": round(R.weight_bytes(N, K, g) / (t_us * 1e-6) / 1e9, 1),
             "roof_us": round(troof, 3), "roof_frac": round(troof / t_us, 4),
             "bound": R.bound(M, N, K, g),
+            "launch": mk.marlin_describe(M, N, K, g),
         })
         log("M=%3d: %.3f us/call  %.1f weight GB/s  roofline frac %.3f" %
             (M, t_us, per_m[-1]["weight_GBps"], troof / t_us))

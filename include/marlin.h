@@ -150,6 +150,22 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
                             int64_t M, int64_t N, int64_t K, int64_t group,
                             hipStream_t stream);
 
+/*
+ * marlin_describe - the launch configuration marlin_gemm would use for this
+ * problem on the current device (or on a 256-CU device when no device is
+ * visible), as one NUL-terminated line: the kernel's name with its template
+ * arguments as a profiler reports it, then "nb=<16-column blocks per tile>
+ * rg=<row groups of 32> partition=<whole|streamk> grid=<work-groups>", for
+ * the first 128-row pass.  Pure host code apart from reading the device's
+ * compute-unit count; enqueues nothing.
+ *
+ *   buf        host, buf_bytes bytes, written (truncated to fit, always
+ *              NUL-terminated when buf_bytes > 0).
+ * Errors: NULL_POINTER (buf NULL), INVALID_SHAPE, UNSUPPORTED_GROUP.
+ */
+marlin_status_t marlin_describe(int64_t M, int64_t N, int64_t K, int64_t group,
+                                char *buf, size_t buf_bytes);
+
 #ifdef __cplusplus
 }
 #endif

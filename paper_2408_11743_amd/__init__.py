@@ -17,6 +17,7 @@ from ._binding import (  # noqa: F401
     LAYOUT_VERSION,
     MarlinError,
     lib,
+    marlin_describe,
     marlin_gemm,
     marlin_layout_version,
     marlin_pack_weights,

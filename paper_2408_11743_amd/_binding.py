@@ -37,6 +37,7 @@ SIGNATURES = {
     "marlin_pack_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "marlin_unpack_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "marlin_gemm": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _vp]),
+    "marlin_describe": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_char_p, _sz]),
 }
 
 
@@ -127,3 +128,10 @@ def marlin_gemm(A, w_packed, s_packed, C, workspace, workspace_bytes, M, N, K, g
     _check("marlin_gemm", lib().marlin_gemm(
         _ptr(A), _ptr(w_packed), _ptr(s_packed), _ptr(C), _ptr(workspace), workspace_bytes,
         M, N, K, group, _stream(stream)))
+
+
+def marlin_describe(M: int, N: int, K: int, group: int) -> str:
+    """Launch configuration marlin_gemm would use (kernel name and partition)."""
+    buf = ctypes.create_string_buffer(256)
+    _check("marlin_describe", lib().marlin_describe(M, N, K, group, buf, len(buf)))
+    return buf.value.decode()

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -320,6 +321,33 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         const hipError_t e = launch_gemm(cfg, p, stream);
         if (e != hipSuccess) return MARLIN_ERR_HIP;
     }
+    return MARLIN_OK;
+}
+
+marlin_status_t marlin_describe(int64_t M, int64_t N, int64_t K, int64_t group, char *buf,
+                                size_t buf_bytes)
+{
+    if (!buf) return MARLIN_ERR_NULL_POINTER;
+    if (M < 0 || M > (1 << 24)) return MARLIN_ERR_INVALID_SHAPE;
+    const marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    int cus = kMaxCus;
+    int device = 0;
+    int count = 0;
+    if (hipGetDeviceCount(&count) == hipSuccess && count > 0 && hipGetDevice(&device) == hipSuccess) {
+        const int c = device_cu_count(device);
+        if (c > 0) cus = c;
+    } else {
+        (void)hipGetLastError();
+    }
+    const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
+    const int mp = M < 128 ? (M > 0 ? (int)M : 1) : 128;
+    const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus);
+    char name[96];
+    kernel_name(cfg, gu == 0, name, sizeof(name));
+    if (buf_bytes > 0)
+        snprintf(buf, buf_bytes, "%s nb=%d rg=%d partition=%s grid=%d", name, cfg.nb, cfg.rg,
+                 cfg.whole ? "whole" : "streamk", cfg.grid);
     return MARLIN_OK;
 }
 

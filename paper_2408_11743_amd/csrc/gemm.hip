@@ -34,6 +34,7 @@
 //    work-group order (bitwise reproducible) and writes C.  No work-group
 //    ever waits for another, so no co-residency is assumed.
 #include <hip/hip_runtime.h>
+#include <stdio.h>
 
 #include "internal.h"
 
@@ -654,6 +655,32 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
     const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, true>
                                           : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, false>;
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * kStreamWaves), args, 0, stream);
+}
+
+void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
+{
+    int d = 0;
+    switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
+    case 111: d = stream_depth<1, 1, 1>(); break;
+    case 112: d = stream_depth<1, 1, 2>(); break;
+    case 114: d = stream_depth<1, 1, 4>(); break;
+    case 121: d = stream_depth<1, 2, 1>(); break;
+    case 122: d = stream_depth<1, 2, 2>(); break;
+    case 124: d = stream_depth<1, 2, 4>(); break;
+    case 141: d = stream_depth<1, 4, 1>(); break;
+    case 142: d = stream_depth<1, 4, 2>(); break;
+    case 144: d = stream_depth<1, 4, 4>(); break;
+    case 218: d = stream_depth<2, 1, 8>(); break;
+    case 228: d = stream_depth<2, 2, 8>(); break;
+    case 248: d = stream_depth<2, 4, 8>(); break;
+    default: break;
+    }
+    if (d == 0) {
+        if (n) buf[0] = 0;
+        return;
+    }
+    snprintf(buf, n, "w4a16_stream_kernel<%d, %d, %d, %d, %s>", cfg.mb, cfg.nb, d, cfg.ar,
+             per_channel ? "true" : "false");
 }
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)

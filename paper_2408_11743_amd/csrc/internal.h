@@ -63,6 +63,8 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int grid_cap);
 size_t workspace_bytes_for(const GemmConfig &cfg, int N);
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
+// Name of the kernel instantiation launch_gemm runs for cfg ("" if none).
+void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

@@ -1,0 +1,185 @@
+"""Summarise rocprofv3 output of bench.py into the text kept under profiles/.
+
+Usage (after the three profiling runs, see the command block this prints):
+
+    python -m paper_2408_11743_amd.profile_summary --trace DIR --fetch DIR \
+        --write DIR --bench BENCH_JSON --out OUT_PREFIX [--copy-mb 256]
+
+Reads
+  DIR/*kernel_stats.csv          (rocprofv3 --kernel-trace --stats)
+  DIR/*counter_collection.csv    (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)
+  BENCH_JSON                     (the JSON line bench.py printed in the trace run)
+and writes OUT_PREFIX_kernel_trace.md, OUT_PREFIX_traffic.md and
+OUT_PREFIX_traffic.json.  The counters are scaled by what they read for the
+plain device copies bench.py makes with --calibration-copy-mb (bytes known).
+Each M of the sweep is attributed to its kernel instantiation through
+marlin_describe, the library's own account of the launch it makes.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import statistics
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GEMM_SRC = os.path.join(HERE, "csrc", "gemm.hip")
+COPY_KERNEL = "copyBuffer"
+
+
+def _one(pattern: str) -> str:
+    files = sorted(glob.glob(pattern, recursive=True))
+    if not files:
+        raise SystemExit("no file matches %s" % pattern)
+    return files[0]
+
+
+def kernel_stats(trace_dir: str) -> dict[str, dict]:
+    out = {}
+    with open(_one(os.path.join(trace_dir, "**", "*kernel_stats.csv"))) as f:
+        for r in csv.DictReader(f):
+            out[r["Name"]] = {"calls": int(r["Calls"]), "avg_ns": float(r["AverageNs"]),
+                              "total_ns": float(r["TotalDurationNs"])}
+    return out
+
+
+def counter_per_dispatch(pmc_dir: str, counter: str) -> list[tuple[str, float]]:
+    """(kernel name, counter value summed over the dispatch's instances), per dispatch."""
+    per = {}
+    with open(_one(os.path.join(pmc_dir, "**", "*counter_collection.csv"))) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            key = int(r["Dispatch_Id"])
+            name, val = per.get(key, (r["Kernel_Name"], 0.0))
+            per[key] = (name, val + float(r["Counter_Value"]))
+    return [per[k] for k in sorted(per)]
+
+
+def short(name: str) -> str:
+    """'void marlin::(anonymous namespace)::w4a16_stream_kernel<1, 1, 8, 1, false>(...)' -> 'w4a16_stream_kernel<1, 1, 8, 1, false>'."""
+    base = name.replace("(anonymous namespace)::", "").replace("void ", "", 1)
+    base = base.split("(")[0].strip()
+    return base.split("::")[-1]
+
+
+def main() -> None:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--bench", required=True)
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--copy-mb", type=int, default=256)
+    ap.add_argument("--trace-cmd", default="")
+    ap.add_argument("--fetch-cmd", default="")
+    ap.add_argument("--write-cmd", default="")
+    a = ap.parse_args()
+
+    import paper_2408_11743_amd as mk
+
+    bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
+    K, N, g = bench["config"]["K"], bench["config"]["N"], bench["config"]["group"]
+    Ms = bench["config"]["M"]
+    # kernel name as a profiler prints it, e.g. "w4a16_stream_kernel<1, 1, 8, 1, false>"
+    describe = {M: mk.marlin_describe(M, N, K, g) for M in Ms}
+    kname = {M: describe[M].split(" nb=")[0] for M in Ms}
+
+    # ---- kernel trace ----
+    stats = kernel_stats(a.trace)
+    rows, step_ns = [], 0.0
+    for M in Ms:
+        hits = [(n, v) for n, v in stats.items() if short(n) == kname[M]]
+        if not hits:
+            raise SystemExit("kernel %s (M=%d) not in the trace" % (kname[M], M))
+        avg = hits[0][1]["avg_ns"]  # all launches of one instantiation (all Ms that share it)
+        cfg = "nb=" + describe[M].split(" nb=")[1] if " nb=" in describe[M] else ""
+        rows.append((M, kname[M], cfg, hits[0][1]["calls"], avg))
+        step_ns += avg
+    md = ["# Kernel trace: W4A16 GEMM, K = %d, N = %d, g = %d, M sweep %s" % (K, N, g, Ms), "",
+          "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
+          "Average duration per launch of each kernel instantiation over all its",
+          "launches in the run (warm-up included; other kernels, such as the fp16",
+          "comparator's, are not matched):", "",
+          "| M | kernel | configuration | launches | avg kernel us | bench us per launch |",
+          "|---|---|---|---|---|---|"]
+    per_m = {r["M"]: r["us"] for r in bench.get("per_m", [])}
+    for M, k, cfg, calls, avg in rows:
+        md.append("| %d | `%s` | %s | %d | %.3f | %.3f |" % (M, k, cfg, calls, avg / 1e3, per_m.get(M, float("nan"))))
+    bench_avg = bench["roofline"]["avg_launch_us"]
+    md += ["", "Mean over the %d launches of one step: %.3f us of kernel time (rocprofv3)," % (len(Ms), step_ns / len(Ms) / 1e3),
+           "%.3f us per launch measured by bench.py with HIP events over its timed region" % bench_avg,
+           "(`roofline.avg_launch_us`, an unprofiled run: --bench).  The event time of a",
+           "launch also holds the dispatch gap between consecutive graph nodes, which the",
+           "kernel time excludes (an empty kernel costs about 1.7 us per launch in a graph).",
+           "Shared instantiations (same kernel for several M) report one average for all",
+           "of their launches, so the per-M rows are approximate where a kernel is shared.", ""]
+    open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
+
+    # ---- traffic ----
+    fetch = counter_per_dispatch(a.fetch, "FETCH_SIZE")
+    write = counter_per_dispatch(a.write, "WRITE_SIZE")
+    copy_bytes = a.copy_mb * (1 << 20)
+    # The calibration copies are the largest copy dispatches of the run (the
+    # weight clones bench.py makes use the same copy kernel, on 8.65 MB).
+    def largest(samples):
+        v = [x for n, x in samples if COPY_KERNEL in n]
+        return [x for x in v if x >= 0.5 * max(v)] if v else []
+
+    cf, cw = largest(fetch), largest(write)
+    if not cf or not cw:
+        raise SystemExit("no calibration copies in the counter runs (--calibration-copy-mb)")
+    f_scale = copy_bytes / (statistics.median(cf) * 1024.0)
+    w_scale = copy_bytes / (statistics.median(cw) * 1024.0)
+
+    def per_kernel(samples, scale):
+        out = {}
+        for n, v in samples:
+            out.setdefault(short(n), []).append(v * 1024.0 * scale)
+        return {k: statistics.median(v) for k, v in out.items()}
+
+    fk, wk = per_kernel(fetch, f_scale), per_kernel(write, w_scale)
+    import paper_2408_11743_amd.roofline as R
+    trows, hbm = [], {}
+    step_bytes = 0.0
+    for M in Ms:
+        k = kname[M]
+        fb, wb = fk.get(k), wk.get(k)
+        if fb is None or wb is None:
+            raise SystemExit("kernel %s (M=%d) has no counter samples" % (k, M))
+        alg = R.w4a16_bytes(M, N, K, g)
+        trows.append((M, k, fb, wb, fb + wb, alg))
+        hbm["M=%d %s" % (M, k)] = round(fb + wb)
+        step_bytes += fb + wb
+    md = ["# HBM traffic: W4A16 GEMM, K = %d, N = %d, g = %d, M sweep %s" % (K, N, g, Ms), "",
+          "Commands (two counter passes, each its own run, `TMPDIR=/tmp`):", "", "```",
+          a.fetch_cmd, a.write_cmd, "```", "",
+          "Calibration: the same runs make plain device copies of %d MiB (the runtime's" % a.copy_mb,
+          "copy kernel).  Per copy FETCH_SIZE reads %.0f KiB for %d KiB read (scale x%.3f)," %
+          (statistics.median(cf), copy_bytes // 1024, f_scale),
+          "WRITE_SIZE %.0f KiB for %d KiB written (scale x%.3f)." % (statistics.median(cw), copy_bytes // 1024, w_scale),
+          "", "Per dispatch (median over the dispatches of each instantiation), scaled:", "",
+          "| M | kernel | fetch MB | write MB | HBM MB | algorithmic MB | ratio |",
+          "|---|---|---|---|---|---|---|"]
+    for M, k, fb, wb, tb, alg in trows:
+        md.append("| %d | `%s` | %.2f | %.2f | %.2f | %.2f | %.2f |" % (M, k, fb / 1e6, wb / 1e6, tb / 1e6, alg / 1e6, tb / alg))
+    digest = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+    md += ["", "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N.", "",
+           "Step average per launch: %.2f MB (bench.py reports it as `roofline.traffic`" % (step_bytes / len(Ms) / 1e6),
+           "while `paper_2408_11743_amd/csrc/gemm.hip` hashes to `%s...`)." % digest[:16], ""]
+    open(a.out + "_traffic.md", "w").write("\n".join(md) + "\n")
+    rec = {"workload": "W4A16 GEMM K=%d N=%d g=%d, M sweep %s (bench.py)" % (K, N, g, Ms),
+           "gemm_hip_sha256": digest,
+           "counter_scale": {"FETCH_SIZE": round(f_scale, 4), "WRITE_SIZE": round(w_scale, 4),
+                             "calibration": "device copies of %d MiB" % a.copy_mb},
+           "hbm_bytes_per_launch": hbm, "step_launches": Ms,
+           "step_avg_hbm_bytes_per_launch": round(step_bytes / len(Ms))}
+    json.dump(rec, open(a.out + "_traffic.json", "w"), indent=1)
+    print("wrote", a.out + "_kernel_trace.md", a.out + "_traffic.md", a.out + "_traffic.json")
+
+
+if __name__ == "__main__":
+    main()

@@ -121,3 +121,25 @@ def test_binding_raises_named_errors(L):
     with pytest.raises(B.MarlinError) as e:
         B.marlin_gemm(FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, 16, 4096, 4000, 128)
     assert e.value.status == SHAPE and "INVALID_SHAPE" in str(e.value)
+
+
+def test_describe_reports_a_launchable_configuration(L):
+    # no device here: the description is computed for a 256-CU device
+    import ctypes
+    buf = ctypes.create_string_buffer(256)
+    for M, N, K, g in [(1, 4096, 4096, 128), (16, 4096, 4096, 128), (32, 11008, 4096, -1),
+                       (128, 28672, 8192, 128), (200, 1024, 1024, 256)]:
+        assert L.marlin_describe(M, N, K, g, buf, len(buf)) == 0
+        text = buf.value.decode()
+        assert text.startswith("w4a16_stream_kernel<"), text
+        assert ("true>" in text) == (g == -1 or g == K), text
+        assert "partition=whole" in text or "partition=streamk" in text, text
+        assert int(text.split("grid=")[1]) >= 1
+    assert "rg=4" in B.marlin_describe(128, 4096, 4096, 128)
+    assert "rg=1" in B.marlin_describe(32, 4096, 4096, 128)
+    small = ctypes.create_string_buffer(8)
+    assert L.marlin_describe(1, 4096, 4096, 128, small, len(small)) == 0
+    assert len(small.value) == 7  # truncated, NUL-terminated
+    assert L.marlin_describe(1, 4096, 4096, 128, None, 0) == 1
+    assert L.marlin_describe(1, 4096, 4000, 128, buf, len(buf)) == 2
+    assert L.marlin_describe(1, 4096, 4096, 64, buf, len(buf)) == 3

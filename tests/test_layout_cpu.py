@@ -97,3 +97,30 @@ def test_dequant_recipe_every_code_every_slot(slot):
             val = (h[half].astype(np.float32) * np.float32(1 / 16) - np.float32(64 + zp))
             val = np.float16(val)  # one rounding, as a fused multiply-add
         assert float(val) == code - zp, (slot, code, float(val))
+
+
+@pytest.mark.parametrize("slot", range(8))
+def test_subnormal_operands_every_code_every_slot(slot):
+    # The kernel's form of the same trick with the magic number 0: the masked
+    # code alone, read as fp16, is the subnormal q * 2^-24 (lower nibble of a
+    # byte) or 16 q * 2^-24 (upper nibble); the activation paired with an
+    # upper nibble carries 1/16, and the zero point is the same encoding of
+    # the code 8 (8 * 2^-24 or 128 * 2^-24), subtracted.  In exact arithmetic
+    # w * a' - z * a' = (q - 8) * a * 2^-24 for every code in every slot.
+    from fractions import Fraction
+    zp = GOLD["zero_point"]["value"]
+    e = Fraction(1, 1 << 24)
+    half, sub = slot // 4, slot % 4
+    upper = sub % 2 == 1
+    zbits = 0x0080 if upper else 0x0008
+    assert Fraction(float(_fp16(zbits))) == (128 if upper else 8) * e
+    for code in range(16):
+        x = np.uint32(code << (4 * slot))
+        y = x >> np.uint32(8) if sub >= 2 else x
+        mask = np.uint32(0x00F000F0) if upper else np.uint32(0x000F000F)
+        h = np.array([y & mask], dtype=np.uint32).view(np.float16)[half]
+        w = Fraction(float(h))
+        assert w == (16 if upper else 1) * code * e, (slot, code)
+        for a in (Fraction(1), Fraction(-3, 4), Fraction(1027, 1024)):
+            a_scaled = a / 16 if upper else a
+            assert w * a_scaled - Fraction(float(_fp16(zbits))) * a_scaled == (code - zp) * a * e
