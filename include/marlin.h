@@ -141,6 +141,13 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  * product; per-channel scales multiply the final sum once.  M > 128 runs as
  * passes of 128 rows.  Results are bitwise reproducible for a given device,
  * shape and input.
+ *
+ * The launch configuration comes from a cost model of the device (see
+ * marlin_describe).  For tuning and tests, the environment variable
+ * MARLIN_FORCE_CONFIG="kind=<stream|tile>,nb=<1|2|4>,whole=<0|1>,grid=<n>"
+ * (any subset) overrides it where the shape allows, read at every call;
+ * marlin_workspace_bytes follows the same override, so size the workspace
+ * under the setting the calls will see.
  * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,
  * WORKSPACE_TOO_SMALL, HIP.
  */
@@ -154,10 +161,11 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
  * marlin_describe - the launch configuration marlin_gemm would use for this
  * problem on the current device (or on a 256-CU device when no device is
  * visible), as one NUL-terminated line: the kernel's name with its template
- * arguments as a profiler reports it, then "nb=<16-column blocks per tile>
- * rg=<row groups of 32> partition=<whole|streamk> grid=<work-groups>", for
- * the first 128-row pass.  Pure host code apart from reading the device's
- * compute-unit count; enqueues nothing.
+ * arguments as a profiler reports it, then "cols=<columns per tile>
+ * rg=<row groups> partition=<whole|streamk> grid=<work-groups>", for the
+ * first 128-row pass.  Row groups are of 32 rows for the stream kernel and
+ * of 16384 / cols rows for the tile kernel.  Pure host code apart from
+ * reading the device's compute-unit count; enqueues nothing.
  *
  *   buf        host, buf_bytes bytes, written (truncated to fit, always
  *              NUL-terminated when buf_bytes > 0).

@@ -58,13 +58,17 @@ int device_cu_count(int device)
     return cus;
 }
 
-// Tuning override, read once: MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>"
-// forces the column-tile width, the work-group count and the partition
-// (sweeps only; the heuristic below is the default).
+// Tuning and test override, read at every call (a process may change it
+// between calls):
+// MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>,kind=<stream|tile>" forces
+// the stream kernel's column-tile width, the work-group count, the partition
+// and the kernel where the shape allows it (the cost model below is the
+// default).
 struct ForcedConfig {
     int nb = 0;
     int grid = 0;
     int whole = -1;
+    int kind = -1;
 };
 
 static ForcedConfig read_forced()
@@ -78,16 +82,15 @@ static ForcedConfig read_forced()
     if (q) f.grid = atoi(q + 5);
     q = strstr(e, "whole=");
     if (q) f.whole = atoi(q + 6) ? 1 : 0;
+    if (strstr(e, "kind=stream")) f.kind = kKindStream;
+    if (strstr(e, "kind=tile")) f.kind = kKindTile;
     if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
 }
 
-static const ForcedConfig &forced()
-{
-    static const ForcedConfig f = read_forced();
-    return f;
-}
+// Read at every call, so that a process can change it between calls.
+static ForcedConfig forced() { return read_forced(); }
 
 // Configuration by rows of A per pass (at most 128): mb = 1 (M <= 16) or 2
 // 16-row blocks per row group; beyond 32 rows the pass is split into row
@@ -105,6 +108,15 @@ static const ForcedConfig &forced()
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
 namespace {
+// Tile kernel: time of one 128-row block of a tile, by rows per tile (64:
+// 4x1 waves, 128: 2x2), and the cost of combining its 64 KiB fp32 tiles
+// (fixed part, and per contributor: the reducer reads one slot per
+// contributor), fitted to MI355X measurements.
+constexpr double kTileUnitUs[2] = {1.50, 1.55};
+constexpr double kTileTailUs = 10.4, kTileTailPerContributorUs = 1.36;
+// Stream kernel: the combination costs 2.5 us + 0.5 us per contributor.
+constexpr double kStreamTailUs = 2.5, kStreamTailPerContributorUs = 0.5;
+
 // Bytes of weights per microsecond one work-group streams, by rows of A and
 // nb = 4, 2, 1 (measured; the activation rows arrive in LDS in every class).
 double wg_rate(int mb, int ar, int nb)
@@ -122,6 +134,39 @@ double wg_rate(int mb, int ar, int nb)
 }
 }  // namespace
 
+namespace {
+// Best partition of `tiles` tiles of KU units each over at most `grid`
+// work-groups, given the time of one unit: whole tiles per work-group, or a
+// Stream-K split that pays for combining shared tiles at the end.
+struct Partition {
+    double t;
+    int whole;
+    int64_t grid;
+};
+
+Partition best_partition(int64_t tiles, int KU, int64_t grid, double unit_us, double tail_us,
+                         double tail_per_contributor_us)
+{
+    Partition best{1e30, 0, 1};
+    if (forced().whole != 0) {
+        const int64_t g = tiles < grid ? tiles : grid;
+        const double t = (double)((tiles + g - 1) / g) * KU * unit_us;
+        if (t < best.t) best = {t, 1, g};
+    }
+    if (forced().whole != 1) {
+        const int64_t units = tiles * KU;
+        const int64_t g = grid < units ? grid : units;
+        const double per = (double)units / (double)g;  // units per work-group
+        const bool split = (units % g) != 0 || (units / g) % KU != 0;
+        const double contributors = split ? 1.0 + (double)KU / per : 1.0;
+        const double tail = split ? tail_us + tail_per_contributor_us * contributors : 0.0;
+        const double t = per * unit_us + tail;
+        if (t < best.t) best = {t, 0, g};
+    }
+    return best;
+}
+}  // namespace
+
 GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
 {
     (void)group_units;
@@ -129,41 +174,60 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     const int KU = K / 128;
     const int tiles16 = N / 16;
     const int ncu = cus < kMaxCus ? cus : kMaxCus;
-    cfg.mb = (M <= 16) ? 1 : 2;
-    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
-    cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32 (at most 4 per 128-row pass)
-    if (cfg.rg < 1) cfg.rg = 1;
     int64_t grid = (int64_t)ncu * kStreamOcc;
     if (forced().grid) grid = forced().grid;
     if (grid > (int64_t)kMaxCus * kMaxPerCu) grid = (int64_t)kMaxCus * kMaxPerCu;
 
+    // stream kernel
+    cfg.kind = kKindStream;
+    cfg.tile_wm = 0;
+    cfg.mb = (M <= 16) ? 1 : 2;
+    cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
+    cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32 (at most 4 per 128-row pass)
+    if (cfg.rg < 1) cfg.rg = 1;
     double best = 1e30;
     cfg.nb = 0;
     cfg.whole = 0;
     int64_t best_grid = grid;
-    for (int nb = 4; nb >= 1; nb >>= 1) {
-        const double rate = wg_rate(cfg.mb, cfg.ar, nb);
-        if (tiles16 % nb != 0 || rate <= 0.0) continue;
-        if (forced().nb && nb != forced().nb) continue;
-        const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
-        const double tile_us = (double)nb * 8.0 * K / rate;  // 16*nb columns x K rows x 0.5 byte
-        if (forced().whole != 0) {
-            const int64_t g = tiles < grid ? tiles : grid;
-            const double t = (double)((tiles + g - 1) / g) * tile_us;
-            if (t < best) { best = t; cfg.nb = nb; cfg.whole = 1; best_grid = g; }
+    if (forced().kind != kKindTile) {
+        for (int nb = 4; nb >= 1; nb >>= 1) {
+            const double rate = wg_rate(cfg.mb, cfg.ar, nb);
+            if (tiles16 % nb != 0 || rate <= 0.0) continue;
+            if (forced().nb && nb != forced().nb) continue;
+            const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
+            const Partition pt = best_partition(tiles, KU, grid, (double)nb * 1024.0 / rate, kStreamTailUs,
+                                                kStreamTailPerContributorUs);
+            if (pt.t < best) {
+                best = pt.t;
+                cfg.nb = nb;
+                cfg.whole = pt.whole;
+                best_grid = pt.grid;
+            }
         }
-        if (forced().whole != 1) {
-            const int64_t units = tiles * KU;
-            const int64_t g = grid < units ? grid : units;
-            const double per = (double)units / (double)g;  // units per work-group
-            const bool split = (units % g) != 0 || (units / g) % KU != 0;
-            const double contributors = split ? 1.0 + (double)KU / per : 1.0;
-            const double tail = split ? 3.5 + 0.5 * (contributors - 2.0) : 0.0;
-            const double t = per * tile_us / KU + tail;
-            if (t < best) { best = t; cfg.nb = nb; cfg.whole = 0; best_grid = g; }
+    }
+    // tile kernel (M > 32): 2x2 waves for more than 64 rows, else 4x1
+    if (M > 32 && forced().kind != kKindStream) {
+        const int wm = M > 64 ? 2 : 1;
+        const int cols = 64 * (4 / wm), rows = 64 * wm;
+        if (N % cols == 0) {
+            const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
+            const Partition pt = best_partition(tiles, KU, grid, kTileUnitUs[wm - 1], kTileTailUs,
+                                                kTileTailPerContributorUs);
+            if (pt.t < best || forced().kind == kKindTile) {
+                best = pt.t;
+                cfg.kind = kKindTile;
+                cfg.tile_wm = wm;
+                cfg.nb = 4;
+                cfg.mb = 4;
+                cfg.ar = 0;
+                cfg.rg = (M + rows - 1) / rows;
+                cfg.whole = pt.whole;
+                best_grid = pt.grid;
+            }
         }
     }
     if (cfg.nb == 0) {  // only when an override excludes every choice
+        cfg.kind = kKindStream;
         cfg.nb = (tiles16 % 2 == 0) ? 2 : 1;
         cfg.whole = 0;
         const int64_t units = (int64_t)(tiles16 / cfg.nb) * cfg.rg * KU;
@@ -310,7 +374,8 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         p.G = (int)G;
         p.KU = (int)(K / 128);
         p.rg = cfg.rg;
-        p.units = (int)(N / (16 * cfg.nb)) * cfg.rg * p.KU;
+        const int tile_cols = (cfg.kind == kKindTile) ? 64 * (4 / cfg.tile_wm) : 16 * cfg.nb;
+        p.units = (int)(N / tile_cols) * cfg.rg * p.KU;
         p.gran = cfg.whole ? p.KU : 1;
         p.per_wg = (p.units / p.gran) / cfg.grid;
         p.extra = (p.units / p.gran) % cfg.grid;
@@ -346,7 +411,8 @@ marlin_status_t marlin_describe(int64_t M, int64_t N, int64_t K, int64_t group, 
     char name[96];
     kernel_name(cfg, gu == 0, name, sizeof(name));
     if (buf_bytes > 0)
-        snprintf(buf, buf_bytes, "%s nb=%d rg=%d partition=%s grid=%d", name, cfg.nb, cfg.rg,
+        snprintf(buf, buf_bytes, "%s cols=%d rg=%d partition=%s grid=%d", name,
+                 cfg.kind == kKindTile ? 64 * (4 / cfg.tile_wm) : 16 * cfg.nb, cfg.rg,
                  cfg.whole ? "whole" : "streamk", cfg.grid);
     return MARLIN_OK;
 }

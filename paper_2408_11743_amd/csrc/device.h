@@ -1,0 +1,197 @@
+// Device helpers shared by the GEMM kernels: vector types, wait and barrier
+// primitives, the striped partition, and the combination of column tiles
+// shared by several work-groups (Section 3.4, "Striped Partitioning").
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace marlin {
+namespace dev {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kAuxNonTemporal = 2;  // cache-policy bit: non-temporal (streamed once)
+// Word 3 of a gfx9 buffer descriptor for raw (untyped) dword access.
+constexpr int kBufferFlags = 0x00020000;
+
+// s_waitcnt immediate for gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4]<<14.
+template <int V>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(V >= 0 && V < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((V & 15) | (7 << 4) | (15 << 8) | ((V >> 4) << 14));
+    asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0()
+{
+    __builtin_amdgcn_s_waitcnt(63 | (7 << 4) | (0 << 8) | (3 << 14));
+    asm volatile("" ::: "memory");
+}
+
+// Work-group barrier that does not wait for outstanding global loads.
+__device__ __forceinline__ void lds_barrier()
+{
+    wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ half2_t as_h2(uint32_t x) { return __builtin_bit_cast(half2_t, x); }
+__device__ __forceinline__ uint32_t as_u32(half2_t x) { return __builtin_bit_cast(uint32_t, x); }
+
+__device__ __forceinline__ float4_t mfma(half8_t w, half8_t a, float4_t c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, a, c, 0, 0, 0);
+}
+
+// Scale row of 128-row block ku: ku / group_units as one multiply-high with
+// the host's rounded-up reciprocal 2^26 / group_units (exact for ku < 2^13).
+__device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)
+{
+    return (int)__umulhi((uint32_t)ku << 6, p.gmagic);
+}
+
+// First unit of work-group w: gran * floor(w * (units / gran) / grid), from
+// the host's quotient and remainder so that no 64-bit division is needed.
+// gran = KU hands out whole tiles; gran = 1 splits tiles (Stream-K).
+__device__ __forceinline__ int range_start(const GemmProblem &p, int w, int grid)
+{
+    return (w * p.per_wg + (int)((uint32_t)(w * p.extra) / (uint32_t)grid)) * p.gran;
+}
+
+// Work-group that owns unit u: the largest w with range_start(w) <= u
+// (used only when tiles are split, gran = 1).
+__device__ __forceinline__ int unit_owner(const GemmProblem &p, int u, int grid)
+{
+    return (int)((((int64_t)u + 1) * grid - 1) / p.units);
+}
+
+// ---- partial tiles in the workspace ----
+// A work-group that covers a tile only in part writes its fp32 tile to one of
+// its two workspace slots (0: its first tile, 1: its last), in
+// structure-of-arrays order so every store instruction covers 256 contiguous
+// bytes: float index ((blk*4 + i)*64 + lane).  Those bytes are written and
+// read with relaxed agent-scope atomics, which the compiler emits as ordinary
+// vector stores / loads carrying the device-coherence bit, so they bypass the
+// per-XCD L2 non-coherence without a whole-cache writeback or invalidate.
+// Ordering: a wave waits for its stores to complete (vmcnt 0) before the
+// work-group barrier that precedes the arrival counter's atomic increment,
+// and a reducer issues its loads only after it has read the counter.
+__device__ __forceinline__ void store_partial(float *slot, int blk, int lane, float4_t v)
+{
+    float *d = slot + blk * 256 + lane;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) __hip_atomic_store(d + i * 64, v[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float4_t load_partial(const float *slot, int blk, int lane)
+{
+    const float *s = slot + blk * 256 + lane;
+    float4_t v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = __hip_atomic_load(s + i * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return v;
+}
+
+// Combination at the end of a work-group's range.  The first tile (if shared
+// and not also the last) was written to slot 0 when its segment ended; its
+// counter is now bumped.  The last tile (if shared) is in registers
+// (last_out): the counter is read first, and if every other contributor has
+// arrived the work-group adds their slots to its registers and writes C;
+// otherwise it writes slot 1 and arrives with an increment.  Whoever
+// completes a count sums the contributors' slots in work-group order (bitwise
+// reproducible) and resets the counter.  No work-group waits for another.
+//   KOWN         tile blocks this wave holds;  own(j): slot block index of
+//                block j, or -1 if the wave holds none there
+//   store_c(c, out[KOWN])  writes tile c's C from full sums
+template <int KOWN, typename OwnFn, typename StoreFn>
+__device__ __forceinline__ void combine_tiles(const GemmProblem &p, int *flags, int wg, int grid,
+                                              int slot_floats, int lane, bool has_first, int c_first,
+                                              bool has_last, int c_last, const float4_t (&last_out)[KOWN],
+                                              OwnFn own, StoreFn store_c)
+{
+    if (!has_first && !has_last) return;  // uniform across the work-group
+    const int KU = p.KU;
+    float *const my_slots = p.partials + (int64_t)wg * 2 * slot_floats;
+    // Contributors of tile c: work-groups owner(c*KU) .. owner(c*KU + KU - 1);
+    // the slot a contributor used for c: 1 if c is its last tile, else 0.
+    auto slot_of = [&](int w, int c) -> const float * {
+        const int w_last = (int)((uint32_t)(range_start(p, w + 1, grid) - 1) / (uint32_t)KU);
+        return p.partials + ((int64_t)w * 2 + (c == w_last ? 1 : 0)) * slot_floats;
+    };
+    auto others_of = [&](int c) { return unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid); };
+    wait_vmcnt<0>();  // this wave's slot-0 stores are complete
+    lds_barrier();
+    if (threadIdx.x == 0) {
+        int f0 = 0, f1 = 0;
+        if (has_first) {
+            const uint32_t old =
+                __hip_atomic_fetch_add(p.counters + c_first, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (old == (uint32_t)others_of(c_first)) {
+                f0 = 1;
+                __hip_atomic_store(p.counters + c_first, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (has_last) {
+            const uint32_t seen = __hip_atomic_load(p.counters + c_last, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (seen == (uint32_t)others_of(c_last)) {
+                f1 = 1;
+                __hip_atomic_store(p.counters + c_last, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        flags[0] = f0;
+        flags[1] = f1;
+    }
+    lds_barrier();
+    const bool reduce_first = has_first && flags[0] != 0;
+    bool reduce_last = has_last && flags[1] != 0;
+    if (has_last && !reduce_last) {
+        // Not every contributor has arrived: publish slot 1 and arrive.
+#pragma unroll
+        for (int j = 0; j < KOWN; ++j)
+            if (own(j) >= 0) store_partial(my_slots + slot_floats, own(j), lane, last_out[j]);
+        wait_vmcnt<0>();
+        lds_barrier();
+        if (threadIdx.x == 0) {
+            const uint32_t old =
+                __hip_atomic_fetch_add(p.counters + c_last, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            int f1 = 0;
+            if (old == (uint32_t)others_of(c_last)) {
+                f1 = 1;
+                __hip_atomic_store(p.counters + c_last, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            flags[1] = f1;
+        }
+        lds_barrier();
+        reduce_last = flags[1] != 0;
+    }
+    // Sum the contributors' slots in work-group order; this work-group's own
+    // last-tile sum comes from registers (the same values it would store).
+    auto reduce = [&](int c, bool own_in_regs) {
+        const int wf = unit_owner(p, c * KU, grid);
+        const int wl = unit_owner(p, c * KU + KU - 1, grid);
+        float4_t out[KOWN];
+        for (int w = wf; w <= wl; ++w) {
+            const float *slot = slot_of(w, c);
+#pragma unroll
+            for (int j = 0; j < KOWN; ++j) {
+                const int blk = own(j) >= 0 ? own(j) : 0;
+                const float4_t v = (own_in_regs && w == wg) ? last_out[j] : load_partial(slot, blk, lane);
+                out[j] = (w == wf) ? v : out[j] + v;
+            }
+        }
+        store_c(c, out);
+    };
+    if (reduce_last) reduce(c_last, true);
+    if (reduce_first) reduce(c_first, false);
+}
+
+}  // namespace dev
+}  // namespace marlin

@@ -36,45 +36,15 @@
 #include <hip/hip_runtime.h>
 #include <stdio.h>
 
+#include "device.h"
 #include "internal.h"
 
 namespace marlin {
 namespace {
 
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
-typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
-typedef float float4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+using namespace dev;
 
-constexpr int kAuxNonTemporal = 2;  // cache-policy bit: non-temporal (streamed once)
-// Word 3 of a gfx9 buffer descriptor for raw (untyped) dword access.
-constexpr int kBufferFlags = 0x00020000;
 constexpr float kTwo24 = 16777216.0f;  // undoes the 2^-24 of the subnormal operands
-
-// s_waitcnt immediate for gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4]<<14.
-__device__ __forceinline__ void wait_vmcnt0()
-{
-    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8) | (0 << 14));
-    asm volatile("" ::: "memory");
-}
-
-__device__ __forceinline__ void wait_lgkmcnt0()
-{
-    __builtin_amdgcn_s_waitcnt(63 | (7 << 4) | (0 << 8) | (3 << 14));
-    asm volatile("" ::: "memory");
-}
-
-// Work-group barrier that does not wait for outstanding global loads.
-__device__ __forceinline__ void lds_barrier()
-{
-    wait_lgkmcnt0();
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-__device__ __forceinline__ half2_t as_h2(uint32_t x) { return __builtin_bit_cast(half2_t, x); }
-__device__ __forceinline__ uint32_t as_u32(half2_t x) { return __builtin_bit_cast(uint32_t, x); }
 
 // Eight codes of one packed word -> eight MFMA operands in element order
 // j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).  Elements 0, 1, 4, 5
@@ -105,59 +75,6 @@ __device__ __forceinline__ half8_t prescale(half8_t a)
 __device__ __forceinline__ half8_t bias_operand()
 {
     return __builtin_bit_cast(half8_t, u32x4_t{0x00080008u, 0x00800080u, 0x00080008u, 0x00800080u});
-}
-
-__device__ __forceinline__ float4_t mfma(half8_t w, half8_t a, float4_t c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, a, c, 0, 0, 0);
-}
-
-// Scale row of 128-row block ku: ku / group_units as one multiply-high with
-// the host's rounded-up reciprocal 2^26 / group_units (exact for ku < 2^13).
-__device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)
-{
-    return (int)__umulhi((uint32_t)ku << 6, p.gmagic);
-}
-
-// First unit of work-group w: gran * floor(w * (units / gran) / grid), from
-// the host's quotient and remainder so that no 64-bit division is needed.
-// gran = KU hands out whole column tiles; gran = 1 splits tiles (Stream-K).
-__device__ __forceinline__ int range_start(const GemmProblem &p, int w, int grid)
-{
-    return (w * p.per_wg + (int)((uint32_t)(w * p.extra) / (uint32_t)grid)) * p.gran;
-}
-
-// Work-group that owns unit u: the largest w with range_start(w) <= u.
-__device__ __forceinline__ int unit_owner(const GemmProblem &p, int u, int grid)
-{
-    return (int)((((int64_t)u + 1) * grid - 1) / p.units);
-}
-
-// ---- cross-work-group partial tiles ----
-// A work-group that covers a column tile only in part writes its fp32 tile to
-// one of its two workspace slots (0: its first column tile, 1: its last), in
-// structure-of-arrays order so every store instruction covers 256 contiguous
-// bytes: float index ((blk*4 + i)*64 + lane).  Those bytes are written and
-// read with relaxed agent-scope atomics, which the compiler emits as ordinary
-// vector stores / loads carrying the device-coherence bit, so they bypass the
-// per-XCD L2 non-coherence without a whole-cache writeback or invalidate.
-// Ordering: a wave waits for its stores to complete (vmcnt 0) before the
-// work-group barrier that precedes the arrival counter's atomic increment,
-// and a reducer issues its loads only after it has read the counter.
-__device__ __forceinline__ void store_partial(float *slot, int blk, int lane, float4_t v)
-{
-    float *d = slot + blk * 256 + lane;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) __hip_atomic_store(d + i * 64, v[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ float4_t load_partial(const float *slot, int blk, int lane)
-{
-    const float *s = slot + blk * 256 + lane;
-    float4_t v;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = __hip_atomic_load(s + i * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return v;
 }
 
 // ---------------------------------------------------------------------------
@@ -473,7 +390,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     };
 
     const int slot_floats = kBlocks * 256;
-    float *const my_slots = p.partials + (int64_t)wg * 2 * slot_floats;
+    float *const my_slots = p.partials + (int64_t)wg * 2 * slot_floats;  // slot 0; slot 1 follows
     bool has_first = false, has_last = false;
     float4_t last_out[kOwn];
 #pragma unroll
@@ -556,86 +473,17 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     }
 
     // ---- combination of shared tiles ----
-    if (!has_first && !has_last) return;  // uniform across the work-group
-    // Contributors of tile c: work-groups owner(c*KU) .. owner(c*KU + KU - 1);
-    // the slot a contributor used for c: 1 if c is its last tile, else 0.
-    auto slot_of = [&](int w, int c) -> const float * {
-        const int wl_last = (int)((uint32_t)(range_start(p, w + 1, grid) - 1) / (uint32_t)KU);
-        return p.partials + ((int64_t)w * 2 + (c == wl_last ? 1 : 0)) * slot_floats;
-    };
-    wait_vmcnt0();  // this wave's slot-0 stores are complete
-    lds_barrier();
-    if (threadIdx.x == 0) {
-        int f0 = 0, f1 = 0;
-        if (has_first) {
-            const int c = c_first;
-            const int others = unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid);
-            const uint32_t old = __hip_atomic_fetch_add(p.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (old == (uint32_t)others) {
-                f0 = 1;
-                __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-        if (has_last) {
-            const int c = c_last;
-            const int others = unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid);
-            const uint32_t seen = __hip_atomic_load(p.counters + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (seen == (uint32_t)others) {
-                f1 = 1;
-                __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-        flags[0] = f0;
-        flags[1] = f1;
-    }
-    lds_barrier();
-    const bool reduce_first = has_first && flags[0] != 0;
-    bool reduce_last = has_last && flags[1] != 0;
-    if (has_last && !reduce_last) {
-        // Not every contributor has arrived: publish slot 1 and arrive.
-#pragma unroll
-        for (int j = 0; j < kOwn; ++j)
-            if (own(j) < kBlocks) store_partial(my_slots + slot_floats, own(j), lane, last_out[j]);
-        wait_vmcnt0();
-        lds_barrier();
-        if (threadIdx.x == 0) {
-            const int c = c_last;
-            const int others = unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid);
-            const uint32_t old = __hip_atomic_fetch_add(p.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            int f1 = 0;
-            if (old == (uint32_t)others) {
-                f1 = 1;
-                __hip_atomic_store(p.counters + c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            flags[1] = f1;
-        }
-        lds_barrier();
-        reduce_last = flags[1] != 0;
-    }
-    // Sum the contributors' slots in work-group order; this work-group's own
-    // last-tile sum comes from registers (the same values it would store).
-    auto reduce = [&](int c, bool own_in_regs) {
-        const int wf = unit_owner(p, c * KU, grid);
-        const int wl = unit_owner(p, c * KU + KU - 1, grid);
-        float4_t out[kOwn];
-        for (int w = wf; w <= wl; ++w) {
-            const float *slot = slot_of(w, c);
-#pragma unroll
-            for (int j = 0; j < kOwn; ++j) {
-                const int blk = own(j) < kBlocks ? own(j) : 0;
-                const float4_t v = (own_in_regs && w == wg) ? last_out[j] : load_partial(slot, blk, lane);
-                out[j] = (w == wf) ? v : out[j] + v;
-            }
-        }
-        store_c(c, out);
-    };
-    if (reduce_last) reduce(c_last, true);
-    if (reduce_first) reduce(c_first, false);
+    auto own_slot = [&](int j) { return own(j) < kBlocks ? own(j) : -1; };
+    combine_tiles<kOwn>(p, flags, wg, grid, slot_floats, lane, has_first, c_first, has_last, c_last, last_out,
+                        own_slot, store_c);
 }
 
 }  // namespace
 
-int slot_floats(const GemmConfig &cfg) { return cfg.nb * cfg.mb * 256; }
+int slot_floats(const GemmConfig &cfg)
+{
+    return cfg.kind == kKindTile ? 4 * 16 * 256 : cfg.nb * cfg.mb * 256;
+}
 
 // Ring depth: stages in flight per wave (weights in registers: NB words of
 // 16 bytes per lane per stage, so narrow tiles afford deep rings).
@@ -659,6 +507,10 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
 
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 {
+    if (cfg.kind == kKindTile) {
+        tile_kernel_name(cfg, per_channel, buf, n);
+        return;
+    }
     int d = 0;
     switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
     case 111: d = stream_depth<1, 1, 1>(); break;
@@ -685,6 +537,7 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
+    if (cfg.kind == kKindTile) return launch_tile_gemm(cfg, p, stream);
     switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
     case 111: return launch_stream<1, 1, 1>(cfg, p, stream);
     case 112: return launch_stream<1, 1, 2>(cfg, p, stream);

@@ -18,13 +18,18 @@ namespace marlin {
 constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
 constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
+constexpr int kKindStream = 0;  // w4a16_stream_kernel (any M; row groups of 32)
+constexpr int kKindTile = 1;    // w4a16_tile_kernel (M > 32; 64x64 tile per wave)
+
 struct GemmConfig {
+    int kind;
     int mb;
     int nb;
     int ar;
     int rg;
     int whole;
     int grid;
+    int tile_wm;  // tile kernel: waves along M (1: 4x1 waves, 256 x 64; 2: 2x2 waves, 128 x 128)
 };
 
 struct GemmProblem {
@@ -65,6 +70,8 @@ size_t workspace_bytes_for(const GemmConfig &cfg, int N);
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 // Name of the kernel instantiation launch_gemm runs for cfg ("" if none).
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
+hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
+void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

@@ -1,0 +1,390 @@
+// W4A16 GEMM for gfx950, large batches (33 <= M <= 128 rows per pass):
+// C[M,N] = A[M,K] * (s * (q - 8)), fp32 accumulation.
+//
+// Where the stream kernel is bound by its per-weight VALU work (it serves at
+// most 32 rows per dequantized weight), this kernel gives every wave a 64 x 64
+// output tile: each dequantized weight feeds four MFMAs, and the work is
+// bound by the matrix cores.
+//  * A work-group of four waves owns a tile of 64*WN columns x 64*WM rows
+//    (WN x WM waves, each 64 columns x 64 rows) over a range of 128-row blocks
+//    of K (whole tiles or a Stream-K split, as for the stream kernel).
+//  * The activation tile of a 128-row block (64*WM rows) is shared by the WN
+//    waves of a row: gfx950's direct-to-LDS buffer loads stage it in a P-deep
+//    LDS ring (each wave loads a quarter; one barrier per stage), XOR-swizzled
+//    so that the MFMA-operand reads of 16 rows hit 16 bank groups ("Memory
+//    Load Pipelining" of Section 3.4, with CDNA's direct-to-LDS loads in the
+//    role of cp.async).
+//  * Each wave streams its own 64 columns of packed weights (4 KiB per block)
+//    with non-temporal direct-to-LDS loads into its own part of the ring
+//    (registers are the scarce resource here: the 64x64 accumulators, the
+//    activation operands and the fold's temporaries fill them) and reads them
+//    back after the stage barrier.
+//  * int4 -> fp16 with the paper's magic number ("Dequantization and Tensor
+//    Cores"): the code ORed into the low mantissa bits of 1024.0 is 1024 + q,
+//    minus 1032 gives q - 8; the next nibble gives 1024 + 16q, fixed by one
+//    fma (x/16 - 72).  Exact, 9 VALU per 8 weights, no extra MFMA.
+//  * Group scales multiply each 128-row fp32 product (v_fma_mix_f32); per-
+//    channel scales multiply the final sum ("Groups and Instruction
+//    Ordering").
+//  * Tiles shared by work-groups are combined as in the stream kernel.
+#include <hip/hip_runtime.h>
+#include <stdio.h>
+
+#include "device.h"
+#include "internal.h"
+
+namespace marlin {
+namespace {
+
+using namespace dev;
+
+// Masks of the int4 -> fp16 conversion, made opaque once per kernel (an empty
+// asm "redefines" them in vector registers) so that (x & m) | o selects the
+// single v_and_or_b32 with register operands.
+struct DequantConsts {
+    uint32_t lo, hi, ex;
+};
+
+__device__ __forceinline__ DequantConsts dequant_consts()
+{
+    DequantConsts k{0x000F000Fu, 0x00F000F0u, 0x64006400u};
+    asm volatile("" : "+v"(k.lo), "+v"(k.hi), "+v"(k.ex));
+    return k;
+}
+
+// Eight codes of one packed word -> the eight fp16 values q - 8 in element
+// order j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).
+__device__ __forceinline__ half8_t dequant_magic(uint32_t x, const DequantConsts &k)
+{
+    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
+    const half2_t mul = {(_Float16)0.0625f, (_Float16)0.0625f};
+    const half2_t add = {(_Float16)-72.0f, (_Float16)-72.0f};
+    const uint32_t y = x >> 8;
+    const half2_t r0 = as_h2((x & k.lo) | k.ex) - sub;
+    const half2_t r1 = __builtin_elementwise_fma(as_h2((x & k.hi) | k.ex), mul, add);
+    const half2_t r2 = as_h2((y & k.lo) | k.ex) - sub;
+    const half2_t r3 = __builtin_elementwise_fma(as_h2((y & k.hi) | k.ex), mul, add);
+    return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
+}
+
+template <int WN, int WM, bool PER_CHANNEL>
+__global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
+{
+    static_assert(WN * WM == 4, "four waves");
+    constexpr int P = 3;                   // stages in flight (LDS ring of A, register ring of W)
+    constexpr int TR = 64 * WM;            // rows of A per tile
+    constexpr int kAStage = TR * 256;      // bytes of one A stage (TR rows x 128 k x 2 B)
+    constexpr int kDma = TR / 16;          // 1-KiB direct-to-LDS loads per wave per stage
+    // Scale loads per wave per stage: the stage's 64 group scales, or (per
+    // channel) the tile's 64 column scales, so that the epilogue of a tile
+    // finds them in registers instead of draining the load pipeline.
+    constexpr int kSL = 2;
+    constexpr int kStage = kAStage + 4 * 4096;  // A tile, then each wave's 4 KiB of weights
+    constexpr int kLoads = kDma + 4 + kSL;  // vector-memory ops per wave per stage
+    constexpr int kBlocks = 16;            // 16x16 output blocks per wave (4 column x 4 row blocks)
+    static_assert(kLoads + kSL < 64, "vmcnt range");
+    // ring of stages, then a scratch area for the loads issued past the end
+    __shared__ __attribute__((aligned(16))) uint8_t a_lds[P * kStage + (kDma + 4) * 1024];
+    __shared__ int flags[2];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wn = wave % WN, wm = wave / WN;
+    const int lg = lane >> 4;
+    const DequantConsts dq = dequant_consts();
+    const int KU = p.KU;
+    const int grid = gridDim.x;
+    const int wg = blockIdx.x;
+    const int u0 = range_start(p, wg, grid);
+    const int u1 = range_start(p, wg + 1, grid);
+    const int c_first = (int)((uint32_t)u0 / (uint32_t)KU);
+    const int c_last = (int)((uint32_t)(u1 - 1) / (uint32_t)KU);
+    const int k0 = u0 - c_first * KU;
+    const int k1 = u1 - c_last * KU;
+    const int n_st = u1 - u0;  // one 128-row block per stage
+
+    // Tile c: column group c / rg (64*WN columns), row group c % rg (TR rows).
+    const uint32_t RG = (uint32_t)p.rg;
+    auto cg_of = [&](int c) -> uint32_t { return RG == 1 ? (uint32_t)c : (uint32_t)c / RG; };
+    auto row0_of = [&](int c) -> int { return RG == 1 ? 0 : (int)((uint32_t)c - cg_of(c) * RG) * TR; };
+    auto rows_of = [&](int c) -> int {
+        const int r = p.M - row0_of(c);
+        return r < TR ? r : TR;
+    };
+    // this wave's 64-column tile index in the packed layout
+    auto c64_of = [&](int c) -> uint32_t { return cg_of(c) * WN + (uint32_t)wn; };
+
+    // Per-lane address parts.
+    const uint32_t w_lane = (uint32_t)lane * 16u;
+    const uint32_t s_lane = (uint32_t)lg * 32u;
+    uint32_t a_dma[kDma];  // this wave loads rows [wave*TR/4, (wave+1)*TR/4)
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+        const int r = wave * (TR / 4) + 4 * i + lg;
+        a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u;
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
+    uint32_t a_rd[P][4];  // row wm*64 + (lane & 15) (+ 16 mb via the offset field), chunk 4t + lg
+    uint32_t w_rd[P];     // this wave's weights, this lane's 16 bytes (+ 1 KiB per column block)
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            a_rd[j][t] = lds0 + (uint32_t)(j * kStage + (wm * 64 + (lane & 15)) * 256 +
+                                           (((4 * t + lg) ^ (lane & 15)) << 4));
+        w_rd[j] = lds0 + (uint32_t)(j * kStage + kAStage + wave * 4096 + lane * 16);
+    }
+    const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
+    const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
+
+    half8_t sr[P][2];
+
+    // ---- load cursor: one 128-row block per stage ----
+    int ld_c = c_first, ld_ku = k0;
+    int ld_end = (c_first == c_last) ? k1 : KU;
+    uint32_t ld_w = (c64_of(ld_c) * (uint32_t)KU + (uint32_t)ld_ku) << 12;
+    uint32_t ld_s = (c64_of(ld_c) * (uint32_t)p.G) << 7;
+    const uint16_t *ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
+    uint32_t a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
+
+    auto issue = [&](int j) {
+        const bool on = ld_ku < ld_end;
+        // Activation rows first (oldest loads of the stage).  Past the end they
+        // go to the scratch area: other waves may still read every ring slot.
+        const __amdgpu_buffer_rsrc_t ra =
+            __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, on ? a_bytes : 0u, kBufferFlags);
+        uint8_t *dst = on ? a_lds + j * kStage + wave * (kAStage / 4) : a_lds + P * kStage;
+#pragma unroll
+        for (int i = 0; i < kDma; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (__attribute__((address_space(3))) void *)(dst + i * 1024),
+                                                     16, (int)a_dma[i], ld_ku * 256, 0, 0);
+        const __amdgpu_buffer_rsrc_t rw =
+            __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
+        uint8_t *wdst = on ? a_lds + j * kStage + kAStage + wave * 4096 : a_lds + P * kStage + kDma * 1024;
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wdst + b * 1024),
+                                                     16, (int)(w_lane + b * 1024), (int)ld_w, 0, kAuxNonTemporal);
+        {
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
+            const uint32_t s_off = PER_CHANNEL ? ld_s : ld_s + ((uint32_t)scale_row_of(ld_ku, p) << 7);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                sr[j][i] = __builtin_bit_cast(
+                    half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
+        }
+    };
+    auto advance_ld = [&]() {
+        ld_ku += 1;
+        ld_w += 4096u;
+        if (ld_ku >= ld_end) {  // next tile (rare)
+            ld_c += 1;
+            ld_ku = 0;
+            ld_end = (ld_c < c_last) ? KU : (ld_c == c_last) ? k1 : 0;  // 0: past the range
+            ld_w = (c64_of(ld_c) * (uint32_t)KU) << 12;
+            ld_s = (c64_of(ld_c) * (uint32_t)p.G) << 7;
+            if (ld_end > 0) {
+                ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
+                a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
+            }
+        }
+    };
+
+#pragma unroll
+    for (int j = 0; j < P - 1; ++j) {
+        issue(j);
+        advance_ld();
+    }
+
+    float4_t acc[4][4];  // [column block][row block]
+    const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) acc[b][mb] = zero4;
+
+    // One stage (ring slot j): the wave's 16 output blocks, column block
+    // outer: each dequantized word feeds the four row blocks.
+    auto compute = [&](int j) {
+        u32x4_t wv[4];    // [column block] this lane's packed weights
+        u32x4_t v[4][4];  // [row block][k-step] activation operands
+        asm volatile("ds_read_b128 %0, %1" : "=v"(wv[0]) : "v"(w_rd[j]));
+        asm volatile("ds_read_b128 %0, %1 offset:1024" : "=v"(wv[1]) : "v"(w_rd[j]));
+        asm volatile("ds_read_b128 %0, %1 offset:2048" : "=v"(wv[2]) : "v"(w_rd[j]));
+        asm volatile("ds_read_b128 %0, %1 offset:3072" : "=v"(wv[3]) : "v"(w_rd[j]));
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            asm volatile("ds_read_b128 %0, %1" : "=v"(v[0][t]) : "v"(a_rd[j][t]));
+            asm volatile("ds_read_b128 %0, %1 offset:4096" : "=v"(v[1][t]) : "v"(a_rd[j][t]));
+            asm volatile("ds_read_b128 %0, %1 offset:8192" : "=v"(v[2][t]) : "v"(a_rd[j][t]));
+            asm volatile("ds_read_b128 %0, %1 offset:12288" : "=v"(v[3][t]) : "v"(a_rd[j][t]));
+        }
+        // The wait "redefines" the results: no use is scheduled before it.
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[0][2]), "+v"(v[0][3]), "+v"(v[1][0]), "+v"(v[1][1]),
+                       "+v"(v[1][2]), "+v"(v[1][3]), "+v"(v[2][0]), "+v"(v[2][1]), "+v"(v[2][2]), "+v"(v[2][3]),
+                       "+v"(v[3][0]), "+v"(v[3][1]), "+v"(v[3][2]), "+v"(v[3][3]), "+v"(wv[0]), "+v"(wv[1]),
+                       "+v"(wv[2]), "+v"(wv[3])::"memory");
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            if constexpr (PER_CHANNEL) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const half8_t w = dequant_magic(wv[b][t], dq);
+#pragma unroll
+                    for (int mb = 0; mb < 4; ++mb)
+                        acc[b][mb] = mfma(w, __builtin_bit_cast(half8_t, v[mb][t]), acc[b][mb]);
+                }
+            } else {
+                float4_t tmp[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const half8_t w = dequant_magic(wv[b][t], dq);
+#pragma unroll
+                    for (int mb = 0; mb < 4; ++mb)
+                        tmp[mb] = mfma(w, __builtin_bit_cast(half8_t, v[mb][t]), t == 0 ? zero4 : tmp[mb]);
+                }
+                const half8_t sv = sr[j][b >> 1];
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        acc[b][mb][i] = __builtin_fmaf(tmp[mb][i], (float)sv[(b & 1) * 4 + i], acc[b][mb][i]);
+            }
+        }
+    };
+
+    // block j of this wave = column block j / 4, row block j % 4; slot index wave*16 + j
+    auto own = [&](int j) { return wave * kBlocks + j; };
+    // Tile c's C from full sums; per-channel scales: this lane's 16 column
+    // scales (column block b, value i at element 4b + i).
+    auto store_c_scaled = [&](int c, const float4_t *out, const half8_t (&cs)[2]) {
+        const int r0 = row0_of(c) + wm * 64, rows = rows_of(c) - wm * 64;
+        const uint32_t c64 = c64_of(c);
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            const int b = j / 4, mb = j % 4;
+            const int m = mb * 16 + (lane & 15);
+            if (m < rows) {
+                float4_t vv = out[j];
+                if constexpr (PER_CHANNEL) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) vv[i] *= (float)cs[b >> 1][(b & 1) * 4 + i];
+                }
+                const half4_t h = {(_Float16)vv[0], (_Float16)vv[1], (_Float16)vv[2], (_Float16)vv[3]};
+                *(half4_t *)(p.C + (int64_t)(r0 + m) * p.N + c64 * 64 + b * 16 + lg * 4) = h;
+            }
+        }
+    };
+
+    const int slot_floats = 4 * kBlocks * 256;
+    float *const my_slots = p.partials + (int64_t)wg * 2 * slot_floats;  // slot 0; slot 1 follows
+    bool has_first = false, has_last = false;
+
+    int cp_c = c_first, cp_ku = k0, cp_begin = k0;
+    int cp_end = (c_first == c_last) ? k1 : KU;
+    // A segment is complete: write C (whole tile) or slot 0 (shared first
+    // tile).  A shared last tile stays in acc: it is the range's final
+    // segment, combined after the loop.
+    auto finish_segment = [&](int j_stage) {
+        const bool partial = cp_begin != 0 || cp_end != KU;
+        if (partial && cp_c == c_last) {
+            has_last = true;
+            return;
+        }
+        float4_t out[kBlocks];
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            out[j] = acc[j / 4][j % 4];
+            acc[j / 4][j % 4] = zero4;
+        }
+        if (partial) {
+            has_first = true;
+#pragma unroll
+            for (int j = 0; j < kBlocks; ++j) store_partial(my_slots, own(j), lane, out[j]);
+        } else {
+            store_c_scaled(cp_c, out, sr[j_stage]);
+        }
+    };
+
+    // Stage st: wait for this wave's direct-to-LDS loads of the stage (loads
+    // issued after them: the stage's scales and the P - 2 stages issued later;
+    // vector-memory operations complete in order), meet at the barrier (now
+    // the whole stage is in LDS, and every wave is done with the slot of stage
+    // st - 1), refill that slot with stage st + P - 1, compute.
+    // Loads are issued unconditionally (past the range into the scratch
+    // area, through empty descriptors) so that every stage has the same load
+    // pattern and the compiler's own vmcnt waits (for the scale registers)
+    // stay static.
+    constexpr int kAfter = kSL + (P - 2) * kLoads;
+    for (int st0 = 0; st0 < n_st; st0 += P) {
+#pragma unroll
+        for (int j = 0; j < P; ++j) {
+            const bool live = st0 + j < n_st;
+            if (live) {
+                wait_vmcnt<kAfter>();
+                __builtin_amdgcn_s_barrier();
+                asm volatile("" ::: "memory");
+            }
+            issue((j + P - 1) % P);
+            advance_ld();
+            if (live) {
+                compute(j);
+                if (cp_ku + 1 >= cp_end) {
+                    finish_segment(j);
+                    cp_c += 1;
+                    cp_ku = 0;
+                    cp_begin = 0;
+                    cp_end = (cp_c < c_last) ? KU : k1;
+                } else {
+                    cp_ku += 1;
+                }
+            }
+        }
+    }
+
+    float4_t last_out[kBlocks];
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) last_out[j] = acc[j / 4][j % 4];
+    auto own_slot = [&](int j) { return own(j); };
+    // After the loop nothing is in flight to wait behind: load the column
+    // scales directly.
+    auto store_c = [&](int c, const float4_t *out) {
+        half8_t cs[2] = {};
+        if constexpr (PER_CHANNEL) {
+            const half8_t *src = (const half8_t *)(p.S + (int64_t)c64_of(c) * 64 + lg * 16);
+            cs[0] = src[0];
+            cs[1] = src[1];
+        }
+        store_c_scaled(c, out, cs);
+    };
+    combine_tiles<kBlocks>(p, flags, wg, grid, slot_floats, lane, has_first, c_first, has_last, c_last, last_out,
+                           own_slot, store_c);
+}
+
+}  // namespace
+
+template <int WN, int WM>
+hipError_t launch_tile(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
+{
+    GemmProblem arg = p;
+    void *args[] = {&arg};
+    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_tile_kernel<WN, WM, true>
+                                          : (const void *)&w4a16_tile_kernel<WN, WM, false>;
+    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(256), args, 0, stream);
+}
+
+hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
+{
+    if (cfg.tile_wm == 1) return launch_tile<4, 1>(cfg, p, stream);
+    if (cfg.tile_wm == 2) return launch_tile<2, 2>(cfg, p, stream);
+    return hipErrorInvalidValue;
+}
+
+void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
+{
+    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %s>", 4 / cfg.tile_wm, cfg.tile_wm, per_channel ? "true" : "false");
+}
+
+}  // namespace marlin

@@ -86,7 +86,7 @@ def main() -> None:
     Ms = bench["config"]["M"]
     # kernel name as a profiler prints it, e.g. "w4a16_stream_kernel<1, 1, 8, 1, false>"
     describe = {M: mk.marlin_describe(M, N, K, g) for M in Ms}
-    kname = {M: describe[M].split(" nb=")[0] for M in Ms}
+    kname = {M: describe[M].split(" cols=")[0] for M in Ms}
 
     # ---- kernel trace ----
     stats = kernel_stats(a.trace)
@@ -96,7 +96,7 @@ def main() -> None:
         if not hits:
             raise SystemExit("kernel %s (M=%d) not in the trace" % (kname[M], M))
         avg = hits[0][1]["avg_ns"]  # all launches of one instantiation (all Ms that share it)
-        cfg = "nb=" + describe[M].split(" nb=")[1] if " nb=" in describe[M] else ""
+        cfg = "cols=" + describe[M].split(" cols=")[1] if " cols=" in describe[M] else ""
         rows.append((M, kname[M], cfg, hits[0][1]["calls"], avg))
         step_ns += avg
     md = ["# Kernel trace: W4A16 GEMM, K = %d, N = %d, g = %d, M sweep %s" % (K, N, g, Ms), "",

@@ -131,11 +131,14 @@ def test_describe_reports_a_launchable_configuration(L):
                        (128, 28672, 8192, 128), (200, 1024, 1024, 256)]:
         assert L.marlin_describe(M, N, K, g, buf, len(buf)) == 0
         text = buf.value.decode()
-        assert text.startswith("w4a16_stream_kernel<"), text
+        assert text.startswith("w4a16_stream_kernel<") or (M > 32 and text.startswith("w4a16_tile_kernel<")), text
         assert ("true>" in text) == (g == -1 or g == K), text
         assert "partition=whole" in text or "partition=streamk" in text, text
+        cols = int(text.split("cols=")[1].split()[0])
+        assert cols in (16, 32, 64, 128, 256) and N % cols == 0, text
+        rows = 32 if text.startswith("w4a16_stream_kernel<") else 16384 // cols
+        assert int(text.split("rg=")[1].split()[0]) == -(-min(M, 128) // rows), text
         assert int(text.split("grid=")[1]) >= 1
-    assert "rg=4" in B.marlin_describe(128, 4096, 4096, 128)
     assert "rg=1" in B.marlin_describe(32, 4096, 4096, 128)
     small = ctypes.create_string_buffer(8)
     assert L.marlin_describe(1, 4096, 4096, 128, small, len(small)) == 0
@@ -143,3 +146,16 @@ def test_describe_reports_a_launchable_configuration(L):
     assert L.marlin_describe(1, 4096, 4096, 128, None, 0) == 1
     assert L.marlin_describe(1, 4096, 4000, 128, buf, len(buf)) == 2
     assert L.marlin_describe(1, 4096, 4096, 64, buf, len(buf)) == 3
+
+
+def test_override_selects_the_kernel(monkeypatch):
+    # MARLIN_FORCE_CONFIG is read at every call
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile")
+    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, false> cols=256 rg=1")
+    assert B.marlin_describe(128, 1024, 1024, -1).startswith("w4a16_tile_kernel<2, 2, true> cols=128 rg=1")
+    assert B.marlin_describe(16, 1024, 1024, 128).startswith("w4a16_stream_kernel<")  # tile kernel: M > 32 only
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
+    d = B.marlin_describe(128, 1024, 1024, 128)
+    assert d.startswith("w4a16_stream_kernel<") and "cols=32 rg=4 partition=streamk grid=7" in d, d
+    monkeypatch.delenv("MARLIN_FORCE_CONFIG")
+    assert "grid=7" not in B.marlin_describe(128, 1024, 1024, 128)

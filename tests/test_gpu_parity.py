@@ -117,6 +117,27 @@ def test_other_groups(mk, M, g):
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "g=%d M=%d" % (g, M))
 
 
+@pytest.fixture
+def force(monkeypatch):
+    """Set the library's configuration override for one test (read per call)."""
+    def set_(spec):
+        monkeypatch.setenv("MARLIN_FORCE_CONFIG", spec)
+    return set_
+
+
+@pytest.mark.parametrize("spec", ["kind=tile", "kind=tile,whole=1", "kind=tile,whole=0,grid=7",
+                                  "kind=tile,whole=0,grid=96", "kind=stream", "kind=stream,whole=0,grid=7"])
+@pytest.mark.parametrize("M", [33, 64, 65, 100, 128])
+@pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
+def test_each_kernel_and_partition(mk, force, spec, M, K, N, g):
+    # Both kernels serve M > 32; each, under each partition (whole tiles, and
+    # Stream-K splits with several contributors per tile), against the oracle.
+    force(spec)
+    q, s = synth.weights(6, K, N, None if g == -1 else g)
+    A = synth.activations(6, M, K)
+    check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
+
+
 @pytest.mark.parametrize("M", [130, 200, 256])
 def test_M_above_128_runs_in_passes(mk, M):
     K, N = 1024, 512
