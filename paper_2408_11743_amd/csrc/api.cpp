@@ -108,12 +108,13 @@ static ForcedConfig forced() { return read_forced(); }
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
 namespace {
-// Tile kernel: time of one 128-row block of a tile, by rows per tile (64:
-// 4x1 waves, 128: 2x2), and the cost of combining its 64 KiB fp32 tiles
-// (fixed part, and per contributor: the reducer reads one slot per
-// contributor), fitted to MI355X measurements.
-constexpr double kTileUnitUs[2] = {1.50, 1.55};
-constexpr double kTileTailUs = 10.4, kTileTailPerContributorUs = 1.36;
+// Tile kernel: time of one 128-row block of a tile, and the cost of
+// combining shared tiles (fixed part, and per contributor: the reducer reads
+// one fp32 slot per contributor), fitted to MI355X measurements.
+struct TileCost {
+    double unit_us, tail_us, tail_per_contributor_us;
+};
+TileCost tile_cost(int wm) { return {wm == 2 ? 1.55 : 1.50, 10.4, 1.36}; }  // 64 KiB slots
 // Stream kernel: the combination costs 2.5 us + 0.5 us per contributor.
 constexpr double kStreamTailUs = 2.5, kStreamTailPerContributorUs = 0.5;
 
@@ -205,20 +206,25 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
             }
         }
     }
-    // tile kernel (M > 32): 2x2 waves for more than 64 rows, else 4x1
+    // tile kernel (M > 32): the activation tile is shared by the four waves,
+    // each of which owns 64 x 64 outputs (2x2 waves beyond 64 rows, else 4x1).
     if (M > 32 && forced().kind != kKindStream) {
         const int wm = M > 64 ? 2 : 1;
-        const int cols = 64 * (4 / wm), rows = 64 * wm;
-        if (N % cols == 0) {
+        const int mbw = M > 32 ? 4 : M > 16 ? 2 : 1;
+        for (int nbw = 4; nbw >= 1; nbw >>= 1) {
+            if (!tile_config_supported(wm, mbw, nbw)) continue;
+            if (forced().nb && nbw != forced().nb) continue;
+            const int cols = (4 / wm) * 16 * nbw, rows = wm * 16 * mbw;
+            if (N % cols != 0) continue;
             const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
-            const Partition pt = best_partition(tiles, KU, grid, kTileUnitUs[wm - 1], kTileTailUs,
-                                                kTileTailPerContributorUs);
-            if (pt.t < best || forced().kind == kKindTile) {
+            const TileCost tc = tile_cost(wm);
+            const Partition pt = best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us);
+            if (pt.t < best) {
                 best = pt.t;
                 cfg.kind = kKindTile;
                 cfg.tile_wm = wm;
-                cfg.nb = 4;
-                cfg.mb = 4;
+                cfg.nb = nbw;
+                cfg.mb = mbw;
                 cfg.ar = 0;
                 cfg.rg = (M + rows - 1) / rows;
                 cfg.whole = pt.whole;
@@ -374,8 +380,7 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
         p.G = (int)G;
         p.KU = (int)(K / 128);
         p.rg = cfg.rg;
-        const int tile_cols = (cfg.kind == kKindTile) ? 64 * (4 / cfg.tile_wm) : 16 * cfg.nb;
-        p.units = (int)(N / tile_cols) * cfg.rg * p.KU;
+        p.units = (int)(N / tile_cols(cfg)) * cfg.rg * p.KU;
         p.gran = cfg.whole ? p.KU : 1;
         p.per_wg = (p.units / p.gran) / cfg.grid;
         p.extra = (p.units / p.gran) % cfg.grid;
@@ -412,7 +417,7 @@ marlin_status_t marlin_describe(int64_t M, int64_t N, int64_t K, int64_t group, 
     kernel_name(cfg, gu == 0, name, sizeof(name));
     if (buf_bytes > 0)
         snprintf(buf, buf_bytes, "%s cols=%d rg=%d partition=%s grid=%d", name,
-                 cfg.kind == kKindTile ? 64 * (4 / cfg.tile_wm) : 16 * cfg.nb, cfg.rg,
+                 tile_cols(cfg), cfg.rg,
                  cfg.whole ? "whole" : "streamk", cfg.grid);
     return MARLIN_OK;
 }

@@ -482,7 +482,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
 
 int slot_floats(const GemmConfig &cfg)
 {
-    return cfg.kind == kKindTile ? 4 * 16 * 256 : cfg.nb * cfg.mb * 256;
+    return cfg.kind == kKindTile ? 4 * cfg.nb * cfg.mb * 256 : cfg.nb * cfg.mb * 256;
 }
 
 // Ring depth: stages in flight per wave (weights in registers: NB words of

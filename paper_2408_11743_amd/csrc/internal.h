@@ -19,7 +19,7 @@ constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
 constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
 constexpr int kKindStream = 0;  // w4a16_stream_kernel (any M; row groups of 32)
-constexpr int kKindTile = 1;    // w4a16_tile_kernel (M > 32; 64x64 tile per wave)
+constexpr int kKindTile = 1;    // w4a16_tile_kernel (activation tile shared by the waves)
 
 struct GemmConfig {
     int kind;
@@ -29,8 +29,13 @@ struct GemmConfig {
     int rg;
     int whole;
     int grid;
-    int tile_wm;  // tile kernel: waves along M (1: 4x1 waves, 256 x 64; 2: 2x2 waves, 128 x 128)
+    int tile_wm;  // tile kernel: waves along M (1: 4x1 waves; 2: 2x2 waves); mb, nb: row and
+                  // column blocks per wave
 };
+
+// Columns and rows of one tile of a configuration.
+inline int tile_cols(const GemmConfig &c) { return c.kind == kKindTile ? (4 / c.tile_wm) * 16 * c.nb : 16 * c.nb; }
+inline int tile_rows(const GemmConfig &c) { return c.kind == kKindTile ? c.tile_wm * 16 * c.mb : 16 * c.mb; }
 
 struct GemmProblem {
     const uint16_t *A;
@@ -72,6 +77,7 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
+bool tile_config_supported(int wm, int mbw, int nbw);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

@@ -67,24 +67,56 @@ __device__ __forceinline__ half8_t dequant_magic(uint32_t x, const DequantConsts
     return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
 }
 
-template <int WN, int WM, bool PER_CHANNEL>
+// Ring depth: stages that fit in LDS (activation rows, then each wave's
+// weights), capped so that the loads of the stages in flight stay within the
+// vmcnt range.
+template <int WN, int WM, int MBW, int NBW>
+struct TileShape {
+    static constexpr int TR = 16 * MBW * WM;             // rows of A per tile
+    static constexpr int kAStage = TR * 256;             // bytes of one A stage (TR rows x 128 k x 2 B)
+    static constexpr int kDma = TR / 16;                 // 1-KiB direct-to-LDS A loads per wave per stage
+    static constexpr int kWStage = 4 * NBW * 1024;       // every wave's weights for one stage
+    static constexpr int kStage = kAStage + kWStage;
+    static constexpr int kScratch = (kDma + NBW) * 1024;  // target of the loads issued past the end
+    static constexpr int kSL = NBW == 4 ? 2 : 1;          // scale loads per wave per stage
+    static constexpr int kLoads = kDma + NBW + kSL;       // vector-memory ops per wave per stage
+    static constexpr int kLdsBudget = 160 * 1024 - 64;
+    static constexpr int kByLds = (kLdsBudget - kScratch) / kStage;
+    static constexpr int kByVm = (63 - kSL) / kLoads + 2;  // kSL + (P - 2) * kLoads <= 63
+    static constexpr int kCap = 12;
+    static constexpr int P = kByLds < kByVm ? (kByLds < kCap ? kByLds : kCap) : (kByVm < kCap ? kByVm : kCap);
+    static_assert(P >= 3, "ring too shallow");
+};
+
+// This lane's column scales of one stage: NBW column blocks x 4 values
+// (element 4b + i: block b, output column 4 * (lane / 16) + i of the block).
+template <int NBW>
+struct ScaleFrag {
+    half8_t v[2];
+    __device__ __forceinline__ _Float16 at(int e) const { return v[e >> 3][e & 7]; }
+};
+template <>
+struct ScaleFrag<1> {
+    half4_t v;
+    __device__ __forceinline__ _Float16 at(int e) const { return v[e & 3]; }
+};
+
+template <int WN, int WM, int MBW, int NBW, bool PER_CHANNEL>
 __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 {
     static_assert(WN * WM == 4, "four waves");
-    constexpr int P = 3;                   // stages in flight (LDS ring of A, register ring of W)
-    constexpr int TR = 64 * WM;            // rows of A per tile
-    constexpr int kAStage = TR * 256;      // bytes of one A stage (TR rows x 128 k x 2 B)
-    constexpr int kDma = TR / 16;          // 1-KiB direct-to-LDS loads per wave per stage
-    // Scale loads per wave per stage: the stage's 64 group scales, or (per
-    // channel) the tile's 64 column scales, so that the epilogue of a tile
-    // finds them in registers instead of draining the load pipeline.
-    constexpr int kSL = 2;
-    constexpr int kStage = kAStage + 4 * 4096;  // A tile, then each wave's 4 KiB of weights
-    constexpr int kLoads = kDma + 4 + kSL;  // vector-memory ops per wave per stage
-    constexpr int kBlocks = 16;            // 16x16 output blocks per wave (4 column x 4 row blocks)
-    static_assert(kLoads + kSL < 64, "vmcnt range");
-    // ring of stages, then a scratch area for the loads issued past the end
-    __shared__ __attribute__((aligned(16))) uint8_t a_lds[P * kStage + (kDma + 4) * 1024];
+    static_assert(NBW == 1 || NBW == 2 || NBW == 4, "column blocks per wave");
+    static_assert(MBW >= 1 && MBW <= 4, "row blocks per wave");
+    using S = TileShape<WN, WM, MBW, NBW>;
+    constexpr int P = S::P;
+    constexpr int TR = S::TR;
+    constexpr int kAStage = S::kAStage;
+    constexpr int kDma = S::kDma;
+    constexpr int kStage = S::kStage;
+    constexpr int kSL = S::kSL;
+    constexpr int kLoads = S::kLoads;
+    constexpr int kBlocks = NBW * MBW;  // 16x16 output blocks per wave
+    __shared__ __attribute__((aligned(16))) uint8_t a_lds[P * kStage + S::kScratch];
     __shared__ int flags[2];
 
     const int lane = threadIdx.x & 63;
@@ -103,7 +135,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     const int k1 = u1 - c_last * KU;
     const int n_st = u1 - u0;  // one 128-row block per stage
 
-    // Tile c: column group c / rg (64*WN columns), row group c % rg (TR rows).
+    // Tile c: column group c / rg (16*NBW*WN columns), row group c % rg (TR rows).
     const uint32_t RG = (uint32_t)p.rg;
     auto cg_of = [&](int c) -> uint32_t { return RG == 1 ? (uint32_t)c : (uint32_t)c / RG; };
     auto row0_of = [&](int c) -> int { return RG == 1 ? 0 : (int)((uint32_t)c - cg_of(c) * RG) * TR; };
@@ -111,8 +143,17 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
         const int r = p.M - row0_of(c);
         return r < TR ? r : TR;
     };
-    // this wave's 64-column tile index in the packed layout
-    auto c64_of = [&](int c) -> uint32_t { return cg_of(c) * WN + (uint32_t)wn; };
+    // this wave's first 16-column block; its NBW blocks lie in one 64-column
+    // tile of the packed layout
+    auto nbg_of = [&](int c) -> uint32_t { return (cg_of(c) * WN + (uint32_t)wn) * NBW; };
+    auto w_tile = [&](int c) -> uint32_t {
+        const uint32_t nbg = nbg_of(c);
+        return ((nbg >> 2) * (uint32_t)KU * 4u + (nbg & 3u)) << 10;
+    };
+    auto s_tile = [&](int c) -> uint32_t {
+        const uint32_t nbg = nbg_of(c);
+        return (((nbg >> 2) * (uint32_t)p.G) << 7) + (nbg & 3u) * 8u;
+    };
 
     // Per-lane address parts.
     const uint32_t w_lane = (uint32_t)lane * 16u;
@@ -124,33 +165,31 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
         a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u;
     }
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
-    uint32_t a_rd[P][4];  // row wm*64 + (lane & 15) (+ 16 mb via the offset field), chunk 4t + lg
-    uint32_t w_rd[P];     // this wave's weights, this lane's 16 bytes (+ 1 KiB per column block)
+    // row wm*16*MBW + (lane & 15) (+ 16 mb via the offset field), chunk 4t + lg
+    uint32_t a_rd[4];
 #pragma unroll
-    for (int j = 0; j < P; ++j) {
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-            a_rd[j][t] = lds0 + (uint32_t)(j * kStage + (wm * 64 + (lane & 15)) * 256 +
-                                           (((4 * t + lg) ^ (lane & 15)) << 4));
-        w_rd[j] = lds0 + (uint32_t)(j * kStage + kAStage + wave * 4096 + lane * 16);
-    }
+    for (int t = 0; t < 4; ++t)
+        a_rd[t] = lds0 + (uint32_t)((wm * 16 * MBW + (lane & 15)) * 256 + (((4 * t + lg) ^ (lane & 15)) << 4));
+    // this wave's weights, this lane's 16 bytes (+ 1 KiB per column block)
+    const uint32_t w_rd = lds0 + (uint32_t)(kAStage + wave * NBW * 1024 + lane * 16);
     const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
-    half8_t sr[P][2];
+    ScaleFrag<NBW> sr[P];
 
     // ---- load cursor: one 128-row block per stage ----
     int ld_c = c_first, ld_ku = k0;
     int ld_end = (c_first == c_last) ? k1 : KU;
-    uint32_t ld_w = (c64_of(ld_c) * (uint32_t)KU + (uint32_t)ld_ku) << 12;
-    uint32_t ld_s = (c64_of(ld_c) * (uint32_t)p.G) << 7;
+    uint32_t ld_w = w_tile(ld_c) + ((uint32_t)ld_ku << 12);
+    uint32_t ld_s = s_tile(ld_c);
     const uint16_t *ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
     uint32_t a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
 
     auto issue = [&](int j) {
         const bool on = ld_ku < ld_end;
-        // Activation rows first (oldest loads of the stage).  Past the end they
-        // go to the scratch area: other waves may still read every ring slot.
+        // Activation rows first (oldest loads of the stage), then this wave's
+        // weights, then its scales.  Past the end the direct-to-LDS loads go
+        // to the scratch area: other waves may still read every ring slot.
         const __amdgpu_buffer_rsrc_t ra =
             __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, on ? a_bytes : 0u, kBufferFlags);
         uint8_t *dst = on ? a_lds + j * kStage + wave * (kAStage / 4) : a_lds + P * kStage;
@@ -160,18 +199,20 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
                                                      16, (int)a_dma[i], ld_ku * 256, 0, 0);
         const __amdgpu_buffer_rsrc_t rw =
             __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
-        uint8_t *wdst = on ? a_lds + j * kStage + kAStage + wave * 4096 : a_lds + P * kStage + kDma * 1024;
+        uint8_t *wdst = on ? a_lds + j * kStage + kAStage + wave * NBW * 1024 : a_lds + P * kStage + kDma * 1024;
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < NBW; ++b)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wdst + b * 1024),
                                                      16, (int)(w_lane + b * 1024), (int)ld_w, 0, kAuxNonTemporal);
-        {
-            const __amdgpu_buffer_rsrc_t rs =
-                __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
-            const uint32_t s_off = PER_CHANNEL ? ld_s : ld_s + ((uint32_t)scale_row_of(ld_ku, p) << 7);
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
+        const uint32_t s_off = PER_CHANNEL ? ld_s : ld_s + ((uint32_t)scale_row_of(ld_ku, p) << 7);
+        if constexpr (NBW == 1) {
+            sr[j].v = __builtin_bit_cast(half4_t, __builtin_amdgcn_raw_buffer_load_b64(rs, s_lane, s_off, 0));
+        } else {
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                sr[j][i] = __builtin_bit_cast(
+            for (int i = 0; i < NBW / 2; ++i)
+                sr[j].v[i] = __builtin_bit_cast(
                     half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
         }
     };
@@ -182,8 +223,8 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
             ld_c += 1;
             ld_ku = 0;
             ld_end = (ld_c < c_last) ? KU : (ld_c == c_last) ? k1 : 0;  // 0: past the range
-            ld_w = (c64_of(ld_c) * (uint32_t)KU) << 12;
-            ld_s = (c64_of(ld_c) * (uint32_t)p.G) << 7;
+            ld_w = w_tile(ld_c);
+            ld_s = s_tile(ld_c);
             if (ld_end > 0) {
                 ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
                 a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
@@ -197,83 +238,82 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
         advance_ld();
     }
 
-    float4_t acc[4][4];  // [column block][row block]
+    float4_t acc[NBW][MBW];  // [column block][row block]
     const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+    for (int b = 0; b < NBW; ++b)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb) acc[b][mb] = zero4;
+        for (int mb = 0; mb < MBW; ++mb) acc[b][mb] = zero4;
 
-    // One stage (ring slot j): the wave's 16 output blocks, column block
-    // outer: each dequantized word feeds the four row blocks.
+    // One stage (ring slot j): column block outer, so each dequantized word
+    // feeds the MBW row blocks.
     auto compute = [&](int j) {
-        u32x4_t wv[4];    // [column block] this lane's packed weights
-        u32x4_t v[4][4];  // [row block][k-step] activation operands
-        asm volatile("ds_read_b128 %0, %1" : "=v"(wv[0]) : "v"(w_rd[j]));
-        asm volatile("ds_read_b128 %0, %1 offset:1024" : "=v"(wv[1]) : "v"(w_rd[j]));
-        asm volatile("ds_read_b128 %0, %1 offset:2048" : "=v"(wv[2]) : "v"(w_rd[j]));
-        asm volatile("ds_read_b128 %0, %1 offset:3072" : "=v"(wv[3]) : "v"(w_rd[j]));
+        u32x4_t wv[NBW];     // [column block] this lane's packed weights
+        u32x4_t v[MBW][4];   // [row block][k-step] activation operands
+        const uint32_t wj = w_rd + j * kStage;
+#pragma unroll
+        for (int b = 0; b < NBW; ++b) asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(wv[b]) : "v"(wj), "i"(b * 1024));
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            asm volatile("ds_read_b128 %0, %1" : "=v"(v[0][t]) : "v"(a_rd[j][t]));
-            asm volatile("ds_read_b128 %0, %1 offset:4096" : "=v"(v[1][t]) : "v"(a_rd[j][t]));
-            asm volatile("ds_read_b128 %0, %1 offset:8192" : "=v"(v[2][t]) : "v"(a_rd[j][t]));
-            asm volatile("ds_read_b128 %0, %1 offset:12288" : "=v"(v[3][t]) : "v"(a_rd[j][t]));
+            const uint32_t aj = a_rd[t] + j * kStage;
+#pragma unroll
+            for (int mb = 0; mb < MBW; ++mb)
+                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v[mb][t]) : "v"(aj), "i"(mb * 4096));
         }
         // The wait "redefines" the results: no use is scheduled before it.
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[0][2]), "+v"(v[0][3]), "+v"(v[1][0]), "+v"(v[1][1]),
-                       "+v"(v[1][2]), "+v"(v[1][3]), "+v"(v[2][0]), "+v"(v[2][1]), "+v"(v[2][2]), "+v"(v[2][3]),
-                       "+v"(v[3][0]), "+v"(v[3][1]), "+v"(v[3][2]), "+v"(v[3][3]), "+v"(wv[0]), "+v"(wv[1]),
-                       "+v"(wv[2]), "+v"(wv[3])::"memory");
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < NBW; ++b) asm volatile("" : "+v"(wv[b]));
+#pragma unroll
+        for (int mb = 0; mb < MBW; ++mb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) asm volatile("" : "+v"(v[mb][t]));
+#pragma unroll
+        for (int b = 0; b < NBW; ++b) {
             if constexpr (PER_CHANNEL) {
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const half8_t w = dequant_magic(wv[b][t], dq);
 #pragma unroll
-                    for (int mb = 0; mb < 4; ++mb)
+                    for (int mb = 0; mb < MBW; ++mb)
                         acc[b][mb] = mfma(w, __builtin_bit_cast(half8_t, v[mb][t]), acc[b][mb]);
                 }
             } else {
-                float4_t tmp[4];
+                float4_t tmp[MBW];
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const half8_t w = dequant_magic(wv[b][t], dq);
 #pragma unroll
-                    for (int mb = 0; mb < 4; ++mb)
+                    for (int mb = 0; mb < MBW; ++mb)
                         tmp[mb] = mfma(w, __builtin_bit_cast(half8_t, v[mb][t]), t == 0 ? zero4 : tmp[mb]);
                 }
-                const half8_t sv = sr[j][b >> 1];
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb)
+                for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        acc[b][mb][i] = __builtin_fmaf(tmp[mb][i], (float)sv[(b & 1) * 4 + i], acc[b][mb][i]);
+                        acc[b][mb][i] = __builtin_fmaf(tmp[mb][i], (float)sr[j].at(b * 4 + i), acc[b][mb][i]);
             }
         }
     };
 
-    // block j of this wave = column block j / 4, row block j % 4; slot index wave*16 + j
+    // block j of this wave = column block j / MBW, row block j % MBW; slot index wave*kBlocks + j
     auto own = [&](int j) { return wave * kBlocks + j; };
-    // Tile c's C from full sums; per-channel scales: this lane's 16 column
-    // scales (column block b, value i at element 4b + i).
-    auto store_c_scaled = [&](int c, const float4_t *out, const half8_t (&cs)[2]) {
-        const int r0 = row0_of(c) + wm * 64, rows = rows_of(c) - wm * 64;
-        const uint32_t c64 = c64_of(c);
+    // Tile c's C from full sums (per-channel scales from cs).
+    auto store_c_scaled = [&](int c, const float4_t *out, const ScaleFrag<NBW> &cs) {
+        const int r0 = row0_of(c) + wm * 16 * MBW, rows = rows_of(c) - wm * 16 * MBW;
+        const uint32_t col0 = nbg_of(c) * 16u;
 #pragma unroll
         for (int j = 0; j < kBlocks; ++j) {
-            const int b = j / 4, mb = j % 4;
+            const int b = j / MBW, mb = j % MBW;
             const int m = mb * 16 + (lane & 15);
             if (m < rows) {
                 float4_t vv = out[j];
                 if constexpr (PER_CHANNEL) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) vv[i] *= (float)cs[b >> 1][(b & 1) * 4 + i];
+                    for (int i = 0; i < 4; ++i) vv[i] *= (float)cs.at(b * 4 + i);
                 }
                 const half4_t h = {(_Float16)vv[0], (_Float16)vv[1], (_Float16)vv[2], (_Float16)vv[3]};
-                *(half4_t *)(p.C + (int64_t)(r0 + m) * p.N + c64 * 64 + b * 16 + lg * 4) = h;
+                *(half4_t *)(p.C + (int64_t)(r0 + m) * p.N + col0 + b * 16 + lg * 4) = h;
             }
         }
     };
@@ -296,8 +336,8 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
         float4_t out[kBlocks];
 #pragma unroll
         for (int j = 0; j < kBlocks; ++j) {
-            out[j] = acc[j / 4][j % 4];
-            acc[j / 4][j % 4] = zero4;
+            out[j] = acc[j / MBW][j % MBW];
+            acc[j / MBW][j % MBW] = zero4;
         }
         if (partial) {
             has_first = true;
@@ -312,11 +352,10 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     // issued after them: the stage's scales and the P - 2 stages issued later;
     // vector-memory operations complete in order), meet at the barrier (now
     // the whole stage is in LDS, and every wave is done with the slot of stage
-    // st - 1), refill that slot with stage st + P - 1, compute.
-    // Loads are issued unconditionally (past the range into the scratch
-    // area, through empty descriptors) so that every stage has the same load
-    // pattern and the compiler's own vmcnt waits (for the scale registers)
-    // stay static.
+    // st - 1), refill that slot with stage st + P - 1, compute.  Loads are
+    // issued unconditionally (past the range into the scratch area, through
+    // empty descriptors) so that every stage has the same load pattern and the
+    // compiler's own vmcnt waits (for the scale registers) stay static.
     constexpr int kAfter = kSL + (P - 2) * kLoads;
     for (int st0 = 0; st0 < n_st; st0 += P) {
 #pragma unroll
@@ -346,16 +385,20 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 
     float4_t last_out[kBlocks];
 #pragma unroll
-    for (int j = 0; j < kBlocks; ++j) last_out[j] = acc[j / 4][j % 4];
+    for (int j = 0; j < kBlocks; ++j) last_out[j] = acc[j / MBW][j % MBW];
     auto own_slot = [&](int j) { return own(j); };
     // After the loop nothing is in flight to wait behind: load the column
     // scales directly.
     auto store_c = [&](int c, const float4_t *out) {
-        half8_t cs[2] = {};
+        ScaleFrag<NBW> cs{};
         if constexpr (PER_CHANNEL) {
-            const half8_t *src = (const half8_t *)(p.S + (int64_t)c64_of(c) * 64 + lg * 16);
-            cs[0] = src[0];
-            cs[1] = src[1];
+            const _Float16 *src = (const _Float16 *)p.S + (int64_t)(nbg_of(c) >> 2) * 64 + lg * 16 + (nbg_of(c) & 3u) * 4;
+            if constexpr (NBW == 1) {
+                cs.v = *(const half4_t *)src;
+            } else {
+#pragma unroll
+                for (int i = 0; i < NBW / 2; ++i) cs.v[i] = *(const half8_t *)(src + 8 * i);
+            }
         }
         store_c_scaled(c, out, cs);
     };
@@ -365,26 +408,38 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 
 }  // namespace
 
-template <int WN, int WM>
+template <int WN, int WM, int MBW, int NBW>
 hipError_t launch_tile(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     GemmProblem arg = p;
     void *args[] = {&arg};
-    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_tile_kernel<WN, WM, true>
-                                          : (const void *)&w4a16_tile_kernel<WN, WM, false>;
+    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, true>
+                                          : (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, false>;
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(256), args, 0, stream);
 }
 
+// Instantiated shapes: 64 x 64 outputs per wave, 4x1 or 2x2 waves.  (Tiles
+// of 16 or 32 rows per wave compile from the same template, but with one
+// 128-row block of K per work-group stage their fixed per-stage cost keeps
+// them behind the stream kernel at every measured shape.)
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    if (cfg.tile_wm == 1) return launch_tile<4, 1>(cfg, p, stream);
-    if (cfg.tile_wm == 2) return launch_tile<2, 2>(cfg, p, stream);
-    return hipErrorInvalidValue;
+    switch (cfg.tile_wm * 100 + cfg.mb * 10 + cfg.nb) {
+    case 144: return launch_tile<4, 1, 4, 4>(cfg, p, stream);
+    case 244: return launch_tile<2, 2, 4, 4>(cfg, p, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+bool tile_config_supported(int wm, int mbw, int nbw)
+{
+    return mbw == 4 && nbw == 4 && (wm == 1 || wm == 2);
 }
 
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 {
-    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %s>", 4 / cfg.tile_wm, cfg.tile_wm, per_channel ? "true" : "false");
+    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %d, %d, %s>", 4 / cfg.tile_wm, cfg.tile_wm, cfg.mb, cfg.nb,
+             per_channel ? "true" : "false");
 }
 
 }  // namespace marlin

@@ -131,12 +131,18 @@ def test_describe_reports_a_launchable_configuration(L):
                        (128, 28672, 8192, 128), (200, 1024, 1024, 256)]:
         assert L.marlin_describe(M, N, K, g, buf, len(buf)) == 0
         text = buf.value.decode()
-        assert text.startswith("w4a16_stream_kernel<") or (M > 32 and text.startswith("w4a16_tile_kernel<")), text
+        assert text.startswith("w4a16_stream_kernel<") or text.startswith("w4a16_tile_kernel<"), text
         assert ("true>" in text) == (g == -1 or g == K), text
         assert "partition=whole" in text or "partition=streamk" in text, text
         cols = int(text.split("cols=")[1].split()[0])
         assert cols in (16, 32, 64, 128, 256) and N % cols == 0, text
-        rows = 32 if text.startswith("w4a16_stream_kernel<") else 16384 // cols
+        if text.startswith("w4a16_stream_kernel<"):
+            rows = 32
+        else:  # w4a16_tile_kernel<waves along N, waves along M, row blocks, column blocks per wave, ...>
+            wn, wm, mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:4])
+            assert wn * wm == 4 and cols == wn * 16 * nbw, text
+            rows = wm * 16 * mbw
+            assert rows >= min(M, 128) or rows == 128, text
         assert int(text.split("rg=")[1].split()[0]) == -(-min(M, 128) // rows), text
         assert int(text.split("grid=")[1]) >= 1
     assert "rg=1" in B.marlin_describe(32, 4096, 4096, 128)
@@ -151,9 +157,11 @@ def test_describe_reports_a_launchable_configuration(L):
 def test_override_selects_the_kernel(monkeypatch):
     # MARLIN_FORCE_CONFIG is read at every call
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile")
-    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, false> cols=256 rg=1")
-    assert B.marlin_describe(128, 1024, 1024, -1).startswith("w4a16_tile_kernel<2, 2, true> cols=128 rg=1")
-    assert B.marlin_describe(16, 1024, 1024, 128).startswith("w4a16_stream_kernel<")  # tile kernel: M > 32 only
+    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 4, 4, false> cols=256 rg=1")
+    assert B.marlin_describe(128, 1024, 1024, -1).startswith("w4a16_tile_kernel<2, 2, 4, 4, true> cols=128 rg=1")
+    assert B.marlin_describe(16, 1024, 1024, 128).startswith("w4a16_stream_kernel<")  # tile kernel: M > 32
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1")  # no such tile shape: the stream kernel
+    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_stream_kernel<")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
     d = B.marlin_describe(128, 1024, 1024, 128)
     assert d.startswith("w4a16_stream_kernel<") and "cols=32 rg=4 partition=streamk grid=7" in d, d

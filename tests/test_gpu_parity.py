@@ -126,12 +126,14 @@ def force(monkeypatch):
 
 
 @pytest.mark.parametrize("spec", ["kind=tile", "kind=tile,whole=1", "kind=tile,whole=0,grid=7",
-                                  "kind=tile,whole=0,grid=96", "kind=stream", "kind=stream,whole=0,grid=7"])
-@pytest.mark.parametrize("M", [33, 64, 65, 100, 128])
+                                  "kind=tile,whole=0,grid=96", "kind=stream", "kind=stream,whole=0,grid=7",
+                                  "kind=stream,nb=1,whole=1"])
+@pytest.mark.parametrize("M", [1, 5, 16, 17, 32, 33, 64, 65, 100, 128])
 @pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
 def test_each_kernel_and_partition(mk, force, spec, M, K, N, g):
-    # Both kernels serve M > 32; each, under each partition (whole tiles, and
-    # Stream-K splits with several contributors per tile), against the oracle.
+    # Both kernels serve M > 32 (the stream kernel every M); each under each
+    # partition (whole tiles, and Stream-K splits with several contributors
+    # per tile), against the oracle.
     force(spec)
     q, s = synth.weights(6, K, N, None if g == -1 else g)
     A = synth.activations(6, M, K)
