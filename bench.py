@@ -64,11 +64,10 @@ def parse():
 def measured_traffic():
     """HBM bytes per launch from the committed counter summary, or None when
     the kernel source has changed since the counters were taken."""
-    import hashlib
+    from paper_2408_11743_amd.profile_summary import kernel_sources_digest
     try:
         rec = json.load(open(TRAFFIC_FILE))
-        src = os.path.join(ROOT, "paper_2408_11743_amd", "csrc", "gemm.hip")
-        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["gemm_hip_sha256"]:
+        if kernel_sources_digest() != rec["kernel_sources_sha256"]:
             return None
         return rec["step_avg_hbm_bytes_per_launch"]
     except (OSError, KeyError, ValueError):

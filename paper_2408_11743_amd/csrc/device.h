@@ -58,6 +58,19 @@ __device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)
     return (int)__umulhi((uint32_t)ku << 6, p.gmagic);
 }
 
+// Work-group index in the partition, arranged so that consecutive indices
+// run on one XCD: the dispatcher hands work-group b to XCD b mod 8, so XCD x
+// gets the indices [x*q + min(x, r), ...) for grid = 8q + r.  Consecutive
+// ranges then share an L2 (the row groups of one column tile read the same
+// weights, from one L2).
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_local_wg(int b, int grid)
+{
+    const int q = grid / kXcds, r = grid % kXcds;
+    const int x = b % kXcds;
+    return x * q + (x < r ? x : r) + b / kXcds;
+}
+
 // First unit of work-group w: gran * floor(w * (units / gran) / grid), from
 // the host's quotient and remainder so that no 64-bit division is needed.
 // gran = KU hands out whole tiles; gran = 1 splits tiles (Stream-K).

@@ -126,7 +126,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     const DequantConsts dq = dequant_consts();
     const int KU = p.KU;
     const int grid = gridDim.x;
-    const int wg = blockIdx.x;
+    const int wg = xcd_local_wg(blockIdx.x, grid);
     const int u0 = range_start(p, wg, grid);
     const int u1 = range_start(p, wg + 1, grid);
     const int c_first = (int)((uint32_t)u0 / (uint32_t)KU);

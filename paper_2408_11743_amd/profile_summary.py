@@ -26,8 +26,18 @@ import os
 import statistics
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-GEMM_SRC = os.path.join(HERE, "csrc", "gemm.hip")
+# Device sources the GEMM kernels are built from: a counter summary holds
+# for the kernels only while these are unchanged.
+KERNEL_SOURCES = ("gemm.hip", "tile.hip", "device.h", "internal.h")
 COPY_KERNEL = "copyBuffer"
+
+
+def kernel_sources_digest() -> str:
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(name.encode())
+        h.update(open(os.path.join(HERE, "csrc", name), "rb").read())
+    return h.hexdigest()
 
 
 def _one(pattern: str) -> str:
@@ -166,13 +176,14 @@ def main() -> None:
           "|---|---|---|---|---|---|---|"]
     for M, k, fb, wb, tb, alg in trows:
         md.append("| %d | `%s` | %.2f | %.2f | %.2f | %.2f | %.2f |" % (M, k, fb / 1e6, wb / 1e6, tb / 1e6, alg / 1e6, tb / alg))
-    digest = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+    digest = kernel_sources_digest()
     md += ["", "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N.", "",
            "Step average per launch: %.2f MB (bench.py reports it as `roofline.traffic`" % (step_bytes / len(Ms) / 1e6),
-           "while `paper_2408_11743_amd/csrc/gemm.hip` hashes to `%s...`)." % digest[:16], ""]
+           "while the kernel sources (%s under `paper_2408_11743_amd/csrc/`) hash to `%s...`)." %
+           (", ".join(KERNEL_SOURCES), digest[:16]), ""]
     open(a.out + "_traffic.md", "w").write("\n".join(md) + "\n")
     rec = {"workload": "W4A16 GEMM K=%d N=%d g=%d, M sweep %s (bench.py)" % (K, N, g, Ms),
-           "gemm_hip_sha256": digest,
+           "kernel_sources_sha256": digest,
            "counter_scale": {"FETCH_SIZE": round(f_scale, 4), "WRITE_SIZE": round(w_scale, 4),
                              "calibration": "device copies of %d MiB" % a.copy_mb},
            "hbm_bytes_per_launch": hbm, "step_launches": Ms,

@@ -138,3 +138,21 @@ def test_scale_row_magic_exact():
         m = ((1 << 26) + gu - 1) // gu
         for ku in list(range(0, 300)) + list(range(8192 - 300, 8192)):
             assert ((ku << 6) * m) >> 32 == ku // gu, (gu, ku)
+
+
+def xcd_local_wg(b, grid, xcds=8):
+    q, r = divmod(grid, xcds)
+    x = b % xcds
+    return x * q + min(x, r) + b // xcds
+
+
+@pytest.mark.parametrize("grid", list(range(1, 40)) + [172, 224, 255, 256, 448, 512])
+def test_xcd_local_numbering_is_a_bijection_with_runs_per_xcd(grid):
+    # Work-group b runs on XCD b mod 8; its index in the partition is
+    # xcd_local_wg(b): a permutation of 0..grid-1 under which each XCD holds
+    # one run of consecutive indices.
+    ids = [xcd_local_wg(b, grid) for b in range(grid)]
+    assert sorted(ids) == list(range(grid))
+    for x in range(8):
+        run = [xcd_local_wg(b, grid) for b in range(x, grid, 8)]
+        assert run == list(range(run[0], run[0] + len(run))) if run else True
