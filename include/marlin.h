@@ -174,6 +174,76 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
 marlin_status_t marlin_describe(int64_t M, int64_t N, int64_t K, int64_t group,
                                 char *buf, size_t buf_bytes);
 
+/*
+ * ---- 2:4 sparse weights (Section 4, "Sparse-MARLIN") ----
+ *
+ * The weight matrix is 2:4 sparse along K: in every group of 4 consecutive
+ * rows of a column at most two weights are non-zero.  It is given as the
+ * dense code matrix q [K][N] of marlin_pack_weights with the pruned
+ * positions holding code 8 (weight s * (8 - 8) = 0), so the product is the
+ * dense definition C = A * (s * (q - 8)) on that matrix.  The packed form
+ * keeps two codes per group plus their 2-bit row indices, 3/8 byte per
+ * weight instead of 1/2, and feeds v_smfmac_f32_16x16x64_f16.
+ */
+
+/* Bytes of the packed sparse weights: 3*K*N/8 (0 for an invalid shape). */
+size_t marlin_packed_sparse_weight_bytes(int64_t K, int64_t N);
+
+/*
+ * marlin_pack_sparse_weights - codes and scales -> the sparse packed layout.
+ *
+ *   q, s, K, N, group, s_packed, stream: as for marlin_pack_weights (s_packed
+ *              has the same layout and size).
+ *   w_packed   device, marlin_packed_sparse_weight_bytes(K, N) bytes, written.
+ *
+ * Kept rows: in each group of 4 rows of a column, the first two whose code
+ * is not 8; a group with fewer is completed with its lowest rows of code 8.
+ * So a matrix with at most two non-8 codes per group is represented
+ * exactly; codes after the second non-8 code of a group are dropped (such a
+ * matrix is not 2:4 sparse).
+ *
+ * Packed sparse layout (uint32 words; c = 64-column tile, ku = 128-row
+ * block, nb = 16-column block, l = lane 0..63, h = 0..1, g = 0..3, t = 0..1),
+ * unit (c, ku) at word (c*KU + ku)*768:
+ *   codes: word ((d >> 2)*64 + l)*4 + (d & 3), d = 2*nb + h, holds the kept
+ *     codes j = 2g + t of column n = 64c + 16nb + l%16 for the row groups
+ *     128ku + 64h + 16(l/16) + 4g .. + 3, code j in nibble (j >> 1) + 4(j & 1);
+ *   row indices: word 512 + l*4 + nb holds at bits 16h + 4g + 2t the row
+ *     (0..3, increasing in t) of kept code 2g + t within its group.
+ *
+ * Errors: as marlin_pack_weights.
+ */
+marlin_status_t marlin_pack_sparse_weights(const uint8_t *q, const uint16_t *s,
+                                           int64_t K, int64_t N, int64_t group,
+                                           void *w_packed, void *s_packed,
+                                           hipStream_t stream);
+
+/*
+ * marlin_unpack_sparse_weights - inverse of marlin_pack_sparse_weights: q
+ * receives the dense codes (code 8 at the rows not kept), s the scales.
+ * pack followed by unpack is exact for codes with at most two non-8 codes
+ * per group of 4 rows.  Errors: as marlin_unpack_weights.
+ */
+marlin_status_t marlin_unpack_sparse_weights(const void *w_packed, const void *s_packed,
+                                             int64_t K, int64_t N, int64_t group,
+                                             uint8_t *q, uint16_t *s, hipStream_t stream);
+
+/*
+ * marlin_gemm_sparse - C = A * dequant(W) for 2:4 sparse packed weights
+ * (Section 4).  Arguments, workspace rules (marlin_workspace_bytes covers
+ * both entry points), accumulation, errors and reproducibility: as
+ * marlin_gemm, with w_packed in the sparse layout.
+ */
+marlin_status_t marlin_gemm_sparse(const uint16_t *A, const void *w_packed,
+                                   const void *s_packed, uint16_t *C,
+                                   void *workspace, size_t workspace_bytes,
+                                   int64_t M, int64_t N, int64_t K, int64_t group,
+                                   hipStream_t stream);
+
+/* marlin_describe_sparse - as marlin_describe, for marlin_gemm_sparse. */
+marlin_status_t marlin_describe_sparse(int64_t M, int64_t N, int64_t K, int64_t group,
+                                       char *buf, size_t buf_bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -73,3 +73,71 @@ def unpack_scales(sp: np.ndarray, K: int, N: int, group) -> np.ndarray:
                                   np.arange(4), np.arange(4), indexing="ij")
     out[r, 64 * c + 16 * nb + 4 * lg + i] = np.asarray(sp).reshape(C, G, 4, 4, 4)
     return out
+
+
+# ---- 2:4 sparse weights (Section 4) ----
+
+def sparse_selection(q: np.ndarray):
+    """Kept rows of every group of 4 consecutive k in each column.
+
+    Returns (pos, codes), each [K/4, 2, N]: the two kept rows (0..3,
+    increasing) and their codes.  Kept rows are the first two rows whose
+    code is not 8 (non-zero weight); a group with fewer is completed with
+    its lowest rows of code 8 (the documented packing rule)."""
+    K, N = q.shape
+    qg = (q & 0xF).reshape(K // 4, 4, N)
+    r = np.arange(4).reshape(1, 4, 1)
+    key = np.where(qg != 8, r, 4 + r)
+    first2 = np.argsort(key, axis=1, kind="stable")[:, :2, :]
+    pos = np.sort(first2, axis=1)
+    codes = np.take_along_axis(qg, pos, axis=1)
+    return pos.astype(np.uint32), codes.astype(np.uint32)
+
+
+def pack_sparse(q: np.ndarray) -> np.ndarray:
+    """uint8 codes [K, N] (2:4 along K: pruned positions hold code 8) -> uint32
+    words of the packed sparse layout (flat), 768 words per 64 x 128 unit."""
+    K, N = q.shape
+    assert K % 128 == 0 and N % 64 == 0
+    C, KU = N // 64, K // 128
+    pos, codes = sparse_selection(q)
+    out = np.zeros((C, KU, 768), dtype=np.uint32)
+    c, ku, nb, l, h = np.meshgrid(np.arange(C), np.arange(KU), np.arange(4), np.arange(64),
+                                  np.arange(2), indexing="ij")
+    n = 64 * c + 16 * nb + (l % 16)
+    grp0 = (128 * ku + 64 * h + 16 * (l // 16)) // 4
+    word = np.zeros(n.shape, dtype=np.uint32)
+    meta = np.zeros(n.shape, dtype=np.uint32)
+    for g in range(4):
+        for t in range(2):
+            j = 2 * g + t
+            word |= codes[grp0 + g, t, n] << np.uint32(4 * NIBBLE_OF[j])
+            meta |= pos[grp0 + g, t, n] << np.uint32(4 * g + 2 * t)
+    d = 2 * nb + h
+    out[c, ku, ((d >> 2) * 64 + l) * 4 + (d & 3)] = word
+    m2 = np.zeros((C, KU, 4, 64), dtype=np.uint32)
+    for hh in range(2):
+        m2 |= meta[..., hh] << np.uint32(16 * hh)
+    c2, ku2, nb2, l2 = np.meshgrid(np.arange(C), np.arange(KU), np.arange(4), np.arange(64), indexing="ij")
+    out[c2, ku2, 512 + l2 * 4 + nb2] = m2
+    return out.reshape(-1)
+
+
+def unpack_sparse(words: np.ndarray, K: int, N: int) -> np.ndarray:
+    """Inverse of pack_sparse: dense codes [K, N], code 8 at pruned rows."""
+    C, KU = N // 64, K // 128
+    w = np.asarray(words, dtype=np.uint32).reshape(C, KU, 768)
+    q = np.full((K, N), 8, dtype=np.uint8)
+    c, ku, nb, l, h = np.meshgrid(np.arange(C), np.arange(KU), np.arange(4), np.arange(64),
+                                  np.arange(2), indexing="ij")
+    n = 64 * c + 16 * nb + (l % 16)
+    d = 2 * nb + h
+    word = w[c, ku, ((d >> 2) * 64 + l) * 4 + (d & 3)]
+    meta = w[c, ku, 512 + l * 4 + nb] >> np.uint32(16 * h)
+    for g in range(4):
+        for t in range(2):
+            j = 2 * g + t
+            r = (meta >> np.uint32(4 * g + 2 * t)) & 3
+            k = 128 * ku + 64 * h + 16 * (l // 16) + 4 * g + r
+            q[k, n] = ((word >> np.uint32(4 * NIBBLE_OF[j])) & 0xF).astype(np.uint8)
+    return q

@@ -7,7 +7,7 @@ The compute runs in hand-written HIP kernels behind the C ABI of
 * ``marlin_*``   one function per C entry point, same names (``_binding``);
 * ``pack``, ``unpack``, ``gemm``, ``Workspace``: tensor helpers that
   allocate outputs with PyTorch and call the entry points on the current
-  stream (``ops``);
+  stream (``ops``; ``sparse=True`` selects the 2:4 sparse entry points);
 * ``roofline``:  byte / FLOP accounting and MI355X peaks used by the bench.
 
 Importing the package does not load the library; the first call does, and
@@ -18,12 +18,17 @@ from ._binding import (  # noqa: F401
     MarlinError,
     lib,
     marlin_describe,
+    marlin_describe_sparse,
     marlin_gemm,
+    marlin_gemm_sparse,
     marlin_layout_version,
+    marlin_pack_sparse_weights,
     marlin_pack_weights,
     marlin_packed_scale_bytes,
+    marlin_packed_sparse_weight_bytes,
     marlin_packed_weight_bytes,
     marlin_status_string,
+    marlin_unpack_sparse_weights,
     marlin_unpack_weights,
     marlin_workspace_bytes,
 )

@@ -38,6 +38,11 @@ SIGNATURES = {
     "marlin_unpack_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "marlin_gemm": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _vp]),
     "marlin_describe": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_char_p, _sz]),
+    "marlin_packed_sparse_weight_bytes": (_sz, [_i64, _i64]),
+    "marlin_pack_sparse_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
+    "marlin_unpack_sparse_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
+    "marlin_gemm_sparse": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _vp]),
+    "marlin_describe_sparse": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_char_p, _sz]),
 }
 
 
@@ -134,4 +139,32 @@ def marlin_describe(M: int, N: int, K: int, group: int) -> str:
     """Launch configuration marlin_gemm would use (kernel name and partition)."""
     buf = ctypes.create_string_buffer(256)
     _check("marlin_describe", lib().marlin_describe(M, N, K, group, buf, len(buf)))
+    return buf.value.decode()
+
+
+def marlin_packed_sparse_weight_bytes(K: int, N: int) -> int:
+    return lib().marlin_packed_sparse_weight_bytes(K, N)
+
+
+def marlin_pack_sparse_weights(q, s, K, N, group, w_packed, s_packed, stream=None) -> None:
+    _check("marlin_pack_sparse_weights", lib().marlin_pack_sparse_weights(
+        _ptr(q), _ptr(s), K, N, group, _ptr(w_packed), _ptr(s_packed), _stream(stream)))
+
+
+def marlin_unpack_sparse_weights(w_packed, s_packed, K, N, group, q, s, stream=None) -> None:
+    _check("marlin_unpack_sparse_weights", lib().marlin_unpack_sparse_weights(
+        _ptr(w_packed), _ptr(s_packed), K, N, group, _ptr(q), _ptr(s), _stream(stream)))
+
+
+def marlin_gemm_sparse(A, w_packed, s_packed, C, workspace, workspace_bytes, M, N, K, group,
+                       stream=None) -> None:
+    _check("marlin_gemm_sparse", lib().marlin_gemm_sparse(
+        _ptr(A), _ptr(w_packed), _ptr(s_packed), _ptr(C), _ptr(workspace), workspace_bytes,
+        M, N, K, group, _stream(stream)))
+
+
+def marlin_describe_sparse(M: int, N: int, K: int, group: int) -> str:
+    """Launch configuration marlin_gemm_sparse would use."""
+    buf = ctypes.create_string_buffer(256)
+    _check("marlin_describe_sparse", lib().marlin_describe_sparse(M, N, K, group, buf, len(buf)))
     return buf.value.decode()

@@ -168,7 +168,7 @@ Partition best_partition(int64_t tiles, int KU, int64_t grid, double unit_us, do
 }
 }  // namespace
 
-GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
+GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool sparse)
 {
     (void)group_units;
     GemmConfig cfg;
@@ -182,6 +182,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     // stream kernel
     cfg.kind = kKindStream;
     cfg.tile_wm = 0;
+    cfg.sparse = sparse ? 1 : 0;
     cfg.mb = (M <= 16) ? 1 : 2;
     cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
     cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32 (at most 4 per 128-row pass)
@@ -196,7 +197,9 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
             if (tiles16 % nb != 0 || rate <= 0.0) continue;
             if (forced().nb && nb != forced().nb) continue;
             const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
-            const Partition pt = best_partition(tiles, KU, grid, (double)nb * 1024.0 / rate, kStreamTailUs,
+            // sparse units carry 3/4 of the dense bytes (codes and row indices)
+            const double unit_bytes = (double)nb * (sparse ? 768.0 : 1024.0);
+            const Partition pt = best_partition(tiles, KU, grid, unit_bytes / rate, kStreamTailUs,
                                                 kStreamTailPerContributorUs);
             if (pt.t < best) {
                 best = pt.t;
@@ -208,7 +211,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
     }
     // tile kernel (M > 32): the activation tile is shared by the four waves,
     // each of which owns 64 x 64 outputs (2x2 waves beyond 64 rows, else 4x1).
-    if (M > 32 && forced().kind != kKindStream) {
+    if (M > 32 && !sparse && forced().kind != kKindStream) {
         const int wm = M > 64 ? 2 : 1;
         const int mbw = M > 32 ? 4 : M > 16 ? 2 : 1;
         for (int nbw = 4; nbw >= 1; nbw >>= 1) {
@@ -232,7 +235,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus)
             }
         }
     }
-    if (cfg.nb == 0) {  // only when an override excludes every choice
+    if (cfg.nb == 0) {  // only when an override excludes every choice (or asks for the tile kernel, sparse)
         cfg.kind = kKindStream;
         cfg.nb = (tiles16 % 2 == 0) ? 2 : 1;
         cfg.whole = 0;
@@ -258,15 +261,20 @@ size_t workspace_bytes_for(const GemmConfig &cfg, int N)
 }
 
 namespace {
-// Largest workspace over the passes of 128 rows that an M-row call makes.
+// Largest workspace over the passes of 128 rows that an M-row call makes,
+// dense or 2:4 sparse (one size serves both entry points).
 size_t required_workspace(int64_t M, int N, int K, int gu)
 {
     const int m_first = M < 128 ? (int)M : 128;
-    size_t need = workspace_bytes_for(choose_config(m_first, N, K, gu, kMaxCus), N);
     const int m_last = (int)(M % 128);
-    if (M > 128 && m_last != 0) {
-        const size_t b = workspace_bytes_for(choose_config(m_last, N, K, gu, kMaxCus), N);
+    size_t need = 0;
+    for (int sp = 0; sp < 2; ++sp) {
+        size_t b = workspace_bytes_for(choose_config(m_first, N, K, gu, kMaxCus, sp != 0), N);
         if (b > need) need = b;
+        if (M > 128 && m_last != 0) {
+            b = workspace_bytes_for(choose_config(m_last, N, K, gu, kMaxCus, sp != 0), N);
+            if (b > need) need = b;
+        }
     }
     return need;
 }
@@ -275,6 +283,90 @@ size_t required_workspace(int64_t M, int N, int K, int gu)
 }  // namespace marlin
 
 using namespace marlin;
+
+namespace {
+marlin_status_t gemm_impl(const uint16_t *A, const void *w_packed, const void *s_packed, uint16_t *C,
+                          void *workspace, size_t workspace_bytes, int64_t M, int64_t N, int64_t K,
+                          int64_t group, hipStream_t stream, bool sparse)
+{
+    if (M < 0 || M > (1 << 24)) return MARLIN_ERR_INVALID_SHAPE;
+    marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (M == 0) return MARLIN_OK;
+    if (!A || !w_packed || !s_packed || !C || !workspace) return MARLIN_ERR_NULL_POINTER;
+    if (!aligned16(A) || !aligned16(w_packed) || !aligned16(s_packed) || !aligned16(C) ||
+        !aligned16(workspace))
+        return MARLIN_ERR_MISALIGNED;
+
+    const int64_t G = scale_rows(K, group);
+    const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
+    if (workspace_bytes < required_workspace(M, (int)N, (int)K, gu))
+        return MARLIN_ERR_WORKSPACE_TOO_SMALL;
+
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return MARLIN_ERR_HIP;
+    const int cus = device_cu_count(device);
+    if (cus <= 0) return MARLIN_ERR_HIP;
+
+    for (int64_t m0 = 0; m0 < M; m0 += 128) {
+        const int mp = (M - m0) < 128 ? (int)(M - m0) : 128;
+        const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus, sparse);
+        const size_t counter_bytes = kCounterRegionBytes;
+        GemmProblem p;
+        p.A = A + m0 * K;
+        p.W = (const uint32_t *)w_packed;
+        p.S = (const uint16_t *)s_packed;
+        p.C = C + m0 * N;
+        p.counters = (uint32_t *)workspace;
+        p.partials = (float *)((char *)workspace + counter_bytes);
+        p.M = mp;
+        p.N = (int)N;
+        p.K = (int)K;
+        p.G = (int)G;
+        p.KU = (int)(K / 128);
+        p.rg = cfg.rg;
+        p.units = (int)(N / tile_cols(cfg)) * cfg.rg * p.KU;
+        p.gran = cfg.whole ? p.KU : 1;
+        p.per_wg = (p.units / p.gran) / cfg.grid;
+        p.extra = (p.units / p.gran) % cfg.grid;
+        p.group_units = gu;
+        // Exact for every block index below 2^13 (K <= 2^20): with
+        // e = gmagic * gu - 2^26 < gu <= 2^13, ku * e < 2^26.
+        p.gmagic = gu > 0 ? (uint32_t)((((uint64_t)1 << 26) + (uint64_t)gu - 1) / (uint64_t)gu) : 0u;
+        const hipError_t e = launch_gemm(cfg, p, stream);
+        if (e != hipSuccess) return MARLIN_ERR_HIP;
+    }
+    return MARLIN_OK;
+}
+
+marlin_status_t describe_impl(int64_t M, int64_t N, int64_t K, int64_t group, char *buf, size_t buf_bytes,
+                              bool sparse)
+{
+    if (!buf) return MARLIN_ERR_NULL_POINTER;
+    if (M < 0 || M > (1 << 24)) return MARLIN_ERR_INVALID_SHAPE;
+    const marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    int cus = kMaxCus;
+    int device = 0;
+    int count = 0;
+    if (hipGetDeviceCount(&count) == hipSuccess && count > 0 && hipGetDevice(&device) == hipSuccess) {
+        const int c = device_cu_count(device);
+        if (c > 0) cus = c;
+    } else {
+        (void)hipGetLastError();
+    }
+    const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
+    const int mp = M < 128 ? (M > 0 ? (int)M : 1) : 128;
+    const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus, sparse);
+    char name[96];
+    kernel_name(cfg, gu == 0, name, sizeof(name));
+    if (buf_bytes > 0)
+        snprintf(buf, buf_bytes, "%s cols=%d rg=%d partition=%s grid=%d", name,
+                 tile_cols(cfg), cfg.rg,
+                 cfg.whole ? "whole" : "streamk", cfg.grid);
+    return MARLIN_OK;
+}
+}  // namespace
 
 extern "C" {
 
@@ -327,6 +419,36 @@ marlin_status_t marlin_pack_weights(const uint8_t *q, const uint16_t *s, int64_t
     return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
 }
 
+size_t marlin_packed_sparse_weight_bytes(int64_t K, int64_t N)
+{
+    if (!shape_ok(K, N)) return 0;
+    return (size_t)K * (size_t)N / 8 * 3;
+}
+
+marlin_status_t marlin_pack_sparse_weights(const uint8_t *q, const uint16_t *s, int64_t K, int64_t N,
+                                           int64_t group, void *w_packed, void *s_packed, hipStream_t stream)
+{
+    if (!q || !s || !w_packed || !s_packed) return MARLIN_ERR_NULL_POINTER;
+    marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (!aligned16(w_packed) || !aligned16(s_packed)) return MARLIN_ERR_MISALIGNED;
+    const hipError_t e = launch_pack_sparse(q, s, (int)K, (int)N, (int)scale_rows(K, group),
+                                            (uint32_t *)w_packed, (uint16_t *)s_packed, stream);
+    return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
+}
+
+marlin_status_t marlin_unpack_sparse_weights(const void *w_packed, const void *s_packed, int64_t K, int64_t N,
+                                             int64_t group, uint8_t *q, uint16_t *s, hipStream_t stream)
+{
+    if (!q || !s || !w_packed || !s_packed) return MARLIN_ERR_NULL_POINTER;
+    marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (!aligned16(w_packed) || !aligned16(s_packed)) return MARLIN_ERR_MISALIGNED;
+    const hipError_t e = launch_unpack_sparse((const uint32_t *)w_packed, (const uint16_t *)s_packed, (int)K,
+                                              (int)N, (int)scale_rows(K, group), q, s, stream);
+    return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
+}
+
 marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed, int64_t K,
                                       int64_t N, int64_t group, uint8_t *q, uint16_t *s,
                                       hipStream_t stream)
@@ -344,82 +466,26 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed, const void 
                             uint16_t *C, void *workspace, size_t workspace_bytes, int64_t M,
                             int64_t N, int64_t K, int64_t group, hipStream_t stream)
 {
-    if (M < 0 || M > (1 << 24)) return MARLIN_ERR_INVALID_SHAPE;
-    marlin_status_t st = check_weights(K, N, group);
-    if (st != MARLIN_OK) return st;
-    if (M == 0) return MARLIN_OK;
-    if (!A || !w_packed || !s_packed || !C || !workspace) return MARLIN_ERR_NULL_POINTER;
-    if (!aligned16(A) || !aligned16(w_packed) || !aligned16(s_packed) || !aligned16(C) ||
-        !aligned16(workspace))
-        return MARLIN_ERR_MISALIGNED;
+    return gemm_impl(A, w_packed, s_packed, C, workspace, workspace_bytes, M, N, K, group, stream, false);
+}
 
-    const int64_t G = scale_rows(K, group);
-    const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
-    if (workspace_bytes < required_workspace(M, (int)N, (int)K, gu))
-        return MARLIN_ERR_WORKSPACE_TOO_SMALL;
-
-    int device = 0;
-    if (hipGetDevice(&device) != hipSuccess) return MARLIN_ERR_HIP;
-    const int cus = device_cu_count(device);
-    if (cus <= 0) return MARLIN_ERR_HIP;
-
-    for (int64_t m0 = 0; m0 < M; m0 += 128) {
-        const int mp = (M - m0) < 128 ? (int)(M - m0) : 128;
-        const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus);
-        const size_t counter_bytes = kCounterRegionBytes;
-        GemmProblem p;
-        p.A = A + m0 * K;
-        p.W = (const uint32_t *)w_packed;
-        p.S = (const uint16_t *)s_packed;
-        p.C = C + m0 * N;
-        p.counters = (uint32_t *)workspace;
-        p.partials = (float *)((char *)workspace + counter_bytes);
-        p.M = mp;
-        p.N = (int)N;
-        p.K = (int)K;
-        p.G = (int)G;
-        p.KU = (int)(K / 128);
-        p.rg = cfg.rg;
-        p.units = (int)(N / tile_cols(cfg)) * cfg.rg * p.KU;
-        p.gran = cfg.whole ? p.KU : 1;
-        p.per_wg = (p.units / p.gran) / cfg.grid;
-        p.extra = (p.units / p.gran) % cfg.grid;
-        p.group_units = gu;
-        // Exact for every block index below 2^13 (K <= 2^20): with
-        // e = gmagic * gu - 2^26 < gu <= 2^13, ku * e < 2^26.
-        p.gmagic = gu > 0 ? (uint32_t)((((uint64_t)1 << 26) + (uint64_t)gu - 1) / (uint64_t)gu) : 0u;
-        const hipError_t e = launch_gemm(cfg, p, stream);
-        if (e != hipSuccess) return MARLIN_ERR_HIP;
-    }
-    return MARLIN_OK;
+marlin_status_t marlin_gemm_sparse(const uint16_t *A, const void *w_packed, const void *s_packed,
+                                   uint16_t *C, void *workspace, size_t workspace_bytes, int64_t M,
+                                   int64_t N, int64_t K, int64_t group, hipStream_t stream)
+{
+    return gemm_impl(A, w_packed, s_packed, C, workspace, workspace_bytes, M, N, K, group, stream, true);
 }
 
 marlin_status_t marlin_describe(int64_t M, int64_t N, int64_t K, int64_t group, char *buf,
                                 size_t buf_bytes)
 {
-    if (!buf) return MARLIN_ERR_NULL_POINTER;
-    if (M < 0 || M > (1 << 24)) return MARLIN_ERR_INVALID_SHAPE;
-    const marlin_status_t st = check_weights(K, N, group);
-    if (st != MARLIN_OK) return st;
-    int cus = kMaxCus;
-    int device = 0;
-    int count = 0;
-    if (hipGetDeviceCount(&count) == hipSuccess && count > 0 && hipGetDevice(&device) == hipSuccess) {
-        const int c = device_cu_count(device);
-        if (c > 0) cus = c;
-    } else {
-        (void)hipGetLastError();
-    }
-    const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
-    const int mp = M < 128 ? (M > 0 ? (int)M : 1) : 128;
-    const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus);
-    char name[96];
-    kernel_name(cfg, gu == 0, name, sizeof(name));
-    if (buf_bytes > 0)
-        snprintf(buf, buf_bytes, "%s cols=%d rg=%d partition=%s grid=%d", name,
-                 tile_cols(cfg), cfg.rg,
-                 cfg.whole ? "whole" : "streamk", cfg.grid);
-    return MARLIN_OK;
+    return describe_impl(M, N, K, group, buf, buf_bytes, false);
+}
+
+marlin_status_t marlin_describe_sparse(int64_t M, int64_t N, int64_t K, int64_t group, char *buf,
+                                       size_t buf_bytes)
+{
+    return describe_impl(M, N, K, group, buf, buf_bytes, true);
 }
 
 }  // extern "C"

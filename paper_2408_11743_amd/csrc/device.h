@@ -51,6 +51,39 @@ __device__ __forceinline__ float4_t mfma(half8_t w, half8_t a, float4_t c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(w, a, c, 0, 0, 0);
 }
 
+// Masks of the int4 -> fp16 conversion, made opaque once per kernel (an empty
+// asm "redefines" them in vector registers) so that (x & m) | o selects the
+// single v_and_or_b32 with register operands.
+struct DequantConsts {
+    uint32_t lo, hi, ex;
+};
+
+__device__ __forceinline__ DequantConsts dequant_consts()
+{
+    DequantConsts k{0x000F000Fu, 0x00F000F0u, 0x64006400u};
+    asm volatile("" : "+v"(k.lo), "+v"(k.hi), "+v"(k.ex));
+    return k;
+}
+
+// Eight codes of one packed word -> the eight fp16 values q - 8 in element
+// order j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)), with the
+// paper's magic number (Section 3.4, "Dequantization and Tensor Cores"): the
+// code in the low mantissa bits of 1024.0 is 1024 + q, minus 1032 gives q - 8
+// exactly; a code four bits up gives 1024 + 16q, and one fma (x/16 - 72)
+// gives q - 8.
+__device__ __forceinline__ half8_t dequant_magic(uint32_t x, const DequantConsts &k)
+{
+    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
+    const half2_t mul = {(_Float16)0.0625f, (_Float16)0.0625f};
+    const half2_t add = {(_Float16)-72.0f, (_Float16)-72.0f};
+    const uint32_t y = x >> 8;
+    const half2_t r0 = as_h2((x & k.lo) | k.ex) - sub;
+    const half2_t r1 = __builtin_elementwise_fma(as_h2((x & k.hi) | k.ex), mul, add);
+    const half2_t r2 = as_h2((y & k.lo) | k.ex) - sub;
+    const half2_t r3 = __builtin_elementwise_fma(as_h2((y & k.hi) | k.ex), mul, add);
+    return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
+}
+
 // Scale row of 128-row block ku: ku / group_units as one multiply-high with
 // the host's rounded-up reciprocal 2^26 / group_units (exact for ku < 2^13).
 __device__ __forceinline__ int scale_row_of(int ku, const GemmProblem &p)

@@ -77,6 +77,49 @@ __device__ __forceinline__ half8_t bias_operand()
     return __builtin_bit_cast(half8_t, u32x4_t{0x00080008u, 0x00800080u, 0x00080008u, 0x00800080u});
 }
 
+// One stage of 2:4 sparse weights for NB column blocks: per block, two words
+// of kept codes (rows 0..63 and 64..127 of the 128-row block) and one word of
+// row indices (16 bits per half).  Loaded with the narrowest loads that cover
+// them: NB = 4 two 16-byte code loads and one 16-byte index load; NB = 2 one
+// 16-byte and one 8-byte; NB = 1 one 8-byte and one 4-byte.
+template <int NB>
+struct SparseWords {
+    u32x4_t c[NB == 4 ? 2 : 1];
+    u32x4_t m;
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t codes_off,
+                                         uint32_t meta_off)
+    {
+        if constexpr (NB == 4) {
+            c[0] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, codes_off, kAuxNonTemporal));
+            c[1] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + 1024, codes_off, kAuxNonTemporal));
+            m = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, meta_off, kAuxNonTemporal));
+        } else if constexpr (NB == 2) {
+            c[0] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, codes_off, kAuxNonTemporal));
+            const uint64_t v = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, lane_off, meta_off, kAuxNonTemporal));
+            m = u32x4_t{(uint32_t)v, (uint32_t)(v >> 32), 0u, 0u};
+        } else {
+            const uint64_t v = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(r, lane_off, codes_off, kAuxNonTemporal));
+            c[0] = u32x4_t{(uint32_t)v, (uint32_t)(v >> 32), 0u, 0u};
+            m = u32x4_t{__builtin_amdgcn_raw_buffer_load_b32(r, lane_off, meta_off, kAuxNonTemporal), 0u, 0u, 0u};
+        }
+    }
+    // kept codes of column block b, rows 64h .. 64h + 63
+    __device__ __forceinline__ uint32_t code(int b, int h) const { return c[(2 * b + h) >> 2][(2 * b + h) & 3]; }
+    __device__ __forceinline__ uint32_t meta(int b) const { return m[b]; }
+};
+
+// Sparse product of one column block and one 16-row block over 128 rows of
+// K: two smfmac steps (rows 0..63, 64..127), each taking the activation
+// operands of two dense k-steps.
+__device__ __forceinline__ float4_t smfmac2(half8_t w0, half8_t w1, const half8_t *a, uint32_t idx, float4_t c)
+{
+    typedef _Float16 half16_t __attribute__((ext_vector_type(16)));
+    const half16_t b0 = __builtin_shufflevector(a[0], a[1], 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+    const half16_t b1 = __builtin_shufflevector(a[2], a[3], 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+    c = __builtin_amdgcn_smfmac_f32_16x16x64_f16(w0, b0, c, (int)idx, 0, 0);
+    return __builtin_amdgcn_smfmac_f32_16x16x64_f16(w1, b1, c, (int)idx, 0, 1);
+}
+
 // ---------------------------------------------------------------------------
 // Register-streaming kernel.
 //
@@ -99,24 +142,40 @@ __device__ __forceinline__ half8_t bias_operand()
 // they processed that tile at the start of their ranges) the work-group adds
 // their slots to its registers and writes C at once; otherwise it writes slot
 // 1 and arrives like the others.
-template <int MB, int NB, int D, int AR, bool PER_CHANNEL>
-__global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
+//
+// 2:4 sparse weights (SPARSE, Section 4): the same schedule with the sparse
+// packed layout (per 64 x 128 unit: 2 KiB of kept codes, 1 KiB of 2-bit row
+// indices) and v_smfmac_f32_16x16x64_f16, whose first operand is the
+// compressed weights (two kept values of every 4 rows, row indices in a
+// VGPR) and whose second is the dense activations.  With the transposed
+// product the sparse operand is the weights, as the paper's 2:4 kernel does.
+// The activation reads are the dense path's (one smfmac takes the operands of
+// two 16x16x32 steps); codes are converted with the magic number (exact
+// q - 8, no zero-point product: the zero point of a pruned row would depend
+// on the row indices).
+template <int MB, int NB, int D, int AR, bool PER_CHANNEL, bool SPARSE>
+__device__ __forceinline__ void stream_body(const GemmProblem &p)
 {
     constexpr int KW = kStreamWaves;
     constexpr int kBlocks = NB * MB;               // 16x16 output blocks per wave
     constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
     constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
     constexpr int kSL = PER_CHANNEL ? 0 : kSLoads;
+    // weight loads per stage: NB 16-byte words (dense), or codes and row
+    // indices (sparse: 2 + 1 for NB = 4, else 1 + 1)
+    constexpr int kWL = SPARSE ? (NB == 4 ? 3 : 2) : NB;
+    constexpr uint32_t kUnitBytes = SPARSE ? 3072u : 4096u;  // per 64 x 128 unit
+    constexpr float kOutScale = SPARSE ? 1.0f : kTwo24;      // dense operands carry 2^-24
     // Activation rows through LDS (one or two 16-row blocks): the 4*AR rows of
     // the tile's row group for the stage's 128-row block land in a per-wave
     // LDS ring by AR direct-to-LDS loads (only real rows are fetched; the
     // register ring holds weights and scales only).
     constexpr int kARows = 4 * AR;
     constexpr int kAStage = kARows * 256;            // bytes per wave and stage
-    constexpr int kLoads = AR + NB + kSL;            // vector-memory ops per stage
+    constexpr int kLoads = AR + kWL + kSL;           // vector-memory ops per stage
     static_assert(KW == 4, "four waves per work-group");
     static_assert(MB <= 2 && AR >= 1 && kARows <= 16 * MB, "one or two row blocks, at least 4 rows");
-    static_assert((D - 1) * kLoads + NB + kSL < 64, "vmcnt range");
+    static_assert((D - 1) * kLoads + kWL + kSL < 64, "vmcnt range");
     __shared__ float4_t red[KW * kBlocks * 64];
     __shared__ __attribute__((aligned(16))) uint8_t a_lds[KW * D * kAStage + 256];
     __shared__ int flags[2];
@@ -137,12 +196,22 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // A tile c is column tile c / rg and row group c % rg (rows 32*(c % rg)
     // onwards when M exceeds 32; one group otherwise).  Byte offsets of tile
     // c's block 0: weights (4 KiB per (64 columns x 128 rows) block, 1 KiB per
-    // 16 columns) and scale rows (128 B per 64 columns).
+    // 16 columns; sparse: 3 KiB per block, this column block's codes at
+    // 1 KiB * (q/2) + 8 * (q%2) for column block q of the 64) and scale rows
+    // (128 B per 64 columns).
     const uint32_t RG = (uint32_t)p.rg;
     auto col_of = [&](int c) -> uint32_t { return RG == 1 ? (uint32_t)c : (uint32_t)c / RG; };
     auto w_tile = [&](int c) -> uint32_t {
         const uint32_t nbg = col_of(c) * NB;
+        if constexpr (SPARSE)
+            return (nbg >> 2) * (uint32_t)KU * kUnitBytes + ((nbg & 3u) >> 1) * 1024u + (nbg & 1u) * 8u;
         return ((nbg >> 2) * (uint32_t)KU * 4u + (nbg & 3u)) << 10;
+    };
+    // sparse: the row indices of column block q lie 2 KiB + 4q past the unit
+    // start, i.e. this much past the codes
+    auto meta_delta = [&](int c) -> uint32_t {
+        const uint32_t q = (col_of(c) * NB) & 3u;
+        return 2048u + 4u * q - (q >> 1) * 1024u - (q & 1u) * 8u;
     };
     auto s_tile = [&](int c) -> uint32_t {
         const uint32_t nbg = col_of(c) * NB;
@@ -156,7 +225,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     };
 
     // Per-lane parts of the load addresses (fixed for the whole kernel).
-    const uint32_t w_lane = (uint32_t)kw * 4096u + (uint32_t)lane * 16u;
+    const uint32_t w_lane = (uint32_t)kw * kUnitBytes + (uint32_t)lane * 16u;
     const uint32_t s_lane = (uint32_t)lg * 32u;
     // Direct-to-LDS activation loads: load i, lane l fetches row r = 4i + l/16,
     // 16-byte chunk (l % 16) ^ r of the block (an XOR swizzle, so that the
@@ -190,18 +259,20 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
         __syncthreads();  // zero row written before any wave reads it
     }
     // Rows of A past M lie past the end of the A buffer: their loads return 0.
-    const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
+    const uint32_t w_bytes = SPARSE ? (uint32_t)p.K / 8u * (uint32_t)p.N * 3u : (uint32_t)p.K * (uint32_t)(p.N / 2);
 
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
-    u32x4_t wr[D][NB];
+    u32x4_t wr[SPARSE ? 1 : D][NB];   // dense weights
+    SparseWords<NB> sw[SPARSE ? D : 1];  // sparse codes and row indices
     half8_t sr[D][kSLoads];
 
     // ---- load cursor: wave-uniform, advanced once per stage ----
     int ld_c = c_first, ld_ku = k0;
     int ld_end = (c_first == c_last) ? k1 : KU;
-    uint32_t ld_w = w_tile(ld_c) + (uint32_t)ld_ku * 4096u;
+    uint32_t ld_w = w_tile(ld_c) + (uint32_t)ld_ku * kUnitBytes;
     uint32_t ld_s = s_tile(ld_c);
+    uint32_t ld_md = SPARSE ? meta_delta(ld_c) : 0u;
     // The tile's activation rows as their own buffer: rows past M read 0.
     const uint16_t *ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
     uint32_t a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
@@ -220,10 +291,14 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
         }
         const __amdgpu_buffer_rsrc_t rw =
             __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
+        if constexpr (SPARSE) {
+            sw[j].load(rw, w_lane, ld_w, ld_w + ld_md);
+        } else {
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
-            wr[j][b] = __builtin_bit_cast(
-                u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, ld_w, kAuxNonTemporal));
+            for (int b = 0; b < NB; ++b)
+                wr[j][b] = __builtin_bit_cast(
+                    u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, ld_w, kAuxNonTemporal));
+        }
         if constexpr (!PER_CHANNEL) {
             const __amdgpu_buffer_rsrc_t rs =
                 __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
@@ -245,13 +320,14 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     };
     auto advance_ld = [&]() {
         ld_ku += KW;
-        ld_w += KW * 4096u;
+        ld_w += KW * kUnitBytes;
         if (ld_ku >= ld_end) {  // next segment (rare)
             ld_c += 1;
             ld_ku = 0;
             ld_end = (ld_c < c_last) ? KU : (ld_c == c_last) ? k1 : 0;  // 0: past the range
             ld_w = w_tile(ld_c);
             ld_s = s_tile(ld_c);
+            if constexpr (SPARSE) ld_md = meta_delta(ld_c);
             if (RG > 1 && ld_end > 0) {
                 ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
                 a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
@@ -284,6 +360,8 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     half8_t kb = bias_operand();
     asm volatile("" : "+v"(kb));  // keep the constant in vector registers
     const float4_t zero4 = {0.f, 0.f, 0.f, 0.f};
+    const DequantConsts dq = dequant_consts();  // sparse codes: magic-number conversion
+    (void)dq;
 
     // One stage: for each 16-row block of A, four MFMA steps per column block
     // plus four for the zero point.  Group scales: the stage's zero-point
@@ -298,7 +376,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
             // written as assembly, with their own lgkmcnt wait, so that the
             // compiler's conservative tracking of direct-to-LDS writes does
             // not add waits for the whole ring.
-            constexpr int kAfter = (D - 1) * kLoads + NB + kSL;
+            constexpr int kAfter = (D - 1) * kLoads + kWL + kSL;
             __builtin_amdgcn_s_waitcnt((kAfter & 15) | (7 << 4) | (15 << 8) | ((kAfter >> 4) << 14));
             asm volatile("" ::: "memory");
             u32x4_t v[4 * MB];
@@ -317,9 +395,30 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
                                "+v"(v[7])::"memory");
             }
 #pragma unroll
-            for (int i = 0; i < 4 * MB; ++i) a[i] = prescale(__builtin_bit_cast(half8_t, v[i]));
+            for (int i = 0; i < 4 * MB; ++i)
+                a[i] = SPARSE ? __builtin_bit_cast(half8_t, v[i]) : prescale(__builtin_bit_cast(half8_t, v[i]));
         }
-        if constexpr (PER_CHANNEL) {
+        if constexpr (SPARSE) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const half8_t w0 = dequant_magic(sw[j].code(b, 0), dq);
+                const half8_t w1 = dequant_magic(sw[j].code(b, 1), dq);
+                if constexpr (PER_CHANNEL) {
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) acc[b][mb] = smfmac2(w0, w1, a + mb * 4, sw[j].meta(b), acc[b][mb]);
+                } else {
+                    // scales of block b: halves 4b .. 4b+3 of this lane's run
+                    const half8_t sv = sr[j][b >> 1];
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+                        const float4_t t4 = smfmac2(w0, w1, a + mb * 4, sw[j].meta(b), zero4);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            acc[b][mb][i] = __builtin_fmaf(t4[i], (float)sv[(b & 1) * 4 + i], acc[b][mb][i]);
+                    }
+                }
+            }
+        } else if constexpr (PER_CHANNEL) {
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
 #pragma unroll
@@ -378,10 +477,10 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
                 if constexpr (PER_CHANNEL) {
                     const half4_t s4 = *(const half4_t *)(p.S + (int64_t)(nbg >> 2) * 64 + lg * 16 + (nbg & 3) * 4);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] *= (float)s4[i] * kTwo24;
+                    for (int i = 0; i < 4; ++i) v[i] *= (float)s4[i] * kOutScale;
                 } else {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] *= kTwo24;
+                    for (int i = 0; i < 4; ++i) v[i] *= kOutScale;
                 }
                 const half4_t h = {(_Float16)v[0], (_Float16)v[1], (_Float16)v[2], (_Float16)v[3]};
                 *(half4_t *)(p.C + (int64_t)(r0 + m) * p.N + nbg * 16 + lg * 4) = h;
@@ -404,7 +503,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
     // (whole column), keep the sum (shared last tile) or write slot 0
     // (shared first tile).
     auto finish_segment = [&]() {
-        if constexpr (PER_CHANNEL) {
+        if constexpr (PER_CHANNEL && !SPARSE) {
 #pragma unroll
             for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -478,6 +577,18 @@ __global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
                         own_slot, store_c);
 }
 
+template <int MB, int NB, int D, int AR, bool PER_CHANNEL>
+__global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
+{
+    stream_body<MB, NB, D, AR, PER_CHANNEL, false>(p);
+}
+
+template <int MB, int NB, int D, int AR, bool PER_CHANNEL>
+__global__ void __launch_bounds__(256, 1) w4a16_sparse_kernel(GemmProblem p)
+{
+    stream_body<MB, NB, D, AR, PER_CHANNEL, true>(p);
+}
+
 }  // namespace
 
 int slot_floats(const GemmConfig &cfg)
@@ -500,8 +611,11 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
     constexpr int D = stream_depth<MB, NB, AR>();
     GemmProblem arg = p;
     void *args[] = {&arg};
-    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, true>
-                                          : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, false>;
+    const bool pc = p.group_units == 0;
+    const void *fn = cfg.sparse ? (pc ? (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, true>
+                                      : (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, false>)
+                                : (pc ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, true>
+                                      : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, false>);
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * kStreamWaves), args, 0, stream);
 }
 
@@ -531,8 +645,8 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
         if (n) buf[0] = 0;
         return;
     }
-    snprintf(buf, n, "w4a16_stream_kernel<%d, %d, %d, %d, %s>", cfg.mb, cfg.nb, d, cfg.ar,
-             per_channel ? "true" : "false");
+    snprintf(buf, n, "%s<%d, %d, %d, %d, %s>", cfg.sparse ? "w4a16_sparse_kernel" : "w4a16_stream_kernel", cfg.mb,
+             cfg.nb, d, cfg.ar, per_channel ? "true" : "false");
 }
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)

@@ -31,6 +31,7 @@ struct GemmConfig {
     int grid;
     int tile_wm;  // tile kernel: waves along M (1: 4x1 waves; 2: 2x2 waves); mb, nb: row and
                   // column blocks per wave
+    int sparse;   // 2:4 sparse weights (stream kernel only)
 };
 
 // Columns and rows of one tile of a configuration.
@@ -69,7 +70,7 @@ constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4 * 4;
 // Device facts cached per device.
 int device_cu_count(int device);
 
-GemmConfig choose_config(int M, int N, int K, int group_units, int grid_cap);
+GemmConfig choose_config(int M, int N, int K, int group_units, int grid_cap, bool sparse = false);
 size_t workspace_bytes_for(const GemmConfig &cfg, int N);
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
@@ -83,5 +84,9 @@ hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);
 hipError_t launch_unpack(const uint32_t *w_packed, const uint16_t *s_packed, int K, int N,
                          int G, uint8_t *q, uint16_t *s, hipStream_t stream);
+hipError_t launch_pack_sparse(const uint8_t *q, const uint16_t *s, int K, int N, int G, uint32_t *w_packed,
+                              uint16_t *s_packed, hipStream_t stream);
+hipError_t launch_unpack_sparse(const uint32_t *w_packed, const uint16_t *s_packed, int K, int N, int G,
+                                uint8_t *q, uint16_t *s, hipStream_t stream);
 
 }  // namespace marlin

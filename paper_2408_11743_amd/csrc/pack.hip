@@ -90,6 +90,100 @@ __global__ void permute_scales_kernel(const uint16_t *__restrict__ src, int N, i
     }
 }
 
+// ---- 2:4 sparse weights (Section 4) ----
+// Unit (c, ku) = 64-column tile c, 128-row block ku, at word (c*KU + ku)*768:
+//   codes, 512 words: word ((d >> 2)*64 + l)*4 + (d & 3), d = 2*nb + h, holds
+//     the 8 kept codes of column n = 64c + 16nb + l%16 in rows
+//     128ku + 64h + 16(l/16) + [0, 16): group g = 0..3 of 4 rows keeps codes
+//     j = 2g and 2g + 1 (in increasing row order), code j in nibble
+//     (j >> 1) + 4(j & 1);
+//   metadata, 256 words: word 512 + l*4 + nb holds, at bits 16h + 4g + 2t,
+//     the row (0..3) within group g of kept code 2g + t.
+// Kept rows are the first two rows of the group whose code is not 8 (weight
+// not zero); a group with fewer is completed with its lowest rows of code 8,
+// and the pair is kept in increasing row order.
+__global__ void pack_sparse_kernel(const uint8_t *__restrict__ q, int K, int N, uint32_t *__restrict__ w)
+{
+    const int64_t items = (int64_t)K * N / 32;  // (unit, lane, column block)
+    const int KU = K / 128;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < items;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int nb = (int)(idx & 3);
+        const int l = (int)((idx >> 2) & 63);
+        const int64_t unit = idx >> 8;  // c*KU + ku
+        const int ku = (int)(unit % KU);
+        const int c = (int)(unit / KU);
+        const int n = 64 * c + 16 * nb + (l & 15);
+        uint32_t meta = 0;
+        uint32_t *uw = w + unit * 768;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t word = 0;
+            const int kbase = 128 * ku + 64 * h + 16 * (l >> 4);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                uint32_t code[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) code[r] = q[(int64_t)(kbase + 4 * g + r) * N + n] & 0xFu;
+                int p[2] = {-1, -1}, np = 0;
+                for (int r = 0; r < 4 && np < 2; ++r)
+                    if (code[r] != 8u) p[np++] = r;
+                for (int r = 0; r < 4 && np < 2; ++r)
+                    if (r != p[0]) p[np++] = r;
+                if (p[0] > p[1]) {
+                    const int t = p[0];
+                    p[0] = p[1];
+                    p[1] = t;
+                }
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    const int j = 2 * g + t;
+                    word |= code[p[t]] << (4 * nibble_of(j));
+                    meta |= (uint32_t)p[t] << (16 * h + 4 * g + 2 * t);
+                }
+            }
+            const int d = 2 * nb + h;
+            uw[((d >> 2) * 64 + l) * 4 + (d & 3)] = word;
+        }
+        uw[512 + l * 4 + nb] = meta;
+    }
+}
+
+__global__ void unpack_sparse_kernel(const uint32_t *__restrict__ w, int K, int N, uint8_t *__restrict__ q)
+{
+    const int64_t items = (int64_t)K * N / 32;
+    const int KU = K / 128;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < items;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        const int nb = (int)(idx & 3);
+        const int l = (int)((idx >> 2) & 63);
+        const int64_t unit = idx >> 8;
+        const int ku = (int)(unit % KU);
+        const int c = (int)(unit / KU);
+        const int n = 64 * c + 16 * nb + (l & 15);
+        const uint32_t *uw = w + unit * 768;
+        const uint32_t meta = uw[512 + l * 4 + nb];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int d = 2 * nb + h;
+            const uint32_t word = uw[((d >> 2) * 64 + l) * 4 + (d & 3)];
+            const int kbase = 128 * ku + 64 * h + 16 * (l >> 4);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                uint8_t out[4] = {8, 8, 8, 8};
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    const int j = 2 * g + t;
+                    const int r = (int)((meta >> (16 * h + 4 * g + 2 * t)) & 3u);
+                    out[r] = (uint8_t)((word >> (4 * nibble_of(j))) & 0xFu);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) q[(int64_t)(kbase + 4 * g + r) * N + n] = out[r];
+            }
+        }
+    }
+}
+
 int blocks_for(int64_t work, int threads)
 {
     int64_t b = (work + threads - 1) / threads;
@@ -124,6 +218,34 @@ hipError_t launch_unpack(const uint32_t *w_packed, const uint16_t *s_packed, int
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(permute_scales_kernel, dim3(blocks_for((int64_t)G * N, threads)),
                        dim3(threads), 0, stream, s_packed, N, G, 1, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_sparse(const uint8_t *q, const uint16_t *s, int K, int N, int G, uint32_t *w_packed,
+                              uint16_t *s_packed, hipStream_t stream)
+{
+    const int threads = 256;
+    const int64_t items = (int64_t)K * N / 32;
+    hipLaunchKernelGGL(pack_sparse_kernel, dim3(blocks_for(items, threads)), dim3(threads), 0, stream, q, K, N,
+                       w_packed);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(permute_scales_kernel, dim3(blocks_for((int64_t)G * N, threads)), dim3(threads), 0, stream,
+                       s, N, G, 0, s_packed);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_sparse(const uint32_t *w_packed, const uint16_t *s_packed, int K, int N, int G,
+                                uint8_t *q, uint16_t *s, hipStream_t stream)
+{
+    const int threads = 256;
+    const int64_t items = (int64_t)K * N / 32;
+    hipLaunchKernelGGL(unpack_sparse_kernel, dim3(blocks_for(items, threads)), dim3(threads), 0, stream, w_packed,
+                       K, N, q);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(permute_scales_kernel, dim3(blocks_for((int64_t)G * N, threads)), dim3(threads), 0, stream,
+                       s_packed, N, G, 1, s);
     return hipGetLastError();
 }
 

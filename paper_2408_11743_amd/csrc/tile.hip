@@ -38,35 +38,6 @@ namespace {
 
 using namespace dev;
 
-// Masks of the int4 -> fp16 conversion, made opaque once per kernel (an empty
-// asm "redefines" them in vector registers) so that (x & m) | o selects the
-// single v_and_or_b32 with register operands.
-struct DequantConsts {
-    uint32_t lo, hi, ex;
-};
-
-__device__ __forceinline__ DequantConsts dequant_consts()
-{
-    DequantConsts k{0x000F000Fu, 0x00F000F0u, 0x64006400u};
-    asm volatile("" : "+v"(k.lo), "+v"(k.hi), "+v"(k.ex));
-    return k;
-}
-
-// Eight codes of one packed word -> the eight fp16 values q - 8 in element
-// order j = 0..7 (code j sits in nibble (j >> 1) + 4 (j & 1)).
-__device__ __forceinline__ half8_t dequant_magic(uint32_t x, const DequantConsts &k)
-{
-    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
-    const half2_t mul = {(_Float16)0.0625f, (_Float16)0.0625f};
-    const half2_t add = {(_Float16)-72.0f, (_Float16)-72.0f};
-    const uint32_t y = x >> 8;
-    const half2_t r0 = as_h2((x & k.lo) | k.ex) - sub;
-    const half2_t r1 = __builtin_elementwise_fma(as_h2((x & k.hi) | k.ex), mul, add);
-    const half2_t r2 = as_h2((y & k.lo) | k.ex) - sub;
-    const half2_t r3 = __builtin_elementwise_fma(as_h2((y & k.hi) | k.ex), mul, add);
-    return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
-}
-
 // Ring depth: stages that fit in LDS (activation rows, then each wave's
 // weights), capped so that the loads of the stages in flight stay within the
 // vmcnt range.

@@ -19,10 +19,12 @@ def _cur_stream(t: torch.Tensor):
     return torch.cuda.current_stream(t.device)
 
 
-def pack(q: torch.Tensor, s: torch.Tensor, group=128):
+def pack(q: torch.Tensor, s: torch.Tensor, group=128, sparse: bool = False):
     """Pack codes q (uint8 [K, N]) and scales s (fp16 [G, N]) on the GPU.
 
-    Returns (w_packed uint8 [K*N/2], s_packed fp16 [G*N]).
+    Returns (w_packed uint8 [K*N/2], s_packed fp16 [G*N]).  With
+    ``sparse=True`` q is 2:4 sparse along K (pruned rows hold code 8) and
+    w_packed is the sparse layout (uint8 [3*K*N/8]).
     """
     if not (q.is_cuda and s.is_cuda):
         raise ValueError("pack: q and s must be device tensors")
@@ -30,7 +32,7 @@ def pack(q: torch.Tensor, s: torch.Tensor, group=128):
         raise TypeError("pack: q must be uint8, s float16")
     K, N = q.shape
     g = _group(K, group)
-    wb = B.marlin_packed_weight_bytes(K, N)
+    wb = B.marlin_packed_sparse_weight_bytes(K, N) if sparse else B.marlin_packed_weight_bytes(K, N)
     sb = B.marlin_packed_scale_bytes(K, N, g)
     if wb == 0 or sb == 0:
         raise B.MarlinError("pack", 2)
@@ -38,17 +40,19 @@ def pack(q: torch.Tensor, s: torch.Tensor, group=128):
     s = s.contiguous()
     wp = torch.empty(wb, dtype=torch.uint8, device=q.device)
     sp = torch.empty(sb // 2, dtype=torch.float16, device=q.device)
-    B.marlin_pack_weights(q, s, K, N, g, wp, sp, _cur_stream(q))
+    fn = B.marlin_pack_sparse_weights if sparse else B.marlin_pack_weights
+    fn(q, s, K, N, g, wp, sp, _cur_stream(q))
     return wp, sp
 
 
-def unpack(wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128):
+def unpack(wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128, sparse: bool = False):
     """Inverse of ``pack``: returns (q uint8 [K, N], s fp16 [G, N])."""
     g = _group(K, group)
     G = 1 if g == -1 else K // g
     q = torch.empty((K, N), dtype=torch.uint8, device=wp.device)
     s = torch.empty((G, N), dtype=torch.float16, device=wp.device)
-    B.marlin_unpack_weights(wp, sp, K, N, g, q, s, _cur_stream(wp))
+    fn = B.marlin_unpack_sparse_weights if sparse else B.marlin_unpack_weights
+    fn(wp, sp, K, N, g, q, s, _cur_stream(wp))
     return q, s
 
 
@@ -73,8 +77,10 @@ _default_ws: dict = {}
 
 
 def gemm(A: torch.Tensor, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128,
-         out: torch.Tensor | None = None, workspace: Workspace | None = None) -> torch.Tensor:
-    """C = A * dequant(W) with packed W; A fp16 [M, K] -> C fp16 [M, N]."""
+         out: torch.Tensor | None = None, workspace: Workspace | None = None,
+         sparse: bool = False) -> torch.Tensor:
+    """C = A * dequant(W) with packed W; A fp16 [M, K] -> C fp16 [M, N].
+    ``sparse=True``: W packed by ``pack(..., sparse=True)``."""
     if A.dtype != torch.float16 or not A.is_cuda:
         raise TypeError("gemm: A must be a float16 device tensor")
     A = A.contiguous()
@@ -89,5 +95,6 @@ def gemm(A: torch.Tensor, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, gr
         key = (A.device, torch.cuda.current_stream(A.device).cuda_stream)
         workspace = _default_ws.setdefault(key, Workspace(A.device))
     buf = workspace.ensure(need)
-    B.marlin_gemm(A, wp, sp, out, buf, buf.numel(), M, N, K, g, _cur_stream(A))
+    fn = B.marlin_gemm_sparse if sparse else B.marlin_gemm
+    fn(A, wp, sp, out, buf, buf.numel(), M, N, K, g, _cur_stream(A))
     return out

@@ -24,6 +24,8 @@ What each pin stands on:
   blas             C matches numpy's fp64 matmul of A with the dequantised W
   dequant          s = 1 gives q - 8; q = 9 gives the group-expanded scales
   sampled          the sampled routine equals the full routine bit for bit
+  sparse24         2:4 sparse weights: the exact sum over kept entries only equals
+                   the oracle on the dense codes with code 8 at pruned entries
 """
 from __future__ import annotations
 
@@ -241,9 +243,31 @@ def pin_sampled(lib):
     assert np.array_equal(out, C[mi, ni])
 
 
+def pin_sparse24(lib):
+    # 2:4 sparse weights (Section 4): the product over the kept entries only,
+    # in exact rationals, equals the oracle on the dense code matrix whose
+    # pruned entries hold code 8 (weight 0), within the summation bound.
+    for ci, (M, K, N, g) in enumerate([(2, 128, 8, 128), (3, 256, 4, 128), (1, 256, 16, 256)]):
+        rng = _rng(31, ci)
+        G = -(-K // g)
+        A, q, s = _rand_inputs(rng, M, K, N, G)
+        pat = np.array([[1, 1, 0, 0], [1, 0, 1, 0], [1, 0, 0, 1], [0, 1, 1, 0], [0, 1, 0, 1], [0, 0, 1, 1]], bool)
+        keep = pat[rng.integers(0, 6, size=(K // 4, N))].transpose(0, 2, 1).reshape(K, N)
+        qd = np.where(keep, q, np.uint8(8)).astype(np.uint8)
+        C = _gemm(lib, A, qd, s, g)
+        Af = [[Fraction(float(x)) for x in row] for row in A.astype(np.float64)]
+        sf = [[Fraction(float(x)) for x in row] for row in s.astype(np.float64)]
+        for m in range(M):
+            for n in range(N):
+                terms = [Af[m][k] * sf[k // g][n] * (int(q[k, n]) - 8) for k in range(K) if keep[k, n]]
+                exact = sum(terms, Fraction(0))
+                bound = K * 2.0 ** -52 * float(sum(abs(t) for t in terms))
+                assert abs(Fraction(C[m, n]) - exact) <= bound, (ci, m, n)
+
+
 PINS = [pin_f16_decode, pin_exact_rational, pin_identity, pin_zero, pin_one_hot,
         pin_integer_sums, pin_power_of_two, pin_group_channel, pin_linearity,
-        pin_dequant, pin_blas, pin_sampled]
+        pin_dequant, pin_blas, pin_sampled, pin_sparse24]
 
 
 def run_all(lib_path: str) -> list[str]:

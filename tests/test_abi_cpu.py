@@ -167,3 +167,36 @@ def test_override_selects_the_kernel(monkeypatch):
     assert d.startswith("w4a16_stream_kernel<") and "cols=32 rg=4 partition=streamk grid=7" in d, d
     monkeypatch.delenv("MARLIN_FORCE_CONFIG")
     assert "grid=7" not in B.marlin_describe(128, 1024, 1024, 128)
+
+
+def test_sparse_entry_points(L):
+    assert L.marlin_packed_sparse_weight_bytes(8192, 8192) == 8192 * 8192 * 3 // 8
+    assert L.marlin_packed_sparse_weight_bytes(4000, 4096) == 0
+
+    def spack(q=FAKE, s=FAKE, K=256, N=128, g=128, w=FAKE, sp=FAKE):
+        return L.marlin_pack_sparse_weights(q, s, K, N, g, w, sp, None)
+
+    def sunpack(w=FAKE, sp=FAKE, K=256, N=128, g=128, q=FAKE, s=FAKE):
+        return L.marlin_unpack_sparse_weights(w, sp, K, N, g, q, s, None)
+
+    for f in (spack, sunpack):
+        assert f(K=200) == SHAPE
+        assert f(g=64) == GROUP
+        assert f(w=FAKE + 4) == ALIGN
+    assert spack(q=None) == NULLP
+    assert sunpack(q=None) == NULLP
+
+    def sgemm(A=FAKE, W=FAKE, ws=FAKE, wsb=1 << 40, M=16, N=8192, K=8192, g=128):
+        return L.marlin_gemm_sparse(A, W, FAKE, FAKE, ws, wsb, M, N, K, g, None)
+
+    assert sgemm(A=None) == NULLP
+    assert sgemm(K=4000) == SHAPE
+    assert sgemm(g=64) == GROUP
+    assert sgemm(W=FAKE + 8) == ALIGN
+    # one workspace size serves both entry points
+    need = L.marlin_workspace_bytes(16, 8192, 8192, 128)
+    assert sgemm(wsb=need - 1) == WS
+    assert sgemm(M=0, A=None) == OK
+    for M in (1, 16, 32, 64, 128):
+        d = B.marlin_describe_sparse(M, 8192, 8192, 128)
+        assert d.startswith("w4a16_sparse_kernel<") and d.endswith(tuple("0123456789")), d

@@ -124,3 +124,55 @@ def test_subnormal_operands_every_code_every_slot(slot):
         for a in (Fraction(1), Fraction(-3, 4), Fraction(1027, 1024)):
             a_scaled = a / 16 if upper else a
             assert w * a_scaled - Fraction(float(_fp16(zbits))) * a_scaled == (code - zp) * a * e
+
+
+# ---- 2:4 sparse layout ----
+
+def test_sparse_roundtrip_and_selection():
+    import synth
+    for K, N in [(128, 64), (256, 128)]:
+        q, keep, s = synth.sparse24_weights(4, K, N, 128)
+        w = layout.pack_sparse(q)
+        assert w.dtype == np.uint32 and w.size == K * N * 3 // 32
+        assert np.array_equal(layout.unpack_sparse(w, K, N), q)
+    # at most two non-8 codes per group: exact; the kept rows are increasing
+    rng = np.random.default_rng(5)
+    K, N = 128, 64
+    q = np.full((K, N), 8, np.uint8)
+    for r in range(K // 4):
+        for n in range(N):
+            rows = rng.choice(4, size=rng.integers(0, 3), replace=False)
+            q[4 * r + rows, n] = rng.choice([c for c in range(16) if c != 8], size=len(rows))
+    pos, codes = layout.sparse_selection(q)
+    assert (pos[:, 0, :] < pos[:, 1, :]).all()
+    assert np.array_equal(layout.unpack_sparse(layout.pack_sparse(q), K, N), q)
+    # a third non-8 code in a group is dropped, the first two are kept
+    q3 = np.full((K, N), 8, np.uint8)
+    q3[0:3, 0] = [1, 2, 3]
+    out = layout.unpack_sparse(layout.pack_sparse(q3), K, N)
+    assert list(out[0:4, 0]) == [1, 2, 8, 8]
+
+
+def test_sparse_single_positions_follow_header():
+    # a lone non-8 code at (k, n): codes word ((d>>2)*64 + l)*4 + (d&3) of
+    # unit (c, ku), d = 2nb + h, nibble (j>>1) + 4(j&1) with j = 2g + t; the
+    # index word 512 + 4l + nb holds its row at bits 16h + 4g + 2t.
+    K, N = 256, 128
+    KU = K // 128
+    for (k, n, code) in [(0, 0, 3), (5, 17, 15), (66, 64, 0), (130, 127, 9), (255, 90, 1)]:
+        q = np.full((K, N), 8, np.uint8)
+        q[k, n] = code
+        w = layout.pack_sparse(q).reshape(N // 64, KU, 768)
+        c, nb, ku = n // 64, (n % 64) // 16, k // 128
+        h, lg, g, r = (k % 128) // 64, (k % 64) // 16, (k % 16) // 4, k % 4
+        l = 16 * lg + n % 16
+        # the group is completed with its lowest code-8 row: (r, 1) if r == 0, else (0, r)
+        t = 0 if r == 0 else 1
+        j = 2 * g + t
+        d = 2 * nb + h
+        word = w[c, ku, ((d >> 2) * 64 + l) * 4 + (d & 3)]
+        assert (word >> (4 * int(layout.NIBBLE_OF[j]))) & 0xF == code
+        meta = w[c, ku, 512 + 4 * l + nb]
+        assert (meta >> (16 * h + 4 * g + 2 * t)) & 3 == r
+        other = 1 if r == 0 else 0
+        assert (meta >> (16 * h + 4 * g + 2 * (1 - t))) & 3 == other
