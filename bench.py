@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--per-m-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fp16", action="store_true")
+    ap.add_argument("--no-sparse", action="store_true",
+                    help="skip the 2:4 sparse section (K = N = 8192, g = 128, M sweep)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run plain device-to-device copies of this many MB (outside the timed "
                          "region) so hardware byte counters can be scaled against a known size")
@@ -72,6 +74,86 @@ def measured_traffic():
         return rec["step_avg_hbm_bytes_per_launch"]
     except (OSError, KeyError, ValueError):
         return None
+
+
+SPARSE_K, SPARSE_N, SPARSE_WID = 8192, 8192, 4
+
+
+def graph_time_us(launch, count, stream, reps, torch, np):
+    """Median per-launch time of a graph of `count` launches (launch(i))."""
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        launch(0)
+        stream.synchronize()
+        with torch.cuda.graph(gr, stream=stream):
+            for i in range(count):
+                launch(i)
+        gr.replay()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            a0.record(stream)
+            gr.replay()
+            a1.record(stream)
+            a1.synchronize()
+            times.append(a0.elapsed_time(a1) * 1e3 / count)
+    del gr
+    return float(np.median(times))
+
+
+def sparse_section(args, mk, R, synth, torch, np, dev):
+    """The 2:4 sparse workload (Section 4): K = N = 8192, g = 128, M sweep;
+    per M the sparse kernel, the dense W4A16 kernel on the same matrix and
+    fp16 torch.matmul on it, each over >= 1 GiB of rotated weight copies."""
+    K, N, g = SPARSE_K, SPARSE_N, GROUP
+    q, keep, s = synth.sparse24_weights(SPARSE_WID, K, N, g)
+    qd, sd = torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev)
+    L = mk.lib()
+    copies = {}
+    for sp_flag in (True, False):
+        wp, sp = mk.pack(qd, sd, group=g, sparse=sp_flag)
+        n = max(2, math.ceil(ROTATION_BYTES / (wp.numel() + 2 * sp.numel())))
+        copies[sp_flag] = ([wp] + [wp.clone() for _ in range(n - 1)], sp)
+    w16 = ((qd.to(torch.float32) - 8.0) * sd.to(torch.float32).repeat_interleave(g, dim=0)).to(torch.float16)
+    n16 = max(2, math.ceil(ROTATION_BYTES / (w16.numel() * 2)))
+    w16s = [w16] + [w16.clone() for _ in range(n16 - 1)]
+    ws = mk.Workspace(dev)
+    wsbuf = ws.ensure(max(mk.marlin_workspace_bytes(M, N, K, g) for M in M_SWEEP))
+    stream = torch.cuda.Stream(device=dev)
+    rows = []
+    for M in M_SWEEP:
+        A = torch.from_numpy(synth.activations(SPARSE_WID, M, K)).to(dev)
+        C = torch.empty((M, N), dtype=torch.float16, device=dev)
+        t = {}
+        for sp_flag in (True, False):
+            wps, sp = copies[sp_flag]
+            fn = L.marlin_gemm_sparse if sp_flag else L.marlin_gemm
+
+            def launch(i, wps=wps, sp=sp, fn=fn):
+                st = fn(A.data_ptr(), wps[i % len(wps)].data_ptr(), sp.data_ptr(), C.data_ptr(),
+                        wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g, stream.cuda_stream)
+                if st != 0:
+                    raise mk.MarlinError("marlin_gemm_sparse" if sp_flag else "marlin_gemm", st)
+            t[sp_flag] = graph_time_us(launch, len(wps), stream, args.per_m_reps, torch, np)
+        t16 = None
+        if not args.no_fp16:
+            t16 = graph_time_us(lambda i: torch.matmul(A, w16s[i % n16]), n16, stream, args.per_m_reps, torch, np)
+        troof = R.sparse24_t_roof(M, N, K, g) * 1e6
+        rec = {"M": M, "us": round(t[True], 3), "dense_w4_us": round(t[False], 3),
+               "speedup_vs_dense_w4": round(t[False] / t[True], 3),
+               "roof_us": round(troof, 3), "roof_frac": round(troof / t[True], 4),
+               "launch": mk.marlin_describe_sparse(M, N, K, g)}
+        if t16 is not None:
+            rec["fp16_us"] = round(t16, 3)
+            rec["speedup_vs_fp16"] = round(t16 / t[True], 3)
+        rows.append(rec)
+        log("sparse 2:4 %dx%d M=%3d: %.3f us (dense W4 %.3f us, fp16 %s us), roofline frac %.3f" %
+            (K, N, M, t[True], t[False], "%.3f" % t16 if t16 else "-", troof / t[True]))
+    del copies, w16s, w16
+    return {"workload": "2:4 sparse W4A16 GEMM, K=%d N=%d g=%d, M sweep %s" % (K, N, g, M_SWEEP),
+            "bound": "hbm", "per_m": rows}
 
 
 def main():
@@ -278,6 +360,8 @@ def main():
         log("oracle: %.2f s for one step on %d threads; GPU parity %s (max err %.3g)" %
             (tot, threads, ok, worst))
 
+    sparse = None if args.no_sparse else sparse_section(args, mk, R, synth, torch, np, dev)
+
     small = [r for r in per_m if r["M"] <= 16]
     out = {
         "metric": "W4A16 GEMM TFLOP/s & weight GB/s vs roofline, M=1..128; speedup vs fp16 GEMM",
@@ -312,6 +396,7 @@ def main():
         "wall_ms_per_step": round(wall_ms / args.steps, 6),
         "cpu_baseline": cpu,
         "parity": parity,
+        "sparse_2of4": sparse,
     }
     print(json.dumps(out), flush=True)
 

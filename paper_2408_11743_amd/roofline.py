@@ -46,6 +46,21 @@ def w4a16_bytes(M: int, N: int, K: int, g) -> float:
     return paper_memory_bits(M, N, K) / 8.0 + 2.0 * num_groups(K, g) * N
 
 
+def sparse24_bytes(M: int, N: int, K: int, g) -> float:
+    """2:4 sparse weights (Section 4): half the codes (K*N/4 bytes), 2-bit row
+    indices per kept code (K*N/8 bytes), the same scales, A and C."""
+    return K * N / 4.0 + K * N / 8.0 + 2.0 * num_groups(K, g) * N + 2.0 * M * K + 2.0 * M * N
+
+
+def sparse24_flops(M: int, N: int, K: int) -> float:
+    """Kept multiply-accumulates only: M*N*K/2 of 2 FLOPs each."""
+    return 1.0 * M * N * K
+
+
+def sparse24_t_roof(M, N, K, g, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS) -> float:
+    return t_roof(sparse24_bytes(M, N, K, g), sparse24_flops(M, N, K), bw, peak)
+
+
 def fp16_bytes(M: int, N: int, K: int) -> float:
     return 2.0 * K * N + 2.0 * M * K + 2.0 * M * N
 
