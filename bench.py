@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--no-fp16", action="store_true")
     ap.add_argument("--no-sparse", action="store_true",
                     help="skip the 2:4 sparse section (K = N = 8192, g = 128, M sweep)")
+    ap.add_argument("--sparse-only", action="store_true",
+                    help="run only the 2:4 sparse section and print its JSON (for profiling it alone)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run plain device-to-device copies of this many MB (outside the timed "
                          "region) so hardware byte counters can be scaled against a known size")
@@ -116,9 +118,12 @@ def sparse_section(args, mk, R, synth, torch, np, dev):
         wp, sp = mk.pack(qd, sd, group=g, sparse=sp_flag)
         n = max(2, math.ceil(ROTATION_BYTES / (wp.numel() + 2 * sp.numel())))
         copies[sp_flag] = ([wp] + [wp.clone() for _ in range(n - 1)], sp)
-    w16 = ((qd.to(torch.float32) - 8.0) * sd.to(torch.float32).repeat_interleave(g, dim=0)).to(torch.float16)
-    n16 = max(2, math.ceil(ROTATION_BYTES / (w16.numel() * 2)))
-    w16s = [w16] + [w16.clone() for _ in range(n16 - 1)]
+    w16s, n16 = [], 0
+    if not args.no_fp16:
+        w16 = ((qd.to(torch.float32) - 8.0) * sd.to(torch.float32).repeat_interleave(g, dim=0)).to(torch.float16)
+        n16 = max(2, math.ceil(ROTATION_BYTES / (w16.numel() * 2)))
+        w16s = [w16] + [w16.clone() for _ in range(n16 - 1)]
+        del w16
     ws = mk.Workspace(dev)
     wsbuf = ws.ensure(max(mk.marlin_workspace_bytes(M, N, K, g) for M in M_SWEEP))
     stream = torch.cuda.Stream(device=dev)
@@ -151,7 +156,7 @@ def sparse_section(args, mk, R, synth, torch, np, dev):
         rows.append(rec)
         log("sparse 2:4 %dx%d M=%3d: %.3f us (dense W4 %.3f us, fp16 %s us), roofline frac %.3f" %
             (K, N, M, t[True], t[False], "%.3f" % t16 if t16 else "-", troof / t[True]))
-    del copies, w16s, w16
+    del copies, w16s
     return {"workload": "2:4 sparse W4A16 GEMM, K=%d N=%d g=%d, M sweep %s" % (K, N, g, M_SWEEP),
             "bound": "hbm", "per_m": rows}
 
@@ -175,6 +180,18 @@ def main():
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     mk.lib()
+    if args.calibration_copy_mb:
+        nb = args.calibration_copy_mb << 20
+        src = torch.ones(nb // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration: 3 device copies of %d MiB" % args.calibration_copy_mb)
+        del src, dst
+    if args.sparse_only:
+        print(json.dumps({"sparse_2of4": sparse_section(args, mk, R, synth, torch, np, dev)}), flush=True)
+        return
     K, N, g = K_DIM, N_DIM, GROUP
 
     # ---- weights: pack once, replicate to >= 1 GiB ----
@@ -187,15 +204,6 @@ def main():
     log("weights %dx%d g=%d: %d B packed per copy, %d copies (%.2f GB)" %
         (K, N, g, wbytes, nrot, nrot * wbytes / 1e9))
 
-    if args.calibration_copy_mb:
-        nb = args.calibration_copy_mb << 20
-        src = torch.ones(nb // 4, dtype=torch.int32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        log("calibration: 3 device copies of %d MiB" % args.calibration_copy_mb)
-        del src, dst
 
     acts = {M: torch.from_numpy(synth.activations(WID, M, K)).to(dev) for M in M_SWEEP}
     outs = {M: torch.empty((M, N), dtype=torch.float16, device=dev) for M in M_SWEEP}

@@ -69,10 +69,11 @@ size_t marlin_packed_weight_bytes(int64_t K, int64_t N);
 /* Bytes of the packed scales: 2 * G * N.  Returns 0 for invalid arguments. */
 size_t marlin_packed_scale_bytes(int64_t K, int64_t N, int64_t group);
 
-/* Bytes of the workspace marlin_gemm needs for this problem (arrival
- * counters plus fp32 partial tiles of the Stream-K style split, Section 3.4
- * "Striped Partitioning").  Pure host arithmetic: it makes no HIP call and
- * does not depend on the device.  Returns 0 for invalid arguments. */
+/* Bytes of the workspace marlin_gemm (and marlin_gemm_sparse) needs for
+ * this problem (arrival counters plus fp32 partial tiles of the Stream-K
+ * style split, Section 3.4 "Striped Partitioning").  Pure host arithmetic:
+ * it makes no HIP call and does not depend on the device.  Returns 0 for
+ * invalid arguments. */
 size_t marlin_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t group);
 
 /*

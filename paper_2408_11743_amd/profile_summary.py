@@ -92,10 +92,24 @@ def main() -> None:
     import paper_2408_11743_amd as mk
 
     bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
-    K, N, g = bench["config"]["K"], bench["config"]["N"], bench["config"]["group"]
-    Ms = bench["config"]["M"]
+    import paper_2408_11743_amd.roofline as R
+    sparse = "config" not in bench  # bench.py --sparse-only
+    if sparse:
+        sec = bench["sparse_2of4"]
+        K, N, g = 8192, 8192, 128
+        Ms = [r["M"] for r in sec["per_m"]]
+        bench_per_m = sec["per_m"]
+        describe = {M: mk.marlin_describe_sparse(M, N, K, g) for M in Ms}
+        alg_bytes = R.sparse24_bytes
+        title = "2:4 sparse W4A16 GEMM"
+    else:
+        K, N, g = bench["config"]["K"], bench["config"]["N"], bench["config"]["group"]
+        Ms = bench["config"]["M"]
+        bench_per_m = bench.get("per_m", [])
+        describe = {M: mk.marlin_describe(M, N, K, g) for M in Ms}
+        alg_bytes = R.w4a16_bytes
+        title = "W4A16 GEMM"
     # kernel name as a profiler prints it, e.g. "w4a16_stream_kernel<1, 1, 8, 1, false>"
-    describe = {M: mk.marlin_describe(M, N, K, g) for M in Ms}
     kname = {M: describe[M].split(" cols=")[0] for M in Ms}
 
     # ---- kernel trace ----
@@ -109,22 +123,23 @@ def main() -> None:
         cfg = "cols=" + describe[M].split(" cols=")[1] if " cols=" in describe[M] else ""
         rows.append((M, kname[M], cfg, hits[0][1]["calls"], avg))
         step_ns += avg
-    md = ["# Kernel trace: W4A16 GEMM, K = %d, N = %d, g = %d, M sweep %s" % (K, N, g, Ms), "",
+    md = ["# Kernel trace: %s, K = %d, N = %d, g = %d, M sweep %s" % (title, K, N, g, Ms), "",
           "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
           "Average duration per launch of each kernel instantiation over all its",
           "launches in the run (warm-up included; other kernels, such as the fp16",
           "comparator's, are not matched):", "",
           "| M | kernel | configuration | launches | avg kernel us | bench us per launch |",
           "|---|---|---|---|---|---|"]
-    per_m = {r["M"]: r["us"] for r in bench.get("per_m", [])}
+    per_m = {r["M"]: r["us"] for r in bench_per_m}
     for M, k, cfg, calls, avg in rows:
         md.append("| %d | `%s` | %s | %d | %.3f | %.3f |" % (M, k, cfg, calls, avg / 1e3, per_m.get(M, float("nan"))))
-    bench_avg = bench["roofline"]["avg_launch_us"]
-    md += ["", "Mean over the %d launches of one step: %.3f us of kernel time (rocprofv3)," % (len(Ms), step_ns / len(Ms) / 1e3),
-           "%.3f us per launch measured by bench.py with HIP events over its timed region" % bench_avg,
-           "(`roofline.avg_launch_us`, an unprofiled run: --bench).  The event time of a",
-           "launch also holds the dispatch gap between consecutive graph nodes, which the",
-           "kernel time excludes (an empty kernel costs about 1.7 us per launch in a graph).",
+    md += ["", "Mean over the %d launches of one step: %.3f us of kernel time (rocprofv3)." % (len(Ms), step_ns / len(Ms) / 1e3)]
+    if not sparse:
+        md += ["%.3f us per launch measured by bench.py with HIP events over its timed region" % bench["roofline"]["avg_launch_us"],
+               "(`roofline.avg_launch_us`, an unprofiled run: --bench)."]
+    md += ["The event time of a launch (bench us per launch, graph replays) also holds",
+           "the dispatch gap between consecutive graph nodes, which the kernel time",
+           "excludes (an empty kernel costs about 1.7 us per launch in a graph).",
            "Shared instantiations (same kernel for several M) report one average for all",
            "of their launches, so the per-M rows are approximate where a kernel is shared.", ""]
     open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
@@ -134,10 +149,11 @@ def main() -> None:
     write = counter_per_dispatch(a.write, "WRITE_SIZE")
     copy_bytes = a.copy_mb * (1 << 20)
     # The calibration copies are the largest copy dispatches of the run (the
-    # weight clones bench.py makes use the same copy kernel, on 8.65 MB).
+    # weight clones bench.py makes use the same copy kernel, on smaller
+    # buffers: 8.65 MB packed copies, 134 MB fp16 copies in the sparse section).
     def largest(samples):
         v = [x for n, x in samples if COPY_KERNEL in n]
-        return [x for x in v if x >= 0.5 * max(v)] if v else []
+        return [x for x in v if x >= 0.9 * max(v)] if v else []
 
     cf, cw = largest(fetch), largest(write)
     if not cf or not cw:
@@ -152,7 +168,6 @@ def main() -> None:
         return {k: statistics.median(v) for k, v in out.items()}
 
     fk, wk = per_kernel(fetch, f_scale), per_kernel(write, w_scale)
-    import paper_2408_11743_amd.roofline as R
     trows, hbm = [], {}
     step_bytes = 0.0
     for M in Ms:
@@ -160,11 +175,11 @@ def main() -> None:
         fb, wb = fk.get(k), wk.get(k)
         if fb is None or wb is None:
             raise SystemExit("kernel %s (M=%d) has no counter samples" % (k, M))
-        alg = R.w4a16_bytes(M, N, K, g)
+        alg = alg_bytes(M, N, K, g)
         trows.append((M, k, fb, wb, fb + wb, alg))
         hbm["M=%d %s" % (M, k)] = round(fb + wb)
         step_bytes += fb + wb
-    md = ["# HBM traffic: W4A16 GEMM, K = %d, N = %d, g = %d, M sweep %s" % (K, N, g, Ms), "",
+    md = ["# HBM traffic: %s, K = %d, N = %d, g = %d, M sweep %s" % (title, K, N, g, Ms), "",
           "Commands (two counter passes, each its own run, `TMPDIR=/tmp`):", "", "```",
           a.fetch_cmd, a.write_cmd, "```", "",
           "Calibration: the same runs make plain device copies of %d MiB (the runtime's" % a.copy_mb,
@@ -177,12 +192,13 @@ def main() -> None:
     for M, k, fb, wb, tb, alg in trows:
         md.append("| %d | `%s` | %.2f | %.2f | %.2f | %.2f | %.2f |" % (M, k, fb / 1e6, wb / 1e6, tb / 1e6, alg / 1e6, tb / alg))
     digest = kernel_sources_digest()
-    md += ["", "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N.", "",
+    md += ["", ("Algorithmic bytes: K*N/4 + K*N/8 + 2*(K/g)*N + 2*M*K + 2*M*N (kept codes, row indices)."
+                if sparse else "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N."), "",
            "Step average per launch: %.2f MB (bench.py reports it as `roofline.traffic`" % (step_bytes / len(Ms) / 1e6),
            "while the kernel sources (%s under `paper_2408_11743_amd/csrc/`) hash to `%s...`)." %
            (", ".join(KERNEL_SOURCES), digest[:16]), ""]
     open(a.out + "_traffic.md", "w").write("\n".join(md) + "\n")
-    rec = {"workload": "W4A16 GEMM K=%d N=%d g=%d, M sweep %s (bench.py)" % (K, N, g, Ms),
+    rec = {"workload": "%s K=%d N=%d g=%d, M sweep %s (bench.py)" % (title, K, N, g, Ms),
            "kernel_sources_sha256": digest,
            "counter_scale": {"FETCH_SIZE": round(f_scale, 4), "WRITE_SIZE": round(w_scale, 4),
                              "calibration": "device copies of %d MiB" % a.copy_mb},
