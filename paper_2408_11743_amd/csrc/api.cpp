@@ -69,6 +69,7 @@ struct ForcedConfig {
     int grid = 0;
     int whole = -1;
     int kind = -1;
+    int ks = 0;
 };
 
 static ForcedConfig read_forced()
@@ -84,6 +85,8 @@ static ForcedConfig read_forced()
     if (q) f.whole = atoi(q + 6) ? 1 : 0;
     if (strstr(e, "kind=stream")) f.kind = kKindStream;
     if (strstr(e, "kind=tile")) f.kind = kKindTile;
+    q = strstr(e, "ks=");
+    if (q) f.ks = atoi(q + 3);
     if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
@@ -114,7 +117,14 @@ namespace {
 struct TileCost {
     double unit_us, tail_us, tail_per_contributor_us;
 };
-TileCost tile_cost(int wm) { return {wm == 2 ? 1.55 : 1.50, 10.4, 1.36}; }  // 64 KiB slots
+TileCost tile_cost(int wm, int mbw, int nbw)
+{
+    if (mbw == 4) return {wm == 2 ? 1.55 : 1.50, 10.4, 1.36};  // 64 KiB slots
+    // up to 32 rows (several 128-row blocks per stage): time per unit of
+    // 4 KiB * nbw of weights, measured with whole tiles on 8192 x 28672
+    const double per4k = mbw == 1 ? (nbw == 4 ? 0.195 : 0.23) : (nbw == 2 ? 0.275 : 0.355);
+    return {per4k * nbw, 7.0, 0.5};
+}
 // Stream kernel: the combination costs 2.5 us + 0.5 us per contributor.
 constexpr double kStreamTailUs = 2.5, kStreamTailPerContributorUs = 0.5;
 
@@ -182,6 +192,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     // stream kernel
     cfg.kind = kKindStream;
     cfg.tile_wm = 0;
+    cfg.tile_ks = 0;
     cfg.sparse = sparse ? 1 : 0;
     cfg.mb = (M <= 16) ? 1 : 2;
     cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
@@ -209,29 +220,37 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
             }
         }
     }
-    // tile kernel (M > 32): the activation tile is shared by the four waves,
-    // each of which owns 64 x 64 outputs (2x2 waves beyond 64 rows, else 4x1).
-    if (M > 32 && !sparse && forced().kind != kKindStream) {
+    // tile kernel: the activation tile is shared by the four waves.  Beyond
+    // 32 rows each wave owns 64 x 64 outputs (2x2 waves beyond 64 rows, else
+    // 4x1), one 128-row block per stage; up to 32 rows, 4x1 waves of 16 or 32
+    // rows over 2 or 4 blocks per stage (measured to win only where whole
+    // 128-column tiles fill the chip at 17..32 rows, e.g. N = 28672).
+    if (!sparse && forced().kind != kKindStream) {
         const int wm = M > 64 ? 2 : 1;
         const int mbw = M > 32 ? 4 : M > 16 ? 2 : 1;
         for (int nbw = 4; nbw >= 1; nbw >>= 1) {
-            if (!tile_config_supported(wm, mbw, nbw)) continue;
-            if (forced().nb && nbw != forced().nb) continue;
-            const int cols = (4 / wm) * 16 * nbw, rows = wm * 16 * mbw;
-            if (N % cols != 0) continue;
-            const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
-            const TileCost tc = tile_cost(wm);
-            const Partition pt = best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us);
-            if (pt.t < best) {
-                best = pt.t;
-                cfg.kind = kKindTile;
-                cfg.tile_wm = wm;
-                cfg.nb = nbw;
-                cfg.mb = mbw;
-                cfg.ar = 0;
-                cfg.rg = (M + rows - 1) / rows;
-                cfg.whole = pt.whole;
-                best_grid = pt.grid;
+            for (int ks = 4; ks >= 1; ks >>= 1) {
+                if (!tile_config_supported(wm, mbw, nbw, ks)) continue;
+                if (forced().nb && nbw != forced().nb) continue;
+                if (forced().ks && ks != forced().ks) continue;
+                const int cols = (4 / wm) * 16 * nbw, rows = wm * 16 * mbw;
+                if (N % cols != 0) continue;
+                const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
+                const TileCost tc = tile_cost(wm, mbw, nbw);
+                const Partition pt =
+                    best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us);
+                if (pt.t < best) {
+                    best = pt.t;
+                    cfg.kind = kKindTile;
+                    cfg.tile_wm = wm;
+                    cfg.tile_ks = ks;
+                    cfg.nb = nbw;
+                    cfg.mb = mbw;
+                    cfg.ar = 0;
+                    cfg.rg = (M + rows - 1) / rows;
+                    cfg.whole = pt.whole;
+                    best_grid = pt.grid;
+                }
             }
         }
     }

@@ -32,6 +32,7 @@ struct GemmConfig {
     int tile_wm;  // tile kernel: waves along M (1: 4x1 waves; 2: 2x2 waves); mb, nb: row and
                   // column blocks per wave
     int sparse;   // 2:4 sparse weights (stream kernel only)
+    int tile_ks;  // tile kernel: 128-row blocks of K per work-group stage
 };
 
 // Columns and rows of one tile of a configuration.
@@ -78,7 +79,7 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
-bool tile_config_supported(int wm, int mbw, int nbw);
+bool tile_config_supported(int wm, int mbw, int nbw, int ks);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

@@ -38,19 +38,24 @@ namespace {
 
 using namespace dev;
 
-// Ring depth: stages that fit in LDS (activation rows, then each wave's
-// weights), capped so that the loads of the stages in flight stay within the
-// vmcnt range.
-template <int WN, int WM, int MBW, int NBW>
+// One work-group stage covers KS consecutive 128-row blocks of K of one tile
+// (fewer at the end of a segment: the blocks past it load zeros, which add
+// exactly nothing).  Ring depth: stages that fit in LDS (activation rows,
+// then each wave's weights, per block), capped so that the loads of the
+// stages in flight stay within the vmcnt range.
+template <int WN, int WM, int MBW, int NBW, int KS>
 struct TileShape {
-    static constexpr int TR = 16 * MBW * WM;             // rows of A per tile
-    static constexpr int kAStage = TR * 256;             // bytes of one A stage (TR rows x 128 k x 2 B)
-    static constexpr int kDma = TR / 16;                 // 1-KiB direct-to-LDS A loads per wave per stage
-    static constexpr int kWStage = 4 * NBW * 1024;       // every wave's weights for one stage
+    static constexpr int TR = 16 * MBW * WM;              // rows of A per tile
+    static constexpr int kABlock = TR * 256;              // one block of A (TR rows x 128 k x 2 B)
+    static constexpr int kAStage = KS * kABlock;
+    static constexpr int kWBlock = 4 * NBW * 1024;        // every wave's weights for one block
+    static constexpr int kWStage = KS * kWBlock;
     static constexpr int kStage = kAStage + kWStage;
-    static constexpr int kScratch = (kDma + NBW) * 1024;  // target of the loads issued past the end
-    static constexpr int kSL = NBW == 4 ? 2 : 1;          // scale loads per wave per stage
-    static constexpr int kLoads = kDma + NBW + kSL;       // vector-memory ops per wave per stage
+    static constexpr int kDmaB = TR / 16;                 // 1-KiB direct-to-LDS A loads per wave and block
+    static constexpr int kScratch = (kDmaB + NBW) * 1024;  // target of the loads issued past the end
+    static constexpr int kSLB = NBW == 4 ? 2 : 1;         // scale loads per wave and block
+    static constexpr int kLoads = KS * (kDmaB + NBW + kSLB);  // vector-memory ops per wave per stage
+    static constexpr int kSL = KS * kSLB;
     static constexpr int kLdsBudget = 160 * 1024 - 64;
     static constexpr int kByLds = (kLdsBudget - kScratch) / kStage;
     static constexpr int kByVm = (63 - kSL) / kLoads + 2;  // kSL + (P - 2) * kLoads <= 63
@@ -59,7 +64,7 @@ struct TileShape {
     static_assert(P >= 3, "ring too shallow");
 };
 
-// This lane's column scales of one stage: NBW column blocks x 4 values
+// This lane's column scales of one block: NBW column blocks x 4 values
 // (element 4b + i: block b, output column 4 * (lane / 16) + i of the block).
 template <int NBW>
 struct ScaleFrag {
@@ -72,17 +77,20 @@ struct ScaleFrag<1> {
     __device__ __forceinline__ _Float16 at(int e) const { return v[e & 3]; }
 };
 
-template <int WN, int WM, int MBW, int NBW, bool PER_CHANNEL>
+template <int WN, int WM, int MBW, int NBW, int KS, bool PER_CHANNEL>
 __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 {
     static_assert(WN * WM == 4, "four waves");
     static_assert(NBW == 1 || NBW == 2 || NBW == 4, "column blocks per wave");
     static_assert(MBW >= 1 && MBW <= 4, "row blocks per wave");
-    using S = TileShape<WN, WM, MBW, NBW>;
+    static_assert(KS >= 1 && KS <= 4, "blocks per stage");
+    using S = TileShape<WN, WM, MBW, NBW, KS>;
     constexpr int P = S::P;
     constexpr int TR = S::TR;
+    constexpr int kABlock = S::kABlock;
     constexpr int kAStage = S::kAStage;
-    constexpr int kDma = S::kDma;
+    constexpr int kWBlock = S::kWBlock;
+    constexpr int kDmaB = S::kDmaB;
     constexpr int kStage = S::kStage;
     constexpr int kSL = S::kSL;
     constexpr int kLoads = S::kLoads;
@@ -104,7 +112,10 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     const int c_last = (int)((uint32_t)(u1 - 1) / (uint32_t)KU);
     const int k0 = u0 - c_first * KU;
     const int k1 = u1 - c_last * KU;
-    const int n_st = u1 - u0;  // one 128-row block per stage
+    // stages: ceil(segment length / KS) per segment
+    const int n_st = (c_first == c_last) ? (k1 - k0 + KS - 1) / KS
+                                         : (KU - k0 + KS - 1) / KS + (c_last - c_first - 1) * ((KU + KS - 1) / KS) +
+                                               (k1 + KS - 1) / KS;
 
     // Tile c: column group c / rg (16*NBW*WN columns), row group c % rg (TR rows).
     const uint32_t RG = (uint32_t)p.rg;
@@ -129,9 +140,9 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     // Per-lane address parts.
     const uint32_t w_lane = (uint32_t)lane * 16u;
     const uint32_t s_lane = (uint32_t)lg * 32u;
-    uint32_t a_dma[kDma];  // this wave loads rows [wave*TR/4, (wave+1)*TR/4)
+    uint32_t a_dma[kDmaB];  // this wave loads rows [wave*TR/4, (wave+1)*TR/4) of each block
 #pragma unroll
-    for (int i = 0; i < kDma; ++i) {
+    for (int i = 0; i < kDmaB; ++i) {
         const int r = wave * (TR / 4) + 4 * i + lg;
         a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u;
     }
@@ -146,9 +157,9 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
-    ScaleFrag<NBW> sr[P];
+    ScaleFrag<NBW> sr[P][KS];
 
-    // ---- load cursor: one 128-row block per stage ----
+    // ---- load cursor: KS 128-row blocks per stage ----
     int ld_c = c_first, ld_ku = k0;
     int ld_end = (c_first == c_last) ? k1 : KU;
     uint32_t ld_w = w_tile(ld_c) + ((uint32_t)ld_ku << 12);
@@ -157,39 +168,56 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     uint32_t a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
 
     auto issue = [&](int j) {
-        const bool on = ld_ku < ld_end;
+        const bool on = ld_ku < ld_end;  // the stage's first block is in range
         // Activation rows first (oldest loads of the stage), then this wave's
         // weights, then its scales.  Past the end the direct-to-LDS loads go
         // to the scratch area: other waves may still read every ring slot.
-        const __amdgpu_buffer_rsrc_t ra =
-            __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, on ? a_bytes : 0u, kBufferFlags);
-        uint8_t *dst = on ? a_lds + j * kStage + wave * (kAStage / 4) : a_lds + P * kStage;
+        // A block past the segment end loads through an empty buffer
+        // descriptor (no memory is touched; zeros return, which add nothing).
 #pragma unroll
-        for (int i = 0; i < kDma; ++i)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (__attribute__((address_space(3))) void *)(dst + i * 1024),
-                                                     16, (int)a_dma[i], ld_ku * 256, 0, 0);
-        const __amdgpu_buffer_rsrc_t rw =
-            __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
-        uint8_t *wdst = on ? a_lds + j * kStage + kAStage + wave * NBW * 1024 : a_lds + P * kStage + kDma * 1024;
+        for (int kb = 0; kb < KS; ++kb) {
+            const bool in = ld_ku + kb < ld_end;
+            const __amdgpu_buffer_rsrc_t ra =
+                __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, in ? a_bytes : 0u, kBufferFlags);
+            uint8_t *dst = on ? a_lds + j * kStage + kb * kABlock + wave * (kABlock / 4) : a_lds + P * kStage;
 #pragma unroll
-        for (int b = 0; b < NBW; ++b)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wdst + b * 1024),
-                                                     16, (int)(w_lane + b * 1024), (int)ld_w, 0, kAuxNonTemporal);
-        const __amdgpu_buffer_rsrc_t rs =
-            __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, on ? s_bytes : 0u, kBufferFlags);
-        const uint32_t s_off = PER_CHANNEL ? ld_s : ld_s + ((uint32_t)scale_row_of(ld_ku, p) << 7);
-        if constexpr (NBW == 1) {
-            sr[j].v = __builtin_bit_cast(half4_t, __builtin_amdgcn_raw_buffer_load_b64(rs, s_lane, s_off, 0));
-        } else {
+            for (int i = 0; i < kDmaB; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (__attribute__((address_space(3))) void *)(dst + i * 1024),
+                                                         16, (int)a_dma[i], (ld_ku + kb) * 256, 0, 0);
+        }
 #pragma unroll
-            for (int i = 0; i < NBW / 2; ++i)
-                sr[j].v[i] = __builtin_bit_cast(
-                    half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
+        for (int kb = 0; kb < KS; ++kb) {
+            const bool in = ld_ku + kb < ld_end;
+            const __amdgpu_buffer_rsrc_t rw =
+                __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, in ? w_bytes : 0u, kBufferFlags);
+            uint8_t *wdst = on ? a_lds + j * kStage + kAStage + kb * kWBlock + wave * NBW * 1024
+                               : a_lds + P * kStage + kDmaB * 1024;
+#pragma unroll
+            for (int b = 0; b < NBW; ++b)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wdst + b * 1024),
+                                                         16, (int)(w_lane + b * 1024), (int)(ld_w + kb * 4096u), 0,
+                                                         kAuxNonTemporal);
+        }
+#pragma unroll
+        for (int kb = 0; kb < KS; ++kb) {
+            const bool in = ld_ku + kb < ld_end;
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, in ? s_bytes : 0u, kBufferFlags);
+            const uint32_t soff = PER_CHANNEL ? ld_s : ld_s + ((uint32_t)scale_row_of(ld_ku + kb, p) << 7);
+            if constexpr (NBW == 1) {
+                sr[j][kb].v =
+                    __builtin_bit_cast(half4_t, __builtin_amdgcn_raw_buffer_load_b64(rs, s_lane, soff, 0));
+            } else {
+#pragma unroll
+                for (int i = 0; i < NBW / 2; ++i)
+                    sr[j][kb].v[i] = __builtin_bit_cast(
+                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, soff, 0));
+            }
         }
     };
     auto advance_ld = [&]() {
-        ld_ku += 1;
-        ld_w += 4096u;
+        ld_ku += KS;
+        ld_w += KS * 4096u;
         if (ld_ku >= ld_end) {  // next tile (rare)
             ld_c += 1;
             ld_ku = 0;
@@ -216,53 +244,64 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 #pragma unroll
         for (int mb = 0; mb < MBW; ++mb) acc[b][mb] = zero4;
 
-    // One stage (ring slot j): column block outer, so each dequantized word
-    // feeds the MBW row blocks.
+    // One stage (ring slot j): every operand of the KS blocks is read first,
+    // then per block the column blocks, each dequantized word feeding the MBW
+    // row blocks.
     auto compute = [&](int j) {
-        u32x4_t wv[NBW];     // [column block] this lane's packed weights
-        u32x4_t v[MBW][4];   // [row block][k-step] activation operands
-        const uint32_t wj = w_rd + j * kStage;
+        u32x4_t wv[KS][NBW];     // [block][column block] this lane's packed weights
+        u32x4_t v[KS][MBW][4];   // [block][row block][k-step] activation operands
 #pragma unroll
-        for (int b = 0; b < NBW; ++b) asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(wv[b]) : "v"(wj), "i"(b * 1024));
+        for (int kb = 0; kb < KS; ++kb) {
+            const uint32_t wj = w_rd + j * kStage + kb * kWBlock;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const uint32_t aj = a_rd[t] + j * kStage;
+            for (int b = 0; b < NBW; ++b)
+                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(wv[kb][b]) : "v"(wj), "i"(b * 1024));
 #pragma unroll
-            for (int mb = 0; mb < MBW; ++mb)
-                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v[mb][t]) : "v"(aj), "i"(mb * 4096));
+            for (int t = 0; t < 4; ++t) {
+                const uint32_t aj = a_rd[t] + j * kStage + kb * kABlock;
+#pragma unroll
+                for (int mb = 0; mb < MBW; ++mb)
+                    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v[kb][mb][t]) : "v"(aj), "i"(mb * 4096));
+            }
         }
         // The wait "redefines" the results: no use is scheduled before it.
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int b = 0; b < NBW; ++b) asm volatile("" : "+v"(wv[b]));
+        for (int kb = 0; kb < KS; ++kb) {
 #pragma unroll
-        for (int mb = 0; mb < MBW; ++mb)
+            for (int b = 0; b < NBW; ++b) asm volatile("" : "+v"(wv[kb][b]));
 #pragma unroll
-            for (int t = 0; t < 4; ++t) asm volatile("" : "+v"(v[mb][t]));
+            for (int mb = 0; mb < MBW; ++mb)
 #pragma unroll
-        for (int b = 0; b < NBW; ++b) {
-            if constexpr (PER_CHANNEL) {
+                for (int t = 0; t < 4; ++t) asm volatile("" : "+v"(v[kb][mb][t]));
+        }
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const half8_t w = dequant_magic(wv[b][t], dq);
+        for (int kb = 0; kb < KS; ++kb) {
+#pragma unroll
+            for (int b = 0; b < NBW; ++b) {
+                if constexpr (PER_CHANNEL) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const half8_t w = dequant_magic(wv[kb][b][t], dq);
+#pragma unroll
+                        for (int mb = 0; mb < MBW; ++mb)
+                            acc[b][mb] = mfma(w, __builtin_bit_cast(half8_t, v[kb][mb][t]), acc[b][mb]);
+                    }
+                } else {
+                    float4_t tmp[MBW];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const half8_t w = dequant_magic(wv[kb][b][t], dq);
+#pragma unroll
+                        for (int mb = 0; mb < MBW; ++mb)
+                            tmp[mb] = mfma(w, __builtin_bit_cast(half8_t, v[kb][mb][t]), t == 0 ? zero4 : tmp[mb]);
+                    }
 #pragma unroll
                     for (int mb = 0; mb < MBW; ++mb)
-                        acc[b][mb] = mfma(w, __builtin_bit_cast(half8_t, v[mb][t]), acc[b][mb]);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            acc[b][mb][i] = __builtin_fmaf(tmp[mb][i], (float)sr[j][kb].at(b * 4 + i), acc[b][mb][i]);
                 }
-            } else {
-                float4_t tmp[MBW];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const half8_t w = dequant_magic(wv[b][t], dq);
-#pragma unroll
-                    for (int mb = 0; mb < MBW; ++mb)
-                        tmp[mb] = mfma(w, __builtin_bit_cast(half8_t, v[mb][t]), t == 0 ? zero4 : tmp[mb]);
-                }
-#pragma unroll
-                for (int mb = 0; mb < MBW; ++mb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        acc[b][mb][i] = __builtin_fmaf(tmp[mb][i], (float)sr[j].at(b * 4 + i), acc[b][mb][i]);
             }
         }
     };
@@ -297,7 +336,8 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     int cp_end = (c_first == c_last) ? k1 : KU;
     // A segment is complete: write C (whole tile) or slot 0 (shared first
     // tile).  A shared last tile stays in acc: it is the range's final
-    // segment, combined after the loop.
+    // segment, combined after the loop.  Per-channel scales of the tile came
+    // with the stage's first block.
     auto finish_segment = [&](int j_stage) {
         const bool partial = cp_begin != 0 || cp_end != KU;
         if (partial && cp_c == c_last) {
@@ -315,7 +355,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 #pragma unroll
             for (int j = 0; j < kBlocks; ++j) store_partial(my_slots, own(j), lane, out[j]);
         } else {
-            store_c_scaled(cp_c, out, sr[j_stage]);
+            store_c_scaled(cp_c, out, sr[j_stage][0]);
         }
     };
 
@@ -341,14 +381,14 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
             advance_ld();
             if (live) {
                 compute(j);
-                if (cp_ku + 1 >= cp_end) {
+                if (cp_ku + KS >= cp_end) {
                     finish_segment(j);
                     cp_c += 1;
                     cp_ku = 0;
                     cp_begin = 0;
                     cp_end = (cp_c < c_last) ? KU : k1;
                 } else {
-                    cp_ku += 1;
+                    cp_ku += KS;
                 }
             }
         }
@@ -379,38 +419,44 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
 
 }  // namespace
 
-template <int WN, int WM, int MBW, int NBW>
+template <int WN, int WM, int MBW, int NBW, int KS>
 hipError_t launch_tile(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     GemmProblem arg = p;
     void *args[] = {&arg};
-    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, true>
-                                          : (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, false>;
+    const void *fn = (p.group_units == 0) ? (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, KS, true>
+                                          : (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, KS, false>;
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(256), args, 0, stream);
 }
 
-// Instantiated shapes: 64 x 64 outputs per wave, 4x1 or 2x2 waves.  (Tiles
-// of 16 or 32 rows per wave compile from the same template, but with one
-// 128-row block of K per work-group stage their fixed per-stage cost keeps
-// them behind the stream kernel at every measured shape.)
+// Instantiated shapes (waves along M, row blocks per wave, column blocks per
+// wave, 128-row blocks per stage): 64 x 64 per wave for large batches; for
+// up to 32 rows, 16 or 32 rows per wave over 2 or 4 blocks per stage.
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    switch (cfg.tile_wm * 100 + cfg.mb * 10 + cfg.nb) {
-    case 144: return launch_tile<4, 1, 4, 4>(cfg, p, stream);
-    case 244: return launch_tile<2, 2, 4, 4>(cfg, p, stream);
+    switch (cfg.tile_wm * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.tile_ks) {
+    case 1441: return launch_tile<4, 1, 4, 4, 1>(cfg, p, stream);
+    case 2441: return launch_tile<2, 2, 4, 4, 1>(cfg, p, stream);
+    case 1142: return launch_tile<4, 1, 1, 4, 2>(cfg, p, stream);
+    case 1124: return launch_tile<4, 1, 1, 2, 4>(cfg, p, stream);
+    case 1222: return launch_tile<4, 1, 2, 2, 2>(cfg, p, stream);
+    case 1214: return launch_tile<4, 1, 2, 1, 4>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
-bool tile_config_supported(int wm, int mbw, int nbw)
+bool tile_config_supported(int wm, int mbw, int nbw, int ks)
 {
-    return mbw == 4 && nbw == 4 && (wm == 1 || wm == 2);
+    switch (wm * 1000 + mbw * 100 + nbw * 10 + ks) {
+    case 1441: case 2441: case 1142: case 1124: case 1222: case 1214: return true;
+    default: return false;
+    }
 }
 
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 {
-    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %d, %d, %s>", 4 / cfg.tile_wm, cfg.tile_wm, cfg.mb, cfg.nb,
-             per_channel ? "true" : "false");
+    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %d, %d, %d, %s>", 4 / cfg.tile_wm, cfg.tile_wm, cfg.mb, cfg.nb,
+             cfg.tile_ks, per_channel ? "true" : "false");
 }
 
 }  // namespace marlin

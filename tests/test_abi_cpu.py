@@ -138,7 +138,7 @@ def test_describe_reports_a_launchable_configuration(L):
         assert cols in (16, 32, 64, 128, 256) and N % cols == 0, text
         if text.startswith("w4a16_stream_kernel<"):
             rows = 32
-        else:  # w4a16_tile_kernel<waves along N, waves along M, row blocks, column blocks per wave, ...>
+        else:  # w4a16_tile_kernel<waves along N, waves along M, row blocks, column blocks per wave, ks, ...>
             wn, wm, mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:4])
             assert wn * wm == 4 and cols == wn * 16 * nbw, text
             rows = wm * 16 * mbw
@@ -157,10 +157,14 @@ def test_describe_reports_a_launchable_configuration(L):
 def test_override_selects_the_kernel(monkeypatch):
     # MARLIN_FORCE_CONFIG is read at every call
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile")
-    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 4, 4, false> cols=256 rg=1")
-    assert B.marlin_describe(128, 1024, 1024, -1).startswith("w4a16_tile_kernel<2, 2, 4, 4, true> cols=128 rg=1")
-    assert B.marlin_describe(16, 1024, 1024, 128).startswith("w4a16_stream_kernel<")  # tile kernel: M > 32
-    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1")  # no such tile shape: the stream kernel
+    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 4, 4, 1, false> cols=256 rg=1")
+    assert B.marlin_describe(128, 1024, 1024, -1).startswith("w4a16_tile_kernel<2, 2, 4, 4, 1, true> cols=128 rg=1")
+    # up to 32 rows: 16- or 32-row waves over several 128-row blocks per stage
+    assert B.marlin_describe(16, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 1, ")
+    assert B.marlin_describe(32, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 2, ")
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=4")
+    assert B.marlin_describe(20, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 2, 1, 4, false> cols=64 rg=1")
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=1")  # no such tile shape: the stream kernel
     assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_stream_kernel<")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
     d = B.marlin_describe(128, 1024, 1024, 128)

@@ -126,12 +126,16 @@ def force(monkeypatch):
 
 
 @pytest.mark.parametrize("spec", ["kind=tile", "kind=tile,whole=1", "kind=tile,whole=0,grid=7",
-                                  "kind=tile,whole=0,grid=96", "kind=stream", "kind=stream,whole=0,grid=7",
-                                  "kind=stream,nb=1,whole=1"])
+                                  "kind=tile,whole=0,grid=96", "kind=tile,nb=2,ks=4,whole=0,grid=7",
+                                  "kind=tile,nb=4,ks=2,whole=1", "kind=tile,nb=1,ks=4,whole=0,grid=96",
+                                  "kind=tile,nb=2,ks=2,whole=0,grid=7", "kind=stream",
+                                  "kind=stream,whole=0,grid=7", "kind=stream,nb=1,whole=1"])
 @pytest.mark.parametrize("M", [1, 5, 16, 17, 32, 33, 64, 65, 100, 128])
 @pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
 def test_each_kernel_and_partition(mk, force, spec, M, K, N, g):
-    # Both kernels serve M > 32 (the stream kernel every M); each under each
+    # Both kernels serve every M; each tile shape (64 x 64 per wave beyond
+    # 32 rows; 16 or 32 rows per wave over 2 or 4 blocks per stage up to 32
+    # rows, which also covers segments that end inside a stage) under each
     # partition (whole tiles, and Stream-K splits with several contributors
     # per tile), against the oracle.
     force(spec)
