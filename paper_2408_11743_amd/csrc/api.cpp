@@ -70,6 +70,7 @@ struct ForcedConfig {
     int whole = -1;
     int kind = -1;
     int ks = 0;
+    int nw = 0;
 };
 
 static ForcedConfig read_forced()
@@ -87,6 +88,8 @@ static ForcedConfig read_forced()
     if (strstr(e, "kind=tile")) f.kind = kKindTile;
     q = strstr(e, "ks=");
     if (q) f.ks = atoi(q + 3);
+    q = strstr(e, "nw=");
+    if (q) f.nw = atoi(q + 3);
     if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
@@ -117,8 +120,9 @@ namespace {
 struct TileCost {
     double unit_us, tail_us, tail_per_contributor_us;
 };
-TileCost tile_cost(int wm, int mbw, int nbw)
+TileCost tile_cost(int nw, int wm, int mbw, int nbw)
 {
+    if (nw == 8) return {2.2, 12.0, 1.5};  // 256 x 128 tiles, 128 KiB slots
     if (mbw == 4) return {wm == 2 ? 1.55 : 1.50, 10.4, 1.36};  // 64 KiB slots
     // up to 32 rows (several 128-row blocks per stage): time per unit of
     // 4 KiB * nbw of weights, measured with whole tiles on 8192 x 28672
@@ -193,6 +197,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.kind = kKindStream;
     cfg.tile_wm = 0;
     cfg.tile_ks = 0;
+    cfg.tile_nw = 0;
     cfg.sparse = sparse ? 1 : 0;
     cfg.mb = (M <= 16) ? 1 : 2;
     cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
@@ -220,36 +225,41 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
             }
         }
     }
-    // tile kernel: the activation tile is shared by the four waves.  Beyond
-    // 32 rows each wave owns 64 x 64 outputs (2x2 waves beyond 64 rows, else
-    // 4x1), one 128-row block per stage; up to 32 rows, 4x1 waves of 16 or 32
-    // rows over 2 or 4 blocks per stage (measured to win only where whole
-    // 128-column tiles fill the chip at 17..32 rows, e.g. N = 28672).
+    // tile kernel: the activation tile is shared by the waves of a
+    // work-group.  Beyond 32 rows each wave owns 64 x 64 outputs (four waves:
+    // 2x2 beyond 64 rows, else 4x1; eight waves, two per SIMD: 4x2), one
+    // 128-row block per stage; up to 32 rows, 4x1 waves of 16 or 32 rows over
+    // 2 or 4 blocks per stage (measured to win only where whole 128-column
+    // tiles fill the chip at 17..32 rows, e.g. N = 28672).
     if (!sparse && forced().kind != kKindStream) {
         const int wm = M > 64 ? 2 : 1;
         const int mbw = M > 32 ? 4 : M > 16 ? 2 : 1;
-        for (int nbw = 4; nbw >= 1; nbw >>= 1) {
-            for (int ks = 4; ks >= 1; ks >>= 1) {
-                if (!tile_config_supported(wm, mbw, nbw, ks)) continue;
-                if (forced().nb && nbw != forced().nb) continue;
-                if (forced().ks && ks != forced().ks) continue;
-                const int cols = (4 / wm) * 16 * nbw, rows = wm * 16 * mbw;
-                if (N % cols != 0) continue;
-                const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
-                const TileCost tc = tile_cost(wm, mbw, nbw);
-                const Partition pt =
-                    best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us);
-                if (pt.t < best) {
-                    best = pt.t;
-                    cfg.kind = kKindTile;
-                    cfg.tile_wm = wm;
-                    cfg.tile_ks = ks;
-                    cfg.nb = nbw;
-                    cfg.mb = mbw;
-                    cfg.ar = 0;
-                    cfg.rg = (M + rows - 1) / rows;
-                    cfg.whole = pt.whole;
-                    best_grid = pt.grid;
+        for (int nw = 8; nw >= 4; nw -= 4) {
+            if (forced().nw && nw != forced().nw) continue;
+            for (int nbw = 4; nbw >= 1; nbw >>= 1) {
+                for (int ks = 4; ks >= 1; ks >>= 1) {
+                    if (!tile_config_supported(nw, wm, mbw, nbw, ks)) continue;
+                    if (forced().nb && nbw != forced().nb) continue;
+                    if (forced().ks && ks != forced().ks) continue;
+                    const int cols = (nw / wm) * 16 * nbw, rows = wm * 16 * mbw;
+                    if (N % cols != 0) continue;
+                    const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
+                    const TileCost tc = tile_cost(nw, wm, mbw, nbw);
+                    const Partition pt =
+                        best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us);
+                    if (pt.t < best) {
+                        best = pt.t;
+                        cfg.kind = kKindTile;
+                        cfg.tile_nw = nw;
+                        cfg.tile_wm = wm;
+                        cfg.tile_ks = ks;
+                        cfg.nb = nbw;
+                        cfg.mb = mbw;
+                        cfg.ar = 0;
+                        cfg.rg = (M + rows - 1) / rows;
+                        cfg.whole = pt.whole;
+                        best_grid = pt.grid;
+                    }
                 }
             }
         }

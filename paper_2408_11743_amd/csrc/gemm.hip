@@ -593,7 +593,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_sparse_kernel(GemmProblem p)
 
 int slot_floats(const GemmConfig &cfg)
 {
-    return cfg.kind == kKindTile ? 4 * cfg.nb * cfg.mb * 256 : cfg.nb * cfg.mb * 256;
+    return cfg.kind == kKindTile ? cfg.tile_nw * cfg.nb * cfg.mb * 256 : cfg.nb * cfg.mb * 256;
 }
 
 // Ring depth: stages in flight per wave (weights in registers: NB words of

@@ -33,10 +33,14 @@ struct GemmConfig {
                   // column blocks per wave
     int sparse;   // 2:4 sparse weights (stream kernel only)
     int tile_ks;  // tile kernel: 128-row blocks of K per work-group stage
+    int tile_nw;  // tile kernel: waves per work-group (4 or 8)
 };
 
 // Columns and rows of one tile of a configuration.
-inline int tile_cols(const GemmConfig &c) { return c.kind == kKindTile ? (4 / c.tile_wm) * 16 * c.nb : 16 * c.nb; }
+inline int tile_cols(const GemmConfig &c)
+{
+    return c.kind == kKindTile ? (c.tile_nw / c.tile_wm) * 16 * c.nb : 16 * c.nb;
+}
 inline int tile_rows(const GemmConfig &c) { return c.kind == kKindTile ? c.tile_wm * 16 * c.mb : 16 * c.mb; }
 
 struct GemmProblem {
@@ -79,7 +83,7 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
-bool tile_config_supported(int wm, int mbw, int nbw, int ks);
+bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

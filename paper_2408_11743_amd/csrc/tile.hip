@@ -45,16 +45,21 @@ using namespace dev;
 // stages in flight stay within the vmcnt range.
 template <int WN, int WM, int MBW, int NBW, int KS>
 struct TileShape {
+    static constexpr int NW = WN * WM;                    // waves per work-group
     static constexpr int TR = 16 * MBW * WM;              // rows of A per tile
     static constexpr int kABlock = TR * 256;              // one block of A (TR rows x 128 k x 2 B)
     static constexpr int kAStage = KS * kABlock;
-    static constexpr int kWBlock = 4 * NBW * 1024;        // every wave's weights for one block
+    static constexpr int kWBlock = WN * NBW * 1024;       // the tile's weights for one block
     static constexpr int kWStage = KS * kWBlock;
     static constexpr int kStage = kAStage + kWStage;
-    static constexpr int kDmaB = TR / 16;                 // 1-KiB direct-to-LDS A loads per wave and block
-    static constexpr int kScratch = (kDmaB + NBW) * 1024;  // target of the loads issued past the end
+    static constexpr int kDmaB = TR / (4 * NW);           // 1-KiB direct-to-LDS A loads per wave and block
+    static constexpr int kWDma = NBW / WM;                // 1-KiB weight loads per wave and block (the
+                                                          // WM waves of a column group share them)
+    static constexpr int kScratch = (kDmaB + kWDma) * 1024;  // target of the loads issued past the end
     static constexpr int kSLB = NBW == 4 ? 2 : 1;         // scale loads per wave and block
-    static constexpr int kLoads = KS * (kDmaB + NBW + kSLB);  // vector-memory ops per wave per stage
+    static constexpr int kLoads = KS * (kDmaB + kWDma + kSLB);  // vector-memory ops per wave per stage
+    static_assert(kDmaB >= 1 && TR % (4 * NW) == 0, "activation rows per wave");
+    static_assert(kWDma >= 1 && NBW % WM == 0, "weight blocks per wave");
     static constexpr int kSL = KS * kSLB;
     static constexpr int kLdsBudget = 160 * 1024 - 64;
     static constexpr int kByLds = (kLdsBudget - kScratch) / kStage;
@@ -78,9 +83,9 @@ struct ScaleFrag<1> {
 };
 
 template <int WN, int WM, int MBW, int NBW, int KS, bool PER_CHANNEL>
-__global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
+__global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem p)
 {
-    static_assert(WN * WM == 4, "four waves");
+    static_assert(WN * WM == 4 || WN * WM == 8, "four or eight waves");
     static_assert(NBW == 1 || NBW == 2 || NBW == 4, "column blocks per wave");
     static_assert(MBW >= 1 && MBW <= 4, "row blocks per wave");
     static_assert(KS >= 1 && KS <= 4, "blocks per stage");
@@ -91,6 +96,8 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     constexpr int kAStage = S::kAStage;
     constexpr int kWBlock = S::kWBlock;
     constexpr int kDmaB = S::kDmaB;
+    constexpr int kWDma = S::kWDma;
+    constexpr int NW = S::NW;
     constexpr int kStage = S::kStage;
     constexpr int kSL = S::kSL;
     constexpr int kLoads = S::kLoads;
@@ -143,7 +150,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     uint32_t a_dma[kDmaB];  // this wave loads rows [wave*TR/4, (wave+1)*TR/4) of each block
 #pragma unroll
     for (int i = 0; i < kDmaB; ++i) {
-        const int r = wave * (TR / 4) + 4 * i + lg;
+        const int r = wave * (TR / NW) + 4 * i + lg;
         a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u;
     }
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
@@ -153,7 +160,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
     for (int t = 0; t < 4; ++t)
         a_rd[t] = lds0 + (uint32_t)((wm * 16 * MBW + (lane & 15)) * 256 + (((4 * t + lg) ^ (lane & 15)) << 4));
     // this wave's weights, this lane's 16 bytes (+ 1 KiB per column block)
-    const uint32_t w_rd = lds0 + (uint32_t)(kAStage + wave * NBW * 1024 + lane * 16);
+    const uint32_t w_rd = lds0 + (uint32_t)(kAStage + wn * NBW * 1024 + lane * 16);
     const uint32_t w_bytes = (uint32_t)p.K * (uint32_t)(p.N / 2);
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
 
@@ -179,7 +186,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
             const bool in = ld_ku + kb < ld_end;
             const __amdgpu_buffer_rsrc_t ra =
                 __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, in ? a_bytes : 0u, kBufferFlags);
-            uint8_t *dst = on ? a_lds + j * kStage + kb * kABlock + wave * (kABlock / 4) : a_lds + P * kStage;
+            uint8_t *dst = on ? a_lds + j * kStage + kb * kABlock + wave * (kABlock / NW) : a_lds + P * kStage;
 #pragma unroll
             for (int i = 0; i < kDmaB; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (__attribute__((address_space(3))) void *)(dst + i * 1024),
@@ -190,13 +197,14 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
             const bool in = ld_ku + kb < ld_end;
             const __amdgpu_buffer_rsrc_t rw =
                 __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, in ? w_bytes : 0u, kBufferFlags);
-            uint8_t *wdst = on ? a_lds + j * kStage + kAStage + kb * kWBlock + wave * NBW * 1024
+            // this wave's share of its column group's blocks: wm*kWDma ..
+            uint8_t *wdst = on ? a_lds + j * kStage + kAStage + kb * kWBlock + (wn * NBW + wm * kWDma) * 1024
                                : a_lds + P * kStage + kDmaB * 1024;
 #pragma unroll
-            for (int b = 0; b < NBW; ++b)
+            for (int b = 0; b < kWDma; ++b)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wdst + b * 1024),
-                                                         16, (int)(w_lane + b * 1024), (int)(ld_w + kb * 4096u), 0,
-                                                         kAuxNonTemporal);
+                                                         16, (int)(w_lane + (wm * kWDma + b) * 1024),
+                                                         (int)(ld_w + kb * 4096u), 0, kAuxNonTemporal);
         }
 #pragma unroll
         for (int kb = 0; kb < KS; ++kb) {
@@ -328,7 +336,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_tile_kernel(GemmProblem p)
         }
     };
 
-    const int slot_floats = 4 * kBlocks * 256;
+    const int slot_floats = NW * kBlocks * 256;
     float *const my_slots = p.partials + (int64_t)wg * 2 * slot_floats;  // slot 0; slot 1 follows
     bool has_first = false, has_last = false;
 
@@ -426,7 +434,7 @@ hipError_t launch_tile(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
     void *args[] = {&arg};
     const void *fn = (p.group_units == 0) ? (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, KS, true>
                                           : (const void *)&w4a16_tile_kernel<WN, WM, MBW, NBW, KS, false>;
-    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(256), args, 0, stream);
+    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * WN * WM), args, 0, stream);
 }
 
 // Instantiated shapes (waves along M, row blocks per wave, column blocks per
@@ -434,29 +442,30 @@ hipError_t launch_tile(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 // up to 32 rows, 16 or 32 rows per wave over 2 or 4 blocks per stage.
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    switch (cfg.tile_wm * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.tile_ks) {
-    case 1441: return launch_tile<4, 1, 4, 4, 1>(cfg, p, stream);
-    case 2441: return launch_tile<2, 2, 4, 4, 1>(cfg, p, stream);
-    case 1142: return launch_tile<4, 1, 1, 4, 2>(cfg, p, stream);
-    case 1124: return launch_tile<4, 1, 1, 2, 4>(cfg, p, stream);
-    case 1222: return launch_tile<4, 1, 2, 2, 2>(cfg, p, stream);
-    case 1214: return launch_tile<4, 1, 2, 1, 4>(cfg, p, stream);
+    switch (cfg.tile_nw * 10000 + cfg.tile_wm * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.tile_ks) {
+    case 41441: return launch_tile<4, 1, 4, 4, 1>(cfg, p, stream);
+    case 42441: return launch_tile<2, 2, 4, 4, 1>(cfg, p, stream);
+    case 82441: return launch_tile<4, 2, 4, 4, 1>(cfg, p, stream);
+    case 41142: return launch_tile<4, 1, 1, 4, 2>(cfg, p, stream);
+    case 41124: return launch_tile<4, 1, 1, 2, 4>(cfg, p, stream);
+    case 41222: return launch_tile<4, 1, 2, 2, 2>(cfg, p, stream);
+    case 41214: return launch_tile<4, 1, 2, 1, 4>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
-bool tile_config_supported(int wm, int mbw, int nbw, int ks)
+bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks)
 {
-    switch (wm * 1000 + mbw * 100 + nbw * 10 + ks) {
-    case 1441: case 2441: case 1142: case 1124: case 1222: case 1214: return true;
+    switch (nw * 10000 + wm * 1000 + mbw * 100 + nbw * 10 + ks) {
+    case 41441: case 42441: case 82441: case 41142: case 41124: case 41222: case 41214: return true;
     default: return false;
     }
 }
 
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 {
-    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %d, %d, %d, %s>", 4 / cfg.tile_wm, cfg.tile_wm, cfg.mb, cfg.nb,
-             cfg.tile_ks, per_channel ? "true" : "false");
+    snprintf(buf, n, "w4a16_tile_kernel<%d, %d, %d, %d, %d, %s>", cfg.tile_nw / cfg.tile_wm, cfg.tile_wm, cfg.mb,
+             cfg.nb, cfg.tile_ks, per_channel ? "true" : "false");
 }
 
 }  // namespace marlin

@@ -140,7 +140,7 @@ def test_describe_reports_a_launchable_configuration(L):
             rows = 32
         else:  # w4a16_tile_kernel<waves along N, waves along M, row blocks, column blocks per wave, ks, ...>
             wn, wm, mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:4])
-            assert wn * wm == 4 and cols == wn * 16 * nbw, text
+            assert wn * wm in (4, 8) and cols == wn * 16 * nbw, text
             rows = wm * 16 * mbw
             assert rows >= min(M, 128) or rows == 128, text
         assert int(text.split("rg=")[1].split()[0]) == -(-min(M, 128) // rows), text
@@ -164,6 +164,8 @@ def test_override_selects_the_kernel(monkeypatch):
     assert B.marlin_describe(32, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 2, ")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=4")
     assert B.marlin_describe(20, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 2, 1, 4, false> cols=64 rg=1")
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nw=8")  # eight waves, 2 per SIMD: 256 x 128 tiles
+    assert B.marlin_describe(128, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 2, 4, 4, 1, false> cols=256 rg=1")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=1")  # no such tile shape: the stream kernel
     assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_stream_kernel<")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
