@@ -122,7 +122,8 @@ struct TileCost {
 };
 TileCost tile_cost(int nw, int wm, int mbw, int nbw)
 {
-    if (nw == 8) return {2.2, 12.0, 1.5};  // 256 x 128 tiles, 128 KiB slots
+    if (nw == 8) return mbw == 4 ? TileCost{2.2, 12.0, 1.5}   // 256 x 128 tiles, 128 KiB slots
+                                 : TileCost{1.4, 10.0, 1.0};  // 256 x 64 (to be fitted)
     if (mbw == 4) return {wm == 2 ? 1.55 : 1.50, 10.4, 1.36};  // 64 KiB slots
     // up to 32 rows (several 128-row blocks per stage): time per unit of
     // 4 KiB * nbw of weights, measured with whole tiles on 8192 x 28672
@@ -232,10 +233,12 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     // 2 or 4 blocks per stage (measured to win only where whole 128-column
     // tiles fill the chip at 17..32 rows, e.g. N = 28672).
     if (!sparse && forced().kind != kKindStream) {
-        const int wm = M > 64 ? 2 : 1;
-        const int mbw = M > 32 ? 4 : M > 16 ? 2 : 1;
         for (int nw = 8; nw >= 4; nw -= 4) {
             if (forced().nw && nw != forced().nw) continue;
+            // rows per tile: 64*wm with 64-row waves; eight waves at 33..64
+            // rows use 4x2 waves of 32 rows
+            const int wm = (M > 64 || (nw == 8 && M > 32)) ? 2 : 1;
+            const int mbw = (nw == 8 && M > 32 && M <= 64) ? 2 : M > 32 ? 4 : M > 16 ? 2 : 1;
             for (int nbw = 4; nbw >= 1; nbw >>= 1) {
                 for (int ks = 4; ks >= 1; ks >>= 1) {
                     if (!tile_config_supported(nw, wm, mbw, nbw, ks)) continue;

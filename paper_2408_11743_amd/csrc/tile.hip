@@ -446,6 +446,7 @@ hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStre
     case 41441: return launch_tile<4, 1, 4, 4, 1>(cfg, p, stream);
     case 42441: return launch_tile<2, 2, 4, 4, 1>(cfg, p, stream);
     case 82441: return launch_tile<4, 2, 4, 4, 1>(cfg, p, stream);
+    case 82241: return launch_tile<4, 2, 2, 4, 1>(cfg, p, stream);
     case 41142: return launch_tile<4, 1, 1, 4, 2>(cfg, p, stream);
     case 41124: return launch_tile<4, 1, 1, 2, 4>(cfg, p, stream);
     case 41222: return launch_tile<4, 1, 2, 2, 2>(cfg, p, stream);
@@ -457,7 +458,7 @@ hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStre
 bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks)
 {
     switch (nw * 10000 + wm * 1000 + mbw * 100 + nbw * 10 + ks) {
-    case 41441: case 42441: case 82441: case 41142: case 41124: case 41222: case 41214: return true;
+    case 41441: case 42441: case 82441: case 82241: case 41142: case 41124: case 41222: case 41214: return true;
     default: return false;
     }
 }

@@ -156,7 +156,7 @@ def test_describe_reports_a_launchable_configuration(L):
 
 def test_override_selects_the_kernel(monkeypatch):
     # MARLIN_FORCE_CONFIG is read at every call
-    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile")
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nw=4")
     assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 4, 4, 1, false> cols=256 rg=1")
     assert B.marlin_describe(128, 1024, 1024, -1).startswith("w4a16_tile_kernel<2, 2, 4, 4, 1, true> cols=128 rg=1")
     # up to 32 rows: 16- or 32-row waves over several 128-row blocks per stage
@@ -164,8 +164,9 @@ def test_override_selects_the_kernel(monkeypatch):
     assert B.marlin_describe(32, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 2, ")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=4")
     assert B.marlin_describe(20, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 1, 2, 1, 4, false> cols=64 rg=1")
-    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nw=8")  # eight waves, 2 per SIMD: 256 x 128 tiles
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nw=8")  # eight waves, 2 per SIMD: 256 x 128 / 256 x 64
     assert B.marlin_describe(128, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 2, 4, 4, 1, false> cols=256 rg=1")
+    assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 2, 2, 4, 1, false> cols=256 rg=1")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=1")  # no such tile shape: the stream kernel
     assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_stream_kernel<")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")

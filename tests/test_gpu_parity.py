@@ -129,7 +129,7 @@ def force(monkeypatch):
                                   "kind=tile,whole=0,grid=96", "kind=tile,nb=2,ks=4,whole=0,grid=7",
                                   "kind=tile,nb=4,ks=2,whole=1", "kind=tile,nb=1,ks=4,whole=0,grid=96",
                                   "kind=tile,nb=2,ks=2,whole=0,grid=7", "kind=tile,nw=8",
-                                  "kind=tile,nw=8,whole=1", "kind=tile,nw=8,whole=0,grid=7", "kind=stream",
+                                  "kind=tile,nw=8,whole=1", "kind=tile,nw=8,whole=0,grid=7", "kind=tile,nw=8,whole=0,grid=96", "kind=stream",
                                   "kind=stream,whole=0,grid=7", "kind=stream,nb=1,whole=1"])
 @pytest.mark.parametrize("M", [1, 5, 16, 17, 32, 33, 64, 65, 100, 128])
 @pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
