@@ -145,8 +145,11 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  *
  * The launch configuration comes from a cost model of the device (see
  * marlin_describe).  For tuning and tests, the environment variable
- * MARLIN_FORCE_CONFIG="kind=<stream|tile>,nb=<1|2|4>,whole=<0|1>,grid=<n>"
- * (any subset) overrides it where the shape allows, read at every call;
+ * MARLIN_FORCE_CONFIG="kind=<stream|tile>,nb=<1|2|4>,whole=<0|1>,grid=<n>,
+ * waves=<4|8>,nw=<4|8>,ks=<1|2|4>" (any subset: kernel, column blocks per
+ * tile, partition, work-groups, stream-kernel waves per work-group, tile-kernel
+ * waves and 128-row blocks per stage) overrides it where the shape allows,
+ * read at every call;
  * marlin_workspace_bytes follows the same override, so size the workspace
  * under the setting the calls will see.
  * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,
@@ -164,8 +167,12 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
  * visible), as one NUL-terminated line: the kernel's name with its template
  * arguments as a profiler reports it, then "cols=<columns per tile>
  * rg=<row groups> partition=<whole|streamk> grid=<work-groups>", for the
- * first 128-row pass.  Row groups are of 32 rows for the stream kernel and
- * of 16384 / cols rows for the tile kernel.  Pure host code apart from
+ * first 128-row pass.  The stream kernel's template arguments are
+ * <16-row blocks, 16-column blocks, ring depth, activation rows / 4, waves,
+ * per-channel>, the tile kernel's <waves along N, waves along M, 16-row
+ * blocks per wave, 16-column blocks per wave, 128-row blocks per stage,
+ * per-channel>.  Row groups are of 32 rows for the stream kernel and of the
+ * tile's rows for the tile kernel.  Pure host code apart from
  * reading the device's compute-unit count; enqueues nothing.
  *
  *   buf        host, buf_bytes bytes, written (truncated to fit, always

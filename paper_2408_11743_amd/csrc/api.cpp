@@ -60,10 +60,11 @@ int device_cu_count(int device)
 
 // Tuning and test override, read at every call (a process may change it
 // between calls):
-// MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>,kind=<stream|tile>" forces
-// the stream kernel's column-tile width, the work-group count, the partition
-// and the kernel where the shape allows it (the cost model below is the
-// default).
+// MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>,kind=<stream|tile>,
+// waves=<4|8>,nw=<4|8>,ks=<1|2|4>" forces the column-tile width, the
+// work-group count, the partition, the kernel, the stream kernel's waves per
+// work-group and the tile kernel's waves and blocks per stage where the shape
+// allows it (the cost model below is the default).
 struct ForcedConfig {
     int nb = 0;
     int grid = 0;
@@ -71,6 +72,7 @@ struct ForcedConfig {
     int kind = -1;
     int ks = 0;
     int nw = 0;
+    int waves = 0;
 };
 
 static ForcedConfig read_forced()
@@ -90,6 +92,9 @@ static ForcedConfig read_forced()
     if (q) f.ks = atoi(q + 3);
     q = strstr(e, "nw=");
     if (q) f.nw = atoi(q + 3);
+    q = strstr(e, "waves=");
+    if (q) f.waves = atoi(q + 6);
+    if (f.waves != 4 && f.waves != 8) f.waves = 0;
     if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
@@ -101,16 +106,19 @@ static ForcedConfig forced() { return read_forced(); }
 // Configuration by rows of A per pass (at most 128): mb = 1 (M <= 16) or 2
 // 16-row blocks per row group; beyond 32 rows the pass is split into row
 // groups of 32 that are tiles of their own (a tile is a column tile of one
-// row group); 4 * ar activation rows per group arrive in LDS; kStreamWaves
-// waves split K, kStreamOcc work-groups per CU.
+// row group); 4 * ar activation rows per group arrive in LDS; 4 or (one
+// row block) 8 waves split K, kStreamOcc work-groups per CU.
 //
-// Column tile width (nb 16-column blocks) and partition come from a cost
-// model fitted to MI355X measurements: a work-group streams its weights at a
-// rate that depends on the tile width and the rows of A (narrow tiles and
-// more rows cost more instructions per weight byte), whole tiles per
-// work-group cost ceil(tiles / grid) tiles (idle CUs allowed), and Stream-K
-// costs the average share plus the combination of shared tiles at the end
-// (device-coherent round trips, longer with more contributors per tile).
+// Column tile width (nb 16-column blocks), waves and partition come from a
+// cost model fitted to MI355X measurements (218 whole-tile timings over the
+// Llama-7B and 70B layer shapes, 4% rms): a fixed cost per launch, plus the
+// larger of the busiest work-group's weight bytes over its streaming rate
+// (which depends on the tile width, the rows of A and the waves: narrow tiles
+// and more rows cost more instructions per weight byte) and the layer's
+// weight bytes over the chip's sustained rate.  Whole tiles per work-group
+// cost ceil(tiles / grid) tiles (idle CUs allowed); Stream-K costs the
+// average share plus the combination of shared tiles at the end
+// (device-coherent round trips, longer with larger partial tiles).
 // cus bounds the compute units used (the device's when launching, kMaxCus when
 // sizing the workspace, so that the size does not depend on the device).
 namespace {
@@ -123,37 +131,49 @@ struct TileCost {
 TileCost tile_cost(int nw, int wm, int mbw, int nbw)
 {
     if (nw == 8) return mbw == 4 ? TileCost{2.2, 12.0, 1.5}   // 256 x 128 tiles, 128 KiB slots
-                                 : TileCost{1.4, 10.0, 1.0};  // 256 x 64 (to be fitted)
+                                 : TileCost{1.35, 10.0, 1.0};  // 256 x 64, 64 KiB slots
     if (mbw == 4) return {wm == 2 ? 1.55 : 1.50, 10.4, 1.36};  // 64 KiB slots
     // up to 32 rows (several 128-row blocks per stage): time per unit of
     // 4 KiB * nbw of weights, measured with whole tiles on 8192 x 28672
     const double per4k = mbw == 1 ? (nbw == 4 ? 0.195 : 0.23) : (nbw == 2 ? 0.275 : 0.355);
     return {per4k * nbw, 7.0, 0.5};
 }
-// Stream kernel: the combination costs 2.5 us + 0.5 us per contributor.
-constexpr double kStreamTailUs = 2.5, kStreamTailPerContributorUs = 0.5;
+// Fixed cost of a launch (dispatch, prologue, epilogue), the sustained weight
+// stream of the whole chip, and the stream kernel's combination: 3 us with
+// fp32 partial tiles up to 4 KiB per work-group, 4.5 us with 8 KiB.
+constexpr double kFixedUs = 4.0;
+constexpr double kChipBytesPerUs = 7.0e6;
+double stream_tail_us(int slot_kib) { return slot_kib > 4 ? 4.5 : 3.0; }
 
-// Bytes of weights per microsecond one work-group streams, by rows of A and
-// nb = 4, 2, 1 (measured; the activation rows arrive in LDS in every class).
-double wg_rate(int mb, int ar, int nb)
+// Bytes of weights per microsecond one work-group streams, by rows of A,
+// nb = 4, 2, 1 and waves per work-group (measured; the activation rows arrive
+// in LDS in every class).
+double wg_rate(int mb, int ar, int nb, int waves)
 {
-    static const double r[4][3] = {
-        {24.5e3, 20.7e3, 13.1e3},  // M <= 4
-        {22.9e3, 18.4e3, 12.1e3},  // M <= 8
-        {19.1e3, 15.1e3, 10.4e3},  // M <= 16
-        {13.9e3, 11.5e3, 6.9e3},   // M <= 32 (also each row group of 32 for larger M)
+    static const double r4[4][3] = {
+        {31.8e3, 22.3e3, 13.3e3},  // M <= 4
+        {32.5e3, 20.8e3, 13.0e3},  // M <= 8
+        {25.2e3, 16.6e3, 10.7e3},  // M <= 16
+        {17.6e3, 11.6e3, 7.1e3},   // M <= 32 (also each row group of 32 for larger M)
+    };
+    static const double r8[3][3] = {
+        {38.8e3, 34.2e3, 20.2e3},  // M <= 4
+        {32.7e3, 22.1e3, 15.6e3},  // M <= 8
+        {26.0e3, 16.4e3, 11.0e3},  // M <= 16
     };
     const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : 3;
-    (void)ar;
     const int col = (nb == 4) ? 0 : (nb == 2) ? 1 : 2;
-    return r[row][col];
+    if (waves == 8) return row < 3 ? r8[row][col] : 0.0;
+    return r4[row][col];
 }
 }  // namespace
 
 namespace {
 // Best partition of `tiles` tiles of KU units each over at most `grid`
 // work-groups, given the time of one unit: whole tiles per work-group, or a
-// Stream-K split that pays for combining shared tiles at the end.
+// Stream-K split that pays for combining shared tiles at the end (tail_us,
+// plus tail_per_contributor_us per contributor of a shared tile).  Every
+// launch costs kFixedUs, and no partition streams faster than floor_us.
 struct Partition {
     double t;
     int whole;
@@ -161,12 +181,13 @@ struct Partition {
 };
 
 Partition best_partition(int64_t tiles, int KU, int64_t grid, double unit_us, double tail_us,
-                         double tail_per_contributor_us)
+                         double tail_per_contributor_us, double floor_us)
 {
     Partition best{1e30, 0, 1};
     if (forced().whole != 0) {
         const int64_t g = tiles < grid ? tiles : grid;
-        const double t = (double)((tiles + g - 1) / g) * KU * unit_us;
+        const double stream = (double)((tiles + g - 1) / g) * KU * unit_us;
+        const double t = kFixedUs + (stream > floor_us ? stream : floor_us);
         if (t < best.t) best = {t, 1, g};
     }
     if (forced().whole != 1) {
@@ -176,7 +197,8 @@ Partition best_partition(int64_t tiles, int KU, int64_t grid, double unit_us, do
         const bool split = (units % g) != 0 || (units / g) % KU != 0;
         const double contributors = split ? 1.0 + (double)KU / per : 1.0;
         const double tail = split ? tail_us + tail_per_contributor_us * contributors : 0.0;
-        const double t = per * unit_us + tail;
+        const double stream = per * unit_us;
+        const double t = kFixedUs + (stream > floor_us ? stream : floor_us) + tail;
         if (t < best.t) best = {t, 0, g};
     }
     return best;
@@ -199,6 +221,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.tile_wm = 0;
     cfg.tile_ks = 0;
     cfg.tile_nw = 0;
+    cfg.waves = 4;
     cfg.sparse = sparse ? 1 : 0;
     cfg.mb = (M <= 16) ? 1 : 2;
     cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
@@ -209,20 +232,30 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.whole = 0;
     int64_t best_grid = grid;
     if (forced().kind != kKindTile) {
-        for (int nb = 4; nb >= 1; nb >>= 1) {
-            const double rate = wg_rate(cfg.mb, cfg.ar, nb);
-            if (tiles16 % nb != 0 || rate <= 0.0) continue;
-            if (forced().nb && nb != forced().nb) continue;
-            const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
-            // sparse units carry 3/4 of the dense bytes (codes and row indices)
-            const double unit_bytes = (double)nb * (sparse ? 768.0 : 1024.0);
-            const Partition pt = best_partition(tiles, KU, grid, unit_bytes / rate, kStreamTailUs,
-                                                kStreamTailPerContributorUs);
-            if (pt.t < best) {
-                best = pt.t;
-                cfg.nb = nb;
-                cfg.whole = pt.whole;
-                best_grid = pt.grid;
+        // eight waves exist for one 16-row block only; an override to eight
+        // applies where they do
+        const int forced_waves = (forced().waves == 8 && cfg.mb != 1) ? 4 : forced().waves;
+        for (int waves = 8; waves >= 4; waves -= 4) {
+            if (forced_waves && waves != forced_waves) continue;
+            for (int nb = 4; nb >= 1; nb >>= 1) {
+                const double rate = wg_rate(cfg.mb, cfg.ar, nb, waves);
+                if (tiles16 % nb != 0 || rate <= 0.0) continue;
+                if (forced().nb && nb != forced().nb) continue;
+                const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
+                // sparse units carry 3/4 of the dense bytes (codes and row indices)
+                const double unit_bytes = (double)nb * (sparse ? 768.0 : 1024.0);
+                const double layer_bytes = (double)KU * (double)(tiles16 / nb) * unit_bytes;
+                // fp32 partial tile: 16 x 16 x 4 bytes per block
+                const Partition pt = best_partition(tiles, KU, grid, unit_bytes / rate,
+                                                    stream_tail_us(nb * cfg.mb), 0.0,
+                                                    layer_bytes / kChipBytesPerUs);
+                if (pt.t < best) {
+                    best = pt.t;
+                    cfg.nb = nb;
+                    cfg.waves = waves;
+                    cfg.whole = pt.whole;
+                    best_grid = pt.grid;
+                }
             }
         }
     }
@@ -249,11 +282,12 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
                     const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
                     const TileCost tc = tile_cost(nw, wm, mbw, nbw);
                     const Partition pt =
-                        best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us);
+                        best_partition(tiles, KU, grid, tc.unit_us, tc.tail_us, tc.tail_per_contributor_us, 0.0);
                     if (pt.t < best) {
                         best = pt.t;
                         cfg.kind = kKindTile;
                         cfg.tile_nw = nw;
+                        cfg.waves = 0;
                         cfg.tile_wm = wm;
                         cfg.tile_ks = ks;
                         cfg.nb = nbw;
@@ -269,6 +303,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     }
     if (cfg.nb == 0) {  // only when an override excludes every choice (or asks for the tile kernel, sparse)
         cfg.kind = kKindStream;
+        cfg.waves = 4;
         cfg.nb = (tiles16 % 2 == 0) ? 2 : 1;
         cfg.whole = 0;
         const int64_t units = (int64_t)(tiles16 / cfg.nb) * cfg.rg * KU;
@@ -281,11 +316,10 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
 
 int slot_floats(const GemmConfig &cfg);
 
-// The workspace starts with a fixed region of arrival counters, one per
-// column tile, big enough for the finest tiling (16 columns) of the largest N.
-// It never moves, whatever the shape, so any sequence of calls on one
-// workspace finds every counter it uses at zero; the fp32 partial slots
-// follow it.
+// The workspace starts with a fixed 1 MiB region of arrival counters (one
+// per shared tile, on its own 128-byte line).  It never moves, whatever the
+// shape, so any sequence of calls on one workspace finds every counter it
+// uses at zero; the fp32 partial slots follow it.
 size_t workspace_bytes_for(const GemmConfig &cfg, int N)
 {
     (void)N;

@@ -147,13 +147,20 @@ __device__ __forceinline__ float4_t load_partial(const float *slot, int blk, int
 }
 
 // Combination at the end of a work-group's range.  The first tile (if shared
-// and not also the last) was written to slot 0 when its segment ended; its
-// counter is now bumped.  The last tile (if shared) is in registers
-// (last_out): the counter is read first, and if every other contributor has
-// arrived the work-group adds their slots to its registers and writes C;
-// otherwise it writes slot 1 and arrives with an increment.  Whoever
-// completes a count sums the contributors' slots in work-group order (bitwise
-// reproducible) and resets the counter.  No work-group waits for another.
+// and not also the last) was written to slot 0 when its segment ended; the
+// last tile (if shared) is in registers (last_out) and is written to slot 1
+// now.  The work-group then arrives at each shared tile's counter with an
+// increment; whoever completes a count sums the contributors' slots in
+// work-group order (bitwise reproducible; its own last tile from registers)
+// and resets the counter.  No work-group waits for another.
+//
+// Arrival is not preceded by a look at the counter: with balanced ranges all
+// contributors of a tile finish together, so the look almost never finds the
+// count complete and would only add a device-coherent round trip.  A shared
+// tile's counter is indexed by its first contributor (unique: a work-group
+// that owns the first block of two tiles owns the whole first one) and has a
+// 128-byte line of its own, so concurrent arrivals at different tiles do not
+// queue on one cache line.
 //   KOWN         tile blocks this wave holds;  own(j): slot block index of
 //                block j, or -1 if the wave holds none there
 //   store_c(c, out[KOWN])  writes tile c's C from full sums
@@ -173,23 +180,30 @@ __device__ __forceinline__ void combine_tiles(const GemmProblem &p, int *flags, 
         return p.partials + ((int64_t)w * 2 + (c == w_last ? 1 : 0)) * slot_floats;
     };
     auto others_of = [&](int c) { return unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid); };
-    wait_vmcnt<0>();  // this wave's slot-0 stores are complete
+    auto counter_of = [&](int c) { return p.counters + kCounterStride * unit_owner(p, c * KU, grid); };
+    if (has_last) {
+#pragma unroll
+        for (int j = 0; j < KOWN; ++j)
+            if (own(j) >= 0) store_partial(my_slots + slot_floats, own(j), lane, last_out[j]);
+    }
+    wait_vmcnt<0>();  // this wave's slot stores are complete
     lds_barrier();
     if (threadIdx.x == 0) {
         int f0 = 0, f1 = 0;
         if (has_first) {
-            const uint32_t old =
-                __hip_atomic_fetch_add(p.counters + c_first, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (old == (uint32_t)others_of(c_first)) {
+            uint32_t *const ctr = counter_of(c_first);
+            if (__hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                (uint32_t)others_of(c_first)) {
                 f0 = 1;
-                __hip_atomic_store(p.counters + c_first, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
         if (has_last) {
-            const uint32_t seen = __hip_atomic_load(p.counters + c_last, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (seen == (uint32_t)others_of(c_last)) {
+            uint32_t *const ctr = counter_of(c_last);
+            if (__hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                (uint32_t)others_of(c_last)) {
                 f1 = 1;
-                __hip_atomic_store(p.counters + c_last, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
         flags[0] = f0;
@@ -197,40 +211,34 @@ __device__ __forceinline__ void combine_tiles(const GemmProblem &p, int *flags, 
     }
     lds_barrier();
     const bool reduce_first = has_first && flags[0] != 0;
-    bool reduce_last = has_last && flags[1] != 0;
-    if (has_last && !reduce_last) {
-        // Not every contributor has arrived: publish slot 1 and arrive.
-#pragma unroll
-        for (int j = 0; j < KOWN; ++j)
-            if (own(j) >= 0) store_partial(my_slots + slot_floats, own(j), lane, last_out[j]);
-        wait_vmcnt<0>();
-        lds_barrier();
-        if (threadIdx.x == 0) {
-            const uint32_t old =
-                __hip_atomic_fetch_add(p.counters + c_last, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            int f1 = 0;
-            if (old == (uint32_t)others_of(c_last)) {
-                f1 = 1;
-                __hip_atomic_store(p.counters + c_last, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            flags[1] = f1;
-        }
-        lds_barrier();
-        reduce_last = flags[1] != 0;
-    }
+    const bool reduce_last = has_last && flags[1] != 0;
     // Sum the contributors' slots in work-group order; this work-group's own
     // last-tile sum comes from registers (the same values it would store).
+    // The slots of up to kBatch contributors are loaded before they are added
+    // (past the last contributor the last one is reloaded and ignored), so
+    // their round trips overlap.
+    constexpr int kBatch = KOWN >= 4 ? 1 : 4 / KOWN;
     auto reduce = [&](int c, bool own_in_regs) {
         const int wf = unit_owner(p, c * KU, grid);
         const int wl = unit_owner(p, c * KU + KU - 1, grid);
         float4_t out[KOWN];
-        for (int w = wf; w <= wl; ++w) {
-            const float *slot = slot_of(w, c);
+        for (int w0 = wf; w0 <= wl; w0 += kBatch) {
+            float4_t v[kBatch][KOWN];
 #pragma unroll
-            for (int j = 0; j < KOWN; ++j) {
-                const int blk = own(j) >= 0 ? own(j) : 0;
-                const float4_t v = (own_in_regs && w == wg) ? last_out[j] : load_partial(slot, blk, lane);
-                out[j] = (w == wf) ? v : out[j] + v;
+            for (int b = 0; b < kBatch; ++b) {
+                const int w = w0 + b <= wl ? w0 + b : wl;
+                const float *slot = slot_of(w, c);
+#pragma unroll
+                for (int j = 0; j < KOWN; ++j) {
+                    const int blk = own(j) >= 0 ? own(j) : 0;
+                    v[b][j] = (own_in_regs && w == wg) ? last_out[j] : load_partial(slot, blk, lane);
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < kBatch; ++b) {
+                if (w0 + b > wl) break;
+#pragma unroll
+                for (int j = 0; j < KOWN; ++j) out[j] = (w0 + b == wf) ? v[b][j] : out[j] + v[b][j];
             }
         }
         store_c(c, out);

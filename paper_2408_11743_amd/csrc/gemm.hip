@@ -22,7 +22,9 @@
 //    with the bias add (v_fma_mix_f32 reads the fp16 scale directly);
 //    per-channel scales multiply the final sum ("Groups and Instruction
 //    Ordering").
-//  * The four waves of a work-group take consecutive 128-row blocks of one
+//  * The waves of a work-group (four; eight, two per SIMD, with a single
+//    16-row block of A, so that one wave's dependent MFMA chain and LDS
+//    latency overlap the other's) take consecutive 128-row blocks of one
 //    column tile per stage and meet in LDS when a tile segment ends
 //    (Algorithm 1's reduction over waves that share an output tile).
 //  * Stream-K style striped partitioning over a persistent grid: work-group w
@@ -124,7 +126,7 @@ __device__ __forceinline__ float4_t smfmac2(half8_t w0, half8_t w1, const half8_
 // Register-streaming kernel.
 //
 // A work-group owns a column tile of 16*NB columns (NB 16-column blocks) over
-// a range of 128-row blocks of K (the striped partition); its four waves take
+// a range of 128-row blocks of K (the striped partition); its KW waves take
 // consecutive 128-row blocks of each stage (waves split K), so no weight or
 // activation byte is shared between waves: each lane loads exactly its MFMA
 // operands (16-byte non-temporal buffer loads of the pre-shuffled weights,
@@ -153,10 +155,9 @@ __device__ __forceinline__ float4_t smfmac2(half8_t w0, half8_t w1, const half8_
 // two 16x16x32 steps); codes are converted with the magic number (exact
 // q - 8, no zero-point product: the zero point of a pruned row would depend
 // on the row indices).
-template <int MB, int NB, int D, int AR, bool PER_CHANNEL, bool SPARSE>
+template <int MB, int NB, int D, int AR, int KW, bool PER_CHANNEL, bool SPARSE>
 __device__ __forceinline__ void stream_body(const GemmProblem &p)
 {
-    constexpr int KW = kStreamWaves;
     constexpr int kBlocks = NB * MB;               // 16x16 output blocks per wave
     constexpr int kOwn = (kBlocks + KW - 1) / KW;  // blocks a wave owns after the LDS reduction
     constexpr int kSLoads = (NB + 1) / 2;          // 16-byte scale loads per stage
@@ -173,7 +174,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     constexpr int kARows = 4 * AR;
     constexpr int kAStage = kARows * 256;            // bytes per wave and stage
     constexpr int kLoads = AR + kWL + kSL;           // vector-memory ops per stage
-    static_assert(KW == 4, "four waves per work-group");
+    static_assert(KW == 4 || (KW == 8 && MB == 1), "four waves, or eight with one row block");
     static_assert(MB <= 2 && AR >= 1 && kARows <= 16 * MB, "one or two row blocks, at least 4 rows");
     static_assert((D - 1) * kLoads + kWL + kSL < 64, "vmcnt range");
     __shared__ float4_t red[KW * kBlocks * 64];
@@ -499,7 +500,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     int cp_c = c_first, cp_ku = k0, cp_begin = k0;
     int cp_end = (c_first == c_last) ? k1 : KU;
 
-    // A segment is complete: sum the four waves' tiles in LDS, then write C
+    // A segment is complete: sum the waves' tiles in LDS, then write C
     // (whole column), keep the sum (shared last tile) or write slot 0
     // (shared first tile).
     auto finish_segment = [&]() {
@@ -577,16 +578,16 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
                         own_slot, store_c);
 }
 
-template <int MB, int NB, int D, int AR, bool PER_CHANNEL>
-__global__ void __launch_bounds__(256, 1) w4a16_stream_kernel(GemmProblem p)
+template <int MB, int NB, int D, int AR, int KW, bool PER_CHANNEL>
+__global__ void __launch_bounds__(64 * KW, 1) w4a16_stream_kernel(GemmProblem p)
 {
-    stream_body<MB, NB, D, AR, PER_CHANNEL, false>(p);
+    stream_body<MB, NB, D, AR, KW, PER_CHANNEL, false>(p);
 }
 
-template <int MB, int NB, int D, int AR, bool PER_CHANNEL>
-__global__ void __launch_bounds__(256, 1) w4a16_sparse_kernel(GemmProblem p)
+template <int MB, int NB, int D, int AR, int KW, bool PER_CHANNEL>
+__global__ void __launch_bounds__(64 * KW, 1) w4a16_sparse_kernel(GemmProblem p)
 {
-    stream_body<MB, NB, D, AR, PER_CHANNEL, true>(p);
+    stream_body<MB, NB, D, AR, KW, PER_CHANNEL, true>(p);
 }
 
 }  // namespace
@@ -597,26 +598,31 @@ int slot_floats(const GemmConfig &cfg)
 }
 
 // Ring depth: stages in flight per wave (weights in registers: NB words of
-// 16 bytes per lane per stage, so narrow tiles afford deep rings).
-template <int MB, int NB, int AR>
+// 16 bytes per lane per stage, so narrow tiles afford deep rings).  Eight
+// waves keep as many bytes in flight per work-group with half the depth
+// (and half the LDS ring each).
+template <int MB, int NB, int AR, int KW>
 constexpr int stream_depth()
 {
-    if constexpr (MB == 1) return NB == 4 ? 4 : NB == 2 ? 5 : 8;
+    if constexpr (MB == 1) {
+        constexpr int d = NB == 4 ? 4 : NB == 2 ? 5 : 8;
+        return KW == 8 ? (d + 1) / 2 : d;
+    }
     return NB == 4 ? 3 : 4;  // LDS ring of 32 rows: 8 KiB per wave-stage
 }
 
-template <int MB, int NB, int AR>
+template <int MB, int NB, int AR, int KW>
 hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
-    constexpr int D = stream_depth<MB, NB, AR>();
+    constexpr int D = stream_depth<MB, NB, AR, KW>();
     GemmProblem arg = p;
     void *args[] = {&arg};
     const bool pc = p.group_units == 0;
-    const void *fn = cfg.sparse ? (pc ? (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, true>
-                                      : (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, false>)
-                                : (pc ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, true>
-                                      : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, false>);
-    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * kStreamWaves), args, 0, stream);
+    const void *fn = cfg.sparse ? (pc ? (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, true>
+                                      : (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, false>)
+                                : (pc ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, true>
+                                      : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, false>);
+    return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * KW), args, 0, stream);
 }
 
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
@@ -626,45 +632,63 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
         return;
     }
     int d = 0;
-    switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
-    case 111: d = stream_depth<1, 1, 1>(); break;
-    case 112: d = stream_depth<1, 1, 2>(); break;
-    case 114: d = stream_depth<1, 1, 4>(); break;
-    case 121: d = stream_depth<1, 2, 1>(); break;
-    case 122: d = stream_depth<1, 2, 2>(); break;
-    case 124: d = stream_depth<1, 2, 4>(); break;
-    case 141: d = stream_depth<1, 4, 1>(); break;
-    case 142: d = stream_depth<1, 4, 2>(); break;
-    case 144: d = stream_depth<1, 4, 4>(); break;
-    case 218: d = stream_depth<2, 1, 8>(); break;
-    case 228: d = stream_depth<2, 2, 8>(); break;
-    case 248: d = stream_depth<2, 4, 8>(); break;
+    switch (cfg.waves * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
+    case 4111: d = stream_depth<1, 1, 1, 4>(); break;
+    case 4112: d = stream_depth<1, 1, 2, 4>(); break;
+    case 4114: d = stream_depth<1, 1, 4, 4>(); break;
+    case 4121: d = stream_depth<1, 2, 1, 4>(); break;
+    case 4122: d = stream_depth<1, 2, 2, 4>(); break;
+    case 4124: d = stream_depth<1, 2, 4, 4>(); break;
+    case 4141: d = stream_depth<1, 4, 1, 4>(); break;
+    case 4142: d = stream_depth<1, 4, 2, 4>(); break;
+    case 4144: d = stream_depth<1, 4, 4, 4>(); break;
+    case 4218: d = stream_depth<2, 1, 8, 4>(); break;
+    case 4228: d = stream_depth<2, 2, 8, 4>(); break;
+    case 4248: d = stream_depth<2, 4, 8, 4>(); break;
+    case 8111: d = stream_depth<1, 1, 1, 8>(); break;
+    case 8112: d = stream_depth<1, 1, 2, 8>(); break;
+    case 8114: d = stream_depth<1, 1, 4, 8>(); break;
+    case 8121: d = stream_depth<1, 2, 1, 8>(); break;
+    case 8122: d = stream_depth<1, 2, 2, 8>(); break;
+    case 8124: d = stream_depth<1, 2, 4, 8>(); break;
+    case 8141: d = stream_depth<1, 4, 1, 8>(); break;
+    case 8142: d = stream_depth<1, 4, 2, 8>(); break;
+    case 8144: d = stream_depth<1, 4, 4, 8>(); break;
     default: break;
     }
     if (d == 0) {
         if (n) buf[0] = 0;
         return;
     }
-    snprintf(buf, n, "%s<%d, %d, %d, %d, %s>", cfg.sparse ? "w4a16_sparse_kernel" : "w4a16_stream_kernel", cfg.mb,
-             cfg.nb, d, cfg.ar, per_channel ? "true" : "false");
+    snprintf(buf, n, "%s<%d, %d, %d, %d, %d, %s>", cfg.sparse ? "w4a16_sparse_kernel" : "w4a16_stream_kernel",
+             cfg.mb, cfg.nb, d, cfg.ar, cfg.waves, per_channel ? "true" : "false");
 }
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     if (cfg.kind == kKindTile) return launch_tile_gemm(cfg, p, stream);
-    switch (cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
-    case 111: return launch_stream<1, 1, 1>(cfg, p, stream);
-    case 112: return launch_stream<1, 1, 2>(cfg, p, stream);
-    case 114: return launch_stream<1, 1, 4>(cfg, p, stream);
-    case 121: return launch_stream<1, 2, 1>(cfg, p, stream);
-    case 122: return launch_stream<1, 2, 2>(cfg, p, stream);
-    case 124: return launch_stream<1, 2, 4>(cfg, p, stream);
-    case 141: return launch_stream<1, 4, 1>(cfg, p, stream);
-    case 142: return launch_stream<1, 4, 2>(cfg, p, stream);
-    case 144: return launch_stream<1, 4, 4>(cfg, p, stream);
-    case 218: return launch_stream<2, 1, 8>(cfg, p, stream);
-    case 228: return launch_stream<2, 2, 8>(cfg, p, stream);
-    case 248: return launch_stream<2, 4, 8>(cfg, p, stream);
+    switch (cfg.waves * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
+    case 4111: return launch_stream<1, 1, 1, 4>(cfg, p, stream);
+    case 4112: return launch_stream<1, 1, 2, 4>(cfg, p, stream);
+    case 4114: return launch_stream<1, 1, 4, 4>(cfg, p, stream);
+    case 4121: return launch_stream<1, 2, 1, 4>(cfg, p, stream);
+    case 4122: return launch_stream<1, 2, 2, 4>(cfg, p, stream);
+    case 4124: return launch_stream<1, 2, 4, 4>(cfg, p, stream);
+    case 4141: return launch_stream<1, 4, 1, 4>(cfg, p, stream);
+    case 4142: return launch_stream<1, 4, 2, 4>(cfg, p, stream);
+    case 4144: return launch_stream<1, 4, 4, 4>(cfg, p, stream);
+    case 4218: return launch_stream<2, 1, 8, 4>(cfg, p, stream);
+    case 4228: return launch_stream<2, 2, 8, 4>(cfg, p, stream);
+    case 4248: return launch_stream<2, 4, 8, 4>(cfg, p, stream);
+    case 8111: return launch_stream<1, 1, 1, 8>(cfg, p, stream);
+    case 8112: return launch_stream<1, 1, 2, 8>(cfg, p, stream);
+    case 8114: return launch_stream<1, 1, 4, 8>(cfg, p, stream);
+    case 8121: return launch_stream<1, 2, 1, 8>(cfg, p, stream);
+    case 8122: return launch_stream<1, 2, 2, 8>(cfg, p, stream);
+    case 8124: return launch_stream<1, 2, 4, 8>(cfg, p, stream);
+    case 8141: return launch_stream<1, 4, 1, 8>(cfg, p, stream);
+    case 8142: return launch_stream<1, 4, 2, 8>(cfg, p, stream);
+    case 8144: return launch_stream<1, 4, 4, 8>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -15,7 +15,8 @@ namespace marlin {
 //   ar   : 0, or (mb <= 2) the activation rows arrive in LDS, 4 * ar of them
 //   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
 //   grid : work-groups
-constexpr int kStreamWaves = 4;  // waves per work-group (they split K)
+//   waves: stream kernel waves per work-group (they split K): 4, or 8 (two per
+//          SIMD) with one 16-row block
 constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
 constexpr int kKindStream = 0;  // w4a16_stream_kernel (any M; row groups of 32)
@@ -34,6 +35,7 @@ struct GemmConfig {
     int sparse;   // 2:4 sparse weights (stream kernel only)
     int tile_ks;  // tile kernel: 128-row blocks of K per work-group stage
     int tile_nw;  // tile kernel: waves per work-group (4 or 8)
+    int waves;    // stream kernel: waves per work-group (4 or 8)
 };
 
 // Columns and rows of one tile of a configuration.
@@ -49,7 +51,7 @@ struct GemmProblem {
     const uint16_t *S;
     uint16_t *C;
     float *partials;      // fp32 partial tiles, 2 slots per work-group
-    uint32_t *counters;   // one arrival counter per column tile
+    uint32_t *counters;   // arrival counters: one per shared tile, kCounterStride words apart
     int M;                // rows in this pass (1 .. 32 * rg)
     int rg;               // row groups (tiles = column tiles * rg)
     int N;
@@ -68,9 +70,15 @@ struct GemmProblem {
 // computed with this bound, never with the device's.
 constexpr int kMaxCus = 256;
 constexpr int kMaxPerCu = 2;  // work-groups per compute unit, at most
-// Arrival counters at the start of every workspace: one per tile for the
-// finest tiling of the largest N (2^20 / 16 column tiles, 4 row groups).
+// Arrival counters at the start of every workspace.  A shared tile's counter
+// is indexed by the tile's first contributor (a work-group index, below
+// kMaxCus * kMaxPerCu) and sits kCounterStride words (one 128-byte line)
+// from the next.  The region keeps its size of 1 MiB (it held one counter
+// per tile of the finest tiling of the largest N before) so that the
+// workspace layout, and a caller's once-zeroed workspace, stay valid.
+constexpr int kCounterStride = 32;
 constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4 * 4;
+static_assert((size_t)kMaxCus * kMaxPerCu * kCounterStride * 4 <= kCounterRegionBytes, "counter region");
 
 // Device facts cached per device.
 int device_cu_count(int device);

@@ -169,6 +169,13 @@ def test_override_selects_the_kernel(monkeypatch):
     assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_tile_kernel<4, 2, 2, 4, 1, false> cols=256 rg=1")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nb=1,ks=1")  # no such tile shape: the stream kernel
     assert B.marlin_describe(64, 1024, 1024, 128).startswith("w4a16_stream_kernel<")
+    # stream kernel: <mb, nb, ring depth, activation rows / 4, waves, per-channel>;
+    # eight waves (half-depth rings) with one 16-row block, else four
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=1,whole=1,waves=8")
+    assert B.marlin_describe(1, 4096, 4096, 128).startswith("w4a16_stream_kernel<1, 1, 4, 1, 8, false> cols=16")
+    assert B.marlin_describe(32, 4096, 4096, 128).startswith("w4a16_stream_kernel<2, 1, 4, 8, 4, false>")
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=1,whole=1,waves=4")
+    assert B.marlin_describe(1, 4096, 4096, 128).startswith("w4a16_stream_kernel<1, 1, 8, 1, 4, false> cols=16")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
     d = B.marlin_describe(128, 1024, 1024, 128)
     assert d.startswith("w4a16_stream_kernel<") and "cols=32 rg=4 partition=streamk grid=7" in d, d

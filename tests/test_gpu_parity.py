@@ -145,6 +145,24 @@ def test_each_kernel_and_partition(mk, force, spec, M, K, N, g):
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
 
 
+@pytest.mark.parametrize("waves", [4, 8])
+@pytest.mark.parametrize("nb", [1, 2, 4])
+@pytest.mark.parametrize("part", ["whole=1", "whole=0,grid=7", "whole=0,grid=96"])
+@pytest.mark.parametrize("M", [1, 6, 13])
+@pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1)])
+def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
+    # The stream kernel with four and with eight waves per work-group, every
+    # column-tile width and activation-row class (4, 8, 16 rows in LDS), whole
+    # tiles and Stream-K splits (7 work-groups: long ranges over several
+    # tiles; 96: several contributors per tile), grouped and per-channel.
+    spec = "kind=stream,waves=%d,nb=%d,%s" % (waves, nb, part)
+    force(spec)
+    assert (", %d, %s>" % (waves, "true" if g == -1 else "false")) in mk.marlin_describe(M, N, K, g)
+    q, s = synth.weights(7, K, N, None if g == -1 else g)
+    A = synth.activations(7, M, K)
+    check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
+
+
 @pytest.mark.parametrize("M", [130, 200, 256])
 def test_M_above_128_runs_in_passes(mk, M):
     K, N = 1024, 512

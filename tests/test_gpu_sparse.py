@@ -83,15 +83,17 @@ def force(monkeypatch):
     return set_
 
 
+@pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("spec", ["nb=1,whole=1", "nb=2,whole=0,grid=7", "nb=4,whole=0,grid=96", "whole=0,grid=7",
                                   "nb=4,whole=1"])
-@pytest.mark.parametrize("M", [1, 16, 32, 100])
-def test_sparse_each_partition(mk, force, spec, M):
-    force(spec)
+@pytest.mark.parametrize("M", [1, 6, 16, 32, 100])
+def test_sparse_each_partition(mk, force, waves, spec, M):
+    # eight waves apply up to 16 rows; beyond, the override falls back to four
+    force("%s,waves=%d" % (spec, waves))
     K, N, g = 2048, 1024, 128
     q, keep, s = synth.sparse24_weights(43, K, N, g)
     A = synth.activations(43, M, K)
-    check_close(run_sparse(mk, A, q, s, g), oracle.gemm(A, q, s, g), "sparse %s M=%d" % (spec, M))
+    check_close(run_sparse(mk, A, q, s, g), oracle.gemm(A, q, s, g), "sparse %s waves=%d M=%d" % (spec, waves, M))
 
 
 @pytest.mark.parametrize("M", [1, 32, 128])
