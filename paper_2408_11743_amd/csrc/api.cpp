@@ -399,6 +399,10 @@ marlin_status_t gemm_impl(const uint16_t *A, const void *w_packed, const void *s
         // Exact for every block index below 2^13 (K <= 2^20): with
         // e = gmagic * gu - 2^26 < gu <= 2^13, ku * e < 2^26.
         p.gmagic = gu > 0 ? (uint32_t)((((uint64_t)1 << 26) + (uint64_t)gu - 1) / (uint64_t)gu) : 0u;
+        // w * extra < grid^2 <= 2^18, so w * extra * grid < 2^27: always exact
+        p.grid_magic = reciprocal32((uint64_t)cfg.grid);
+        // units below p.units: exact when p.units * KU <= 2^32
+        p.ku_magic = (uint64_t)p.units * (uint64_t)p.KU <= ((uint64_t)1 << 32) ? reciprocal32((uint64_t)p.KU) : 0u;
         const hipError_t e = launch_gemm(cfg, p, stream);
         if (e != hipSuccess) return MARLIN_ERR_HIP;
     }

@@ -105,11 +105,19 @@ __device__ __forceinline__ int xcd_local_wg(int b, int grid)
 }
 
 // First unit of work-group w: gran * floor(w * (units / gran) / grid), from
-// the host's quotient and remainder so that no 64-bit division is needed.
-// gran = KU hands out whole tiles; gran = 1 splits tiles (Stream-K).
+// the host's quotient and remainder and its reciprocal of grid, so that no
+// division is needed.  gran = KU hands out whole tiles; gran = 1 splits tiles
+// (Stream-K).  grid is the launch's (the reciprocal was made for it).
 __device__ __forceinline__ int range_start(const GemmProblem &p, int w, int grid)
 {
-    return (w * p.per_wg + (int)((uint32_t)(w * p.extra) / (uint32_t)grid)) * p.gran;
+    (void)grid;
+    return (w * p.per_wg + (int)__umulhi((uint32_t)(w * p.extra), p.grid_magic)) * p.gran;
+}
+
+// Tile of unit u: u / KU, by the host's reciprocal where that is exact.
+__device__ __forceinline__ int tile_of(const GemmProblem &p, int u)
+{
+    return p.ku_magic ? (int)__umulhi((uint32_t)u, p.ku_magic) : (int)((uint32_t)u / (uint32_t)p.KU);
 }
 
 // Work-group that owns unit u: the largest w with range_start(w) <= u
@@ -176,7 +184,7 @@ __device__ __forceinline__ void combine_tiles(const GemmProblem &p, int *flags, 
     // Contributors of tile c: work-groups owner(c*KU) .. owner(c*KU + KU - 1);
     // the slot a contributor used for c: 1 if c is its last tile, else 0.
     auto slot_of = [&](int w, int c) -> const float * {
-        const int w_last = (int)((uint32_t)(range_start(p, w + 1, grid) - 1) / (uint32_t)KU);
+        const int w_last = tile_of(p, range_start(p, w + 1, grid) - 1);
         return p.partials + ((int64_t)w * 2 + (c == w_last ? 1 : 0)) * slot_floats;
     };
     auto others_of = [&](int c) { return unit_owner(p, c * KU + KU - 1, grid) - unit_owner(p, c * KU, grid); };

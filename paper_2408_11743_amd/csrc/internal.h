@@ -64,7 +64,17 @@ struct GemmProblem {
     int extra;            // (units / gran) % grid
     int group_units;      // 128-row blocks per scale group; 0 = per-channel
     uint32_t gmagic;      // ceil(2^26 / group_units): row of block ku = (ku * 2^6 * gmagic) >> 32
+    uint32_t grid_magic;  // ceil(2^32 / grid) (0 for grid 1): w * extra / grid = mulhi(w * extra, grid_magic)
+    uint32_t ku_magic;    // ceil(2^32 / KU) where u / KU = mulhi(u, ku_magic) for every unit u, else 0
 };
+
+// ceil(2^32 / d) for 2 <= d: with it, floor(n / d) = floor(n * m / 2^32) for
+// every n with n * d <= 2^32 (m = (2^32 + e) / d, 0 <= e < d, so the error
+// n * e / (d 2^32) stays below 1/d).  0 when d < 2.
+inline uint32_t reciprocal32(uint64_t d)
+{
+    return d < 2 ? 0u : (uint32_t)((((uint64_t)1 << 32) + d - 1) / d);
+}
 
 // Upper bound on compute units used (MI355X has 256).  Workspace sizes are
 // computed with this bound, never with the device's.

@@ -115,8 +115,8 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
     const int wg = xcd_local_wg(blockIdx.x, grid);
     const int u0 = range_start(p, wg, grid);
     const int u1 = range_start(p, wg + 1, grid);
-    const int c_first = (int)((uint32_t)u0 / (uint32_t)KU);
-    const int c_last = (int)((uint32_t)(u1 - 1) / (uint32_t)KU);
+    const int c_first = tile_of(p, u0);
+    const int c_last = tile_of(p, u1 - 1);
     const int k0 = u0 - c_first * KU;
     const int k1 = u1 - c_last * KU;
     // stages: ceil(segment length / KS) per segment

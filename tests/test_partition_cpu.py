@@ -6,14 +6,16 @@ The kernel gives work-group w the unit range [w*T/grid, (w+1)*T/grid) of
 grid.  It walks the range in stages of KW blocks that never cross a column
 tile.  A tile covered only in part is combined across work-groups: the
 work-group's first tile (when shared and not also its last) goes to slot 0
-when its segment ends; its last tile (when shared) is kept in registers and
-either reduced at once, if every other contributor has already arrived, or
-written to slot 1.  This model re-states that schedule and the arrival
+when its segment ends; its last tile (when shared) goes to slot 1 at the end
+of the range; then the work-group arrives at each shared tile's counter, and
+whoever completes a count reduces.  A shared tile's counter is indexed by
+its first contributor.  This model re-states that schedule and the arrival
 protocol in Python and checks, for many shapes and grid sizes, that every
 unit is computed exactly once, the closed-form stage count matches the walk,
-the slot a reducer reads is the slot its writer used, every shared tile is
-reduced exactly once whatever the arrival order, and every counter returns
-to zero.
+the slot a reducer reads is the slot its writer used, no two shared tiles
+share a counter, every shared tile is reduced exactly once whatever the
+arrival order, and every counter returns to zero.  The divisions the kernel
+replaces by host-computed reciprocals are checked for exactness.
 """
 import random
 
@@ -86,24 +88,21 @@ def model(cols, KU, grid, KW, rng):
                 assert w not in shared.get(c, {})
                 shared.setdefault(c, {})[w] = kind
     assert len(seen) == total and all(v == 1 for v in seen.values())
+    firsts = [contributors(c, KU, total, grid)[0] for c in shared]
+    assert len(set(firsts)) == len(firsts), "two shared tiles on one counter"
     for c, who in shared.items():
         wf, wl = contributors(c, KU, total, grid)
         assert sorted(who) == list(range(wf, wl + 1)), c
         for w, kind in who.items():
             assert reader_slot(w, c, KU, total, grid) == (1 if kind == "last" else 0)
-        # arrival protocol under random orders: "first" contributors arrive
-        # with an increment; "last" ones peek, and arrive only if the peek
-        # does not show every other contributor.
+        # arrival protocol under random orders: every contributor arrives
+        # with an increment; the one that completes the count reduces.
         for _ in range(8):
             counter, reducers = 0, []
             order = list(who)
             rng.shuffle(order)
             others = wl - wf
             for w in order:
-                if who[w] == "last" and counter == others:
-                    reducers.append(w)
-                    counter = 0
-                    continue
                 old = counter
                 counter += 1
                 if old == others:
@@ -138,6 +137,47 @@ def test_scale_row_magic_exact():
         m = ((1 << 26) + gu - 1) // gu
         for ku in list(range(0, 300)) + list(range(8192 - 300, 8192)):
             assert ((ku << 6) * m) >> 32 == ku // gu, (gu, ku)
+
+
+def reciprocal32(d):
+    return 0 if d < 2 else ((1 << 32) + d - 1) // d
+
+
+def mulhi(a, b):
+    return (a * b) >> 32
+
+
+@pytest.mark.parametrize("d", list(range(2, 300)) + [448, 511, 512, 1000, 4096, 8192, 65535])
+def test_reciprocal_division_exact(d):
+    # floor(n / d) = mulhi(n, ceil(2^32 / d)) whenever n * d <= 2^32
+    m = reciprocal32(d)
+    assert m < (1 << 32)
+    top = (1 << 32) // d
+    ns = list(range(0, 2000)) + list(range(max(0, top - 2000), top + 1))
+    ns += [k * d + r for k in (1, 7, top // d // 2) for r in (0, 1, d - 1) if k * d + r <= top]
+    for n in ns:
+        assert mulhi(n, m) == n // d, (n, d)
+
+
+@pytest.mark.parametrize("grid", [1, 2, 3, 7, 64, 96, 172, 255, 256, 448, 512])
+def test_range_start_by_reciprocal(grid):
+    # w * extra / grid with extra < grid and w <= grid, as the kernel computes it
+    m = reciprocal32(grid)
+    for extra in ({0, 1, grid // 3, grid - 1} if grid > 1 else {0}):
+        for w in range(grid + 1):
+            assert mulhi(w * extra, m) == (w * extra) // grid
+
+
+@pytest.mark.parametrize("cols,KU", [(256, 32), (1792, 64), (512, 224), (65536, 32), (4096, 512)])
+def test_tile_of_by_reciprocal(cols, KU):
+    # u / KU for every unit u < units when units * KU <= 2^32 (else the
+    # kernel divides)
+    units = cols * KU
+    if units * KU > (1 << 32):
+        return
+    m = reciprocal32(KU)
+    for u in list(range(0, 5000)) + list(range(units - 5000, units)):
+        assert mulhi(u, m) == u // KU
 
 
 def xcd_local_wg(b, grid, xcds=8):
