@@ -107,7 +107,8 @@ static ForcedConfig forced() { return read_forced(); }
 // 16-row blocks per row group; beyond 32 rows the pass is split into row
 // groups of 32 that are tiles of their own (a tile is a column tile of one
 // row group); 4 * ar activation rows per group arrive in LDS; 4 or (one
-// row block) 8 waves split K, kStreamOcc work-groups per CU.
+// row block, or one column block) 8 waves split K, kStreamOcc work-groups
+// per CU.
 //
 // Column tile width (nb 16-column blocks), waves and partition come from a
 // cost model fitted to MI355X measurements (218 whole-tile timings over the
@@ -163,7 +164,7 @@ double wg_rate(int mb, int ar, int nb, int waves)
     };
     const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : 3;
     const int col = (nb == 4) ? 0 : (nb == 2) ? 1 : 2;
-    if (waves == 8) return row < 3 ? r8[row][col] : 0.0;
+    if (waves == 8) return row < 3 ? r8[row][col] : (nb == 1 ? 7.4e3 : 0.0);
     return r4[row][col];
 }
 }  // namespace
@@ -232,9 +233,10 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.whole = 0;
     int64_t best_grid = grid;
     if (forced().kind != kKindTile) {
-        // eight waves exist for one 16-row block only; an override to eight
-        // applies where they do
-        const int forced_waves = (forced().waves == 8 && cfg.mb != 1) ? 4 : forced().waves;
+        // eight waves exist for one 16-row block, or two with one 16-column
+        // block; an override to eight applies where they do
+        const int forced_waves =
+            (forced().waves == 8 && cfg.mb != 1 && forced().nb > 1) ? 4 : forced().waves;
         for (int waves = 8; waves >= 4; waves -= 4) {
             if (forced_waves && waves != forced_waves) continue;
             for (int nb = 4; nb >= 1; nb >>= 1) {

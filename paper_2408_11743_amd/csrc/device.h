@@ -35,6 +35,19 @@ __device__ __forceinline__ void wait_lgkmcnt0()
     asm volatile("" ::: "memory");
 }
 
+// Keeps every memory operation and every instruction on its side: neither
+// the IR passes (the memory clobber) nor the machine scheduler (the
+// scheduling barrier) move loads across it.  The kernels wait for their
+// direct-to-LDS loads by counting the vector-memory operations issued after
+// them (they complete in order), which holds only if the loads are emitted in
+// the order the code issues them; the compiler is otherwise free to
+// interleave independent loads.
+__device__ __forceinline__ void issue_order_point()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // Work-group barrier that does not wait for outstanding global loads.
 __device__ __forceinline__ void lds_barrier()
 {

@@ -23,8 +23,8 @@
 //    per-channel scales multiply the final sum ("Groups and Instruction
 //    Ordering").
 //  * The waves of a work-group (four; eight, two per SIMD, with a single
-//    16-row block of A, so that one wave's dependent MFMA chain and LDS
-//    latency overlap the other's) take consecutive 128-row blocks of one
+//    16-row block of A or a single 16-column block, so that one wave's
+//    dependent MFMA chain and LDS latency overlap the other's) take consecutive 128-row blocks of one
 //    column tile per stage and meet in LDS when a tile segment ends
 //    (Algorithm 1's reduction over waves that share an output tile).
 //  * Stream-K style striped partitioning over a persistent grid: work-group w
@@ -174,7 +174,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     constexpr int kARows = 4 * AR;
     constexpr int kAStage = kARows * 256;            // bytes per wave and stage
     constexpr int kLoads = AR + kWL + kSL;           // vector-memory ops per stage
-    static_assert(KW == 4 || (KW == 8 && MB == 1), "four waves, or eight with one row block");
+    static_assert(KW == 4 || (KW == 8 && (MB == 1 || NB == 1)), "four waves, or eight with one row block or column block");
     static_assert(MB <= 2 && AR >= 1 && kARows <= 16 * MB, "one or two row blocks, at least 4 rows");
     static_assert((D - 1) * kLoads + kWL + kSL < 64, "vmcnt range");
     __shared__ float4_t red[KW * kBlocks * 64];
@@ -290,6 +290,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
                     rd, (__attribute__((address_space(3))) void *)(a_lds + (kw * D + j) * kAStage + i * 1024), 16,
                     (int)a_dma[i], ld_ku * 256, 0, 0);
         }
+        issue_order_point();  // the rows are the stage's oldest loads
         const __amdgpu_buffer_rsrc_t rw =
             __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
         if constexpr (SPARSE) {
@@ -318,6 +319,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
                         half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
             }
         }
+        issue_order_point();  // stages do not interleave
     };
     auto advance_ld = [&]() {
         ld_ku += KW;
@@ -608,7 +610,10 @@ constexpr int stream_depth()
         constexpr int d = NB == 4 ? 4 : NB == 2 ? 5 : 8;
         return KW == 8 ? (d + 1) / 2 : d;
     }
-    return NB == 4 ? 3 : 4;  // LDS ring of 32 rows: 8 KiB per wave-stage
+    // LDS ring of 32 rows: 8 KiB per wave-stage (eight waves: 16-column
+    // tiles only, two stages, 128 KiB)
+    if constexpr (KW == 8) return 2;
+    return NB == 4 ? 3 : 4;
 }
 
 template <int MB, int NB, int AR, int KW>
@@ -654,6 +659,7 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
     case 8141: d = stream_depth<1, 4, 1, 8>(); break;
     case 8142: d = stream_depth<1, 4, 2, 8>(); break;
     case 8144: d = stream_depth<1, 4, 4, 8>(); break;
+    case 8218: d = stream_depth<2, 1, 8, 8>(); break;
     default: break;
     }
     if (d == 0) {
@@ -689,6 +695,7 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
     case 8141: return launch_stream<1, 4, 1, 8>(cfg, p, stream);
     case 8142: return launch_stream<1, 4, 2, 8>(cfg, p, stream);
     case 8144: return launch_stream<1, 4, 4, 8>(cfg, p, stream);
+    case 8218: return launch_stream<2, 1, 8, 8>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

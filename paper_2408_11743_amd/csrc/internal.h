@@ -16,7 +16,7 @@ namespace marlin {
 //   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
 //   grid : work-groups
 //   waves: stream kernel waves per work-group (they split K): 4, or 8 (two per
-//          SIMD) with one 16-row block
+//          SIMD) with one 16-row block or one 16-column block
 constexpr int kStreamOcc = 1;    // work-groups per compute unit
 
 constexpr int kKindStream = 0;  // w4a16_stream_kernel (any M; row groups of 32)

@@ -99,8 +99,12 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
     constexpr int kWDma = S::kWDma;
     constexpr int NW = S::NW;
     constexpr int kStage = S::kStage;
-    constexpr int kSL = S::kSL;
-    constexpr int kLoads = S::kLoads;
+    // Scale loads per wave and stage: one row per block, or (per-channel
+    // scales, the same row for every block) one row per stage.  The ring
+    // depth was sized with one row per block, an upper bound.
+    constexpr int kSL = PER_CHANNEL ? S::kSLB : S::kSL;
+    constexpr int kLoads = KS * (kDmaB + kWDma) + kSL;
+    static_assert(kSL + (P - 2) * kLoads <= 63, "vmcnt range");
     constexpr int kBlocks = NBW * MBW;  // 16x16 output blocks per wave
     __shared__ __attribute__((aligned(16))) uint8_t a_lds[P * kStage + S::kScratch];
     __shared__ int flags[2];
@@ -206,8 +210,9 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
                                                          16, (int)(w_lane + (wm * kWDma + b) * 1024),
                                                          (int)(ld_w + kb * 4096u), 0, kAuxNonTemporal);
         }
+        issue_order_point();  // the direct-to-LDS loads precede the stage's scale loads
 #pragma unroll
-        for (int kb = 0; kb < KS; ++kb) {
+        for (int kb = 0; kb < (PER_CHANNEL ? 1 : KS); ++kb) {
             const bool in = ld_ku + kb < ld_end;
             const __amdgpu_buffer_rsrc_t rs =
                 __builtin_amdgcn_make_buffer_rsrc((void *)p.S, (short)0, in ? s_bytes : 0u, kBufferFlags);
@@ -222,6 +227,7 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
                         half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, soff, 0));
             }
         }
+        issue_order_point();  // stages do not interleave
     };
     auto advance_ld = [&]() {
         ld_ku += KS;

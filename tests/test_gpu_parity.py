@@ -148,16 +148,19 @@ def test_each_kernel_and_partition(mk, force, spec, M, K, N, g):
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("nb", [1, 2, 4])
 @pytest.mark.parametrize("part", ["whole=1", "whole=0,grid=7", "whole=0,grid=96"])
-@pytest.mark.parametrize("M", [1, 6, 13])
+@pytest.mark.parametrize("M", [1, 6, 13, 20, 32, 70])
 @pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1)])
 def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
     # The stream kernel with four and with eight waves per work-group, every
-    # column-tile width and activation-row class (4, 8, 16 rows in LDS), whole
-    # tiles and Stream-K splits (7 work-groups: long ranges over several
-    # tiles; 96: several contributors per tile), grouped and per-channel.
+    # column-tile width and activation-row class (4, 8, 16, 32 rows in LDS;
+    # 70 rows: three row groups), whole tiles and Stream-K splits (7
+    # work-groups: long ranges over several tiles; 96: several contributors
+    # per tile), grouped and per-channel.  Eight waves with two row blocks
+    # exist for 16-column tiles only; elsewhere the override gives four.
     spec = "kind=stream,waves=%d,nb=%d,%s" % (waves, nb, part)
     force(spec)
-    assert (", %d, %s>" % (waves, "true" if g == -1 else "false")) in mk.marlin_describe(M, N, K, g)
+    w = waves if (M <= 16 or nb == 1) else 4
+    assert (", %d, %s>" % (w, "true" if g == -1 else "false")) in mk.marlin_describe(M, N, K, g)
     q, s = synth.weights(7, K, N, None if g == -1 else g)
     A = synth.activations(7, M, K)
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))

@@ -1,0 +1,82 @@
+"""The kernels wait for their direct-to-LDS loads by counting the vector-memory
+operations issued after them (which complete in order): the stream and
+sparse kernels wait for a stage's activation rows while its weight and scale
+loads and D - 1 later stages may still be in flight; the tile kernel waits
+for a stage's activation and weight blocks while its scale loads and P - 2
+later stages may be.  That holds only if the compiler emits each stage's
+loads as one group, direct-to-LDS loads first, in issue order.  The compiler
+may interleave independent loads (it once moved a weight load between the
+activation loads of a stage, and reading rows before their load had landed
+gave wrong outputs), so the kernels pin the order; this test compiles the
+kernel sources for gfx950 and checks, for every instantiation, that the
+buffer loads form identical stage groups of the size the waits assume.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2408_11743_amd", "csrc")
+
+
+def _hipcc():
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    p = os.path.join(rocm, "bin", "hipcc")
+    return p if os.path.exists(p) else shutil.which("hipcc")
+
+
+@pytest.fixture(scope="module")
+def assembly(tmp_path_factory):
+    hipcc = _hipcc()
+    if not hipcc:
+        pytest.skip("hipcc not available")
+    d = tmp_path_factory.mktemp("asm")
+    procs = {}
+    for src in ("gemm", "tile"):
+        out = str(d / (src + ".s"))
+        cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+               "--cuda-device-only", "-S", "-o", out, os.path.join(CSRC, src + ".hip")]
+        procs[src] = (subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE), out)
+    text = {}
+    for src, (pr, out) in procs.items():
+        _, err = pr.communicate()
+        assert pr.returncode == 0, err.decode()[-2000:]
+        text[src] = open(out).read()
+    return text
+
+
+def _kernels(text):
+    for m in re.finditer(r"^(_ZN6marlin\S*(w4a16_(?:stream|sparse|tile)_kernel)I((?:Li\d+E)+)Lb(\d)E\S*):", text, re.M):
+        body = text[m.end():text.index(".Lfunc_end", m.end())]
+        ints = [int(x) for x in re.findall(r"Li(\d+)E", m.group(3))]
+        yield m.group(1), m.group(2), ints, m.group(4) == "1", body
+
+
+def _expected_group(kind, ints, per_channel):
+    if kind == "w4a16_tile_kernel":
+        WN, WM, MBW, NBW, KS = ints
+        NW, TR = WN * WM, 16 * MBW * WM
+        dma_a, dma_w, scale = TR // (4 * NW), NBW // WM, (2 if NBW == 4 else 1)
+        return "L" * (KS * (dma_a + dma_w)) + "R" * (scale if per_channel else KS * scale)
+    MB, NB, D, AR, KW = ints
+    weights = (3 if NB == 4 else 2) if kind == "w4a16_sparse_kernel" else NB
+    return "L" * AR + "R" * (weights + (0 if per_channel else (NB + 1) // 2))
+
+
+def test_every_kernel_issues_its_loads_in_stage_groups(assembly):
+    n = 0
+    bad = []
+    for src, text in assembly.items():
+        for name, kind, ints, pc, body in _kernels(text):
+            seq = "".join("L" if " lds" in line else "R" for line in body.splitlines()
+                          if "buffer_load" in line and not line.strip().startswith(";"))
+            group = _expected_group(kind, ints, pc)
+            n += 1
+            if not seq or len(seq) % len(group) or seq != group * (len(seq) // len(group)):
+                bad.append("%s: expected groups %s, got %s" % (name, group, seq))
+    assert n >= 100, "kernels not found in the assembly (%d)" % n
+    assert not bad, "\n".join(bad)
