@@ -236,29 +236,13 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     // ones read a zero row (the 256 bytes after the ring) instead.
     uint32_t a_dma[AR];
     uint32_t a_rd[D][MB][4];
-    {
 #pragma unroll
-        for (int i = 0; i < AR; ++i) {
-            const int r = 4 * i + lg;
-            a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u + (uint32_t)kw * 256u;
-        }
-        const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
-        const uint32_t zero_row = lds0 + KW * D * kAStage;
-        if (threadIdx.x < 16) *(u32x4_t *)(a_lds + KW * D * kAStage + threadIdx.x * 16) = u32x4_t{0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < D; ++j)
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int am = mb * 16 + (lane & 15);
-                    const uint32_t chunk = (uint32_t)(((4 * t + lg) ^ (am & 15)) << 4);
-                    a_rd[j][mb][t] = (am < kARows)
-                                         ? lds0 + (uint32_t)((kw * D + j) * kAStage + am * 256) + chunk
-                                         : zero_row + chunk;
-                }
-        __syncthreads();  // zero row written before any wave reads it
+    for (int i = 0; i < AR; ++i) {
+        const int r = 4 * i + lg;
+        a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u + (uint32_t)kw * 256u;
     }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
+    const uint32_t zero_row = lds0 + KW * D * kAStage;
     // Rows of A past M lie past the end of the A buffer: their loads return 0.
     const uint32_t w_bytes = SPARSE ? (uint32_t)p.K / 8u * (uint32_t)p.N * 3u : (uint32_t)p.K * (uint32_t)(p.N / 2);
 
@@ -344,6 +328,32 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
         issue(j);
         advance_ld();
     }
+    // While they are on their way: the LDS read addresses and, where some of
+    // the 16*MB operand rows are not loaded, the zero row (written by an
+    // instruction of its own, so that the compiler's tracking of the
+    // direct-to-LDS writes in flight adds no wait) and the barrier that
+    // publishes it before any wave reads it.  No wave waits for the others
+    // before issuing its loads.
+    if constexpr (kARows < 16 * MB) {
+        if (threadIdx.x < 16)
+            asm volatile("ds_write_b128 %0, %1" ::"v"(zero_row + threadIdx.x * 16u), "v"(u32x4_t{0u, 0u, 0u, 0u})
+                         : "memory");
+    }
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int am = mb * 16 + (lane & 15);
+                const uint32_t chunk = (uint32_t)(((4 * t + lg) ^ (am & 15)) << 4);
+                a_rd[j][mb][t] = (am < kARows) ? lds0 + (uint32_t)((kw * D + j) * kAStage + am * 256) + chunk
+                                               : zero_row + chunk;
+            }
+    // With one row block the barrier also lines the waves up before the
+    // first stage, which measured faster even where no row is zero; with
+    // two it measured slower and is kept only for the zero row.
+    if constexpr (kARows < 16 * MB || MB == 1) lds_barrier();
 
     // Stages of this work-group: ceil(segment length / KW) per segment.
     const int n_st = (c_first == c_last)
