@@ -29,6 +29,34 @@ __device__ __forceinline__ void wait_vmcnt()
     asm volatile("" ::: "memory");
 }
 
+// wait_vmcnt<V> for a V known only after unrolling: the switch folds to
+// one wait when n is a constant (a loop index of a fully unrolled loop).
+__device__ __forceinline__ void wait_vmcnt_n(int n)
+{
+#define MARLIN_VMCNT_CASE(V) \
+    case V:                  \
+        wait_vmcnt<V>();     \
+        break;
+#define MARLIN_VMCNT_CASE8(V) MARLIN_VMCNT_CASE(V) MARLIN_VMCNT_CASE(V + 1) MARLIN_VMCNT_CASE(V + 2) \
+    MARLIN_VMCNT_CASE(V + 3) MARLIN_VMCNT_CASE(V + 4) MARLIN_VMCNT_CASE(V + 5) MARLIN_VMCNT_CASE(V + 6) \
+    MARLIN_VMCNT_CASE(V + 7)
+    switch (n) {
+        MARLIN_VMCNT_CASE8(0)
+        MARLIN_VMCNT_CASE8(8)
+        MARLIN_VMCNT_CASE8(16)
+        MARLIN_VMCNT_CASE8(24)
+        MARLIN_VMCNT_CASE8(32)
+        MARLIN_VMCNT_CASE8(40)
+        MARLIN_VMCNT_CASE8(48)
+        MARLIN_VMCNT_CASE8(56)
+    default:
+        wait_vmcnt<0>();
+        break;
+    }
+#undef MARLIN_VMCNT_CASE8
+#undef MARLIN_VMCNT_CASE
+}
+
 __device__ __forceinline__ void wait_lgkmcnt0()
 {
     __builtin_amdgcn_s_waitcnt(63 | (7 << 4) | (0 << 8) | (3 << 14));

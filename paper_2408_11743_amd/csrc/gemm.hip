@@ -380,18 +380,16 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     // plus four for the zero point.  Group scales: the stage's zero-point
     // product is subtracted from each column block's 128-row product, and the
     // difference scaled and accumulated in one fused multiply-add per value.
-    auto compute = [&](int j) {
+    auto compute = [&](int j, int later) {
         half8_t a[4 * MB];
         {
-            // Wait for this stage's direct-to-LDS rows: loads issued after
-            // them are the stage's own weight and scale loads and D-1 later
-            // stages (vector-memory ops complete in order).  The reads are
-            // written as assembly, with their own lgkmcnt wait, so that the
-            // compiler's conservative tracking of direct-to-LDS writes does
-            // not add waits for the whole ring.
-            constexpr int kAfter = (D - 1) * kLoads + kWL + kSL;
-            __builtin_amdgcn_s_waitcnt((kAfter & 15) | (7 << 4) | (15 << 8) | ((kAfter >> 4) << 14));
-            asm volatile("" ::: "memory");
+            // Wait for this stage's direct-to-LDS rows: the loads issued
+            // after them are the stage's own weight and scale loads and
+            // `later` stages (vector-memory ops complete in order).  The
+            // reads are written as assembly, with their own lgkmcnt wait, so
+            // that the compiler's conservative tracking of direct-to-LDS
+            // writes does not add waits for the whole ring.
+            wait_vmcnt_n(later * kLoads + kWL + kSL);
             u32x4_t v[4 * MB];
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
@@ -561,28 +559,38 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
         }
     };
 
-    // Loads are issued unconditionally (past the range through empty
-    // descriptors) so that every stage has the same load pattern and the
-    // compiler's vmcnt waits stay static.
-    for (int st0 = 0; st0 < n_st; st0 += D) {
+    // Stage st in ring slot j, with `later` stages issued after it: compute,
+    // and close the tile segment at its end.
+    auto step = [&](int j, int st, int later) {
+        if (st < n_st) {
+            if (cp_ku + kw < cp_end) compute(j, later);
+            if (cp_ku + KW >= cp_end) {
+                finish_segment();
+                cp_c += 1;
+                cp_ku = 0;
+                cp_begin = 0;
+                cp_end = (cp_c < c_last) ? KU : k1;
+            } else {
+                cp_ku += KW;
+            }
+        }
+    };
+    // Groups of D stages.  Every group but the last refills each slot after
+    // computing it; loads are issued unconditionally (past the range through
+    // empty descriptors) so that every stage has the same load pattern and
+    // the vmcnt waits stay static.  The last group issues nothing: its slot j
+    // waits with only the D-1-j stages issued after it behind it.
+    const int st_last = (n_st - 1) / D * D;
+    for (int st0 = 0; st0 < st_last; st0 += D) {
 #pragma unroll
         for (int j = 0; j < D; ++j) {
-            if (st0 + j < n_st) {
-                if (cp_ku + kw < cp_end) compute(j);
-                if (cp_ku + KW >= cp_end) {
-                    finish_segment();
-                    cp_c += 1;
-                    cp_ku = 0;
-                    cp_begin = 0;
-                    cp_end = (cp_c < c_last) ? KU : k1;
-                } else {
-                    cp_ku += KW;
-                }
-            }
+            step(j, st0 + j, D - 1);
             issue(j);
             advance_ld();
         }
     }
+#pragma unroll
+    for (int j = 0; j < D; ++j) step(j, st_last + j, D - 1 - j);
 
     // ---- combination of shared tiles ----
     auto own_slot = [&](int j) { return own(j) < kBlocks ? own(j) : -1; };
