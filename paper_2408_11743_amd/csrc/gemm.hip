@@ -243,6 +243,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     }
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
     const uint32_t zero_row = lds0 + KW * D * kAStage;
+    const uint32_t lds_wave = lds0 + (uint32_t)(kw * D * kAStage);  // this wave's ring
     // Rows of A past M lie past the end of the A buffer: their loads return 0.
     const uint32_t w_bytes = SPARSE ? (uint32_t)p.K / 8u * (uint32_t)p.N * 3u : (uint32_t)p.K * (uint32_t)(p.N / 2);
 
@@ -268,10 +269,16 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
         {  // first, so a stage's LDS rows are its oldest loads
             const __amdgpu_buffer_rsrc_t rd =
                 __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, on ? a_bytes : 0u, kBufferFlags);
+            // The slot's LDS address is formed here from one per-wave base
+            // (the opaque copy keeps the compiler from holding all D * AR
+            // destination addresses in scalar registers across the loop).
+            uint32_t slot = lds_wave;
+            asm volatile("" : "+s"(slot));
+            slot += (uint32_t)(j * kAStage);
 #pragma unroll
             for (int i = 0; i < AR; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                    rd, (__attribute__((address_space(3))) void *)(a_lds + (kw * D + j) * kAStage + i * 1024), 16,
+                    rd, (__attribute__((address_space(3))) void *)(uintptr_t)(slot + (uint32_t)(i * 1024)), 16,
                     (int)a_dma[i], ld_ku * 256, 0, 0);
         }
         issue_order_point();  // the rows are the stage's oldest loads

@@ -178,8 +178,19 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
     const uint16_t *ld_a = p.A + (int64_t)row0_of(ld_c) * p.K;
     uint32_t a_bytes = (uint32_t)rows_of(ld_c) * (uint32_t)p.K * 2u;
 
+    // LDS destinations of this wave's direct-to-LDS loads: slot 0's, and the
+    // scratch area that takes the loads issued past the end.  The issue forms
+    // each destination from these (through an opaque copy) so that the
+    // compiler does not hold every slot's and block's address in a scalar
+    // register across the loop.
+    const uint32_t a_dst0 = lds0 + (uint32_t)(wave * (kABlock / NW));
+    const uint32_t w_dst0 = lds0 + (uint32_t)(kAStage + (wn * NBW + wm * kWDma) * 1024);
+    const uint32_t scratch = lds0 + (uint32_t)(P * kStage);
+
     auto issue = [&](int j) {
         const bool on = ld_ku < ld_end;  // the stage's first block is in range
+        uint32_t a_base = a_dst0, w_base = w_dst0, x_base = scratch;
+        asm volatile("" : "+s"(a_base), "+s"(w_base), "+s"(x_base));
         // Activation rows first (oldest loads of the stage), then this wave's
         // weights, then its scales.  Past the end the direct-to-LDS loads go
         // to the scratch area: other waves may still read every ring slot.
@@ -190,11 +201,11 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
             const bool in = ld_ku + kb < ld_end;
             const __amdgpu_buffer_rsrc_t ra =
                 __builtin_amdgcn_make_buffer_rsrc((void *)ld_a, (short)0, in ? a_bytes : 0u, kBufferFlags);
-            uint8_t *dst = on ? a_lds + j * kStage + kb * kABlock + wave * (kABlock / NW) : a_lds + P * kStage;
+            const uint32_t dst = on ? a_base + (uint32_t)(j * kStage + kb * kABlock) : x_base;
 #pragma unroll
             for (int i = 0; i < kDmaB; ++i)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (__attribute__((address_space(3))) void *)(dst + i * 1024),
-                                                         16, (int)a_dma[i], (ld_ku + kb) * 256, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (__attribute__((address_space(3))) void *)(uintptr_t)(dst + (uint32_t)(i * 1024)), 16, (int)a_dma[i],
+                                                         (ld_ku + kb) * 256, 0, 0);
         }
 #pragma unroll
         for (int kb = 0; kb < KS; ++kb) {
@@ -202,12 +213,11 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
             const __amdgpu_buffer_rsrc_t rw =
                 __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, in ? w_bytes : 0u, kBufferFlags);
             // this wave's share of its column group's blocks: wm*kWDma ..
-            uint8_t *wdst = on ? a_lds + j * kStage + kAStage + kb * kWBlock + (wn * NBW + wm * kWDma) * 1024
-                               : a_lds + P * kStage + kDmaB * 1024;
+            const uint32_t wdst = on ? w_base + (uint32_t)(j * kStage + kb * kWBlock) : x_base + kDmaB * 1024u;
 #pragma unroll
             for (int b = 0; b < kWDma; ++b)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(wdst + b * 1024),
-                                                         16, (int)(w_lane + (wm * kWDma + b) * 1024),
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (__attribute__((address_space(3))) void *)(uintptr_t)(wdst + (uint32_t)(b * 1024)), 16,
+                                                         (int)(w_lane + (wm * kWDma + b) * 1024),
                                                          (int)(ld_w + kb * 4096u), 0, kAuxNonTemporal);
         }
         issue_order_point();  // the direct-to-LDS loads precede the stage's scale loads
