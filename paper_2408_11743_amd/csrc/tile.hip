@@ -391,32 +391,42 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
     // issued unconditionally (past the range into the scratch area, through
     // empty descriptors) so that every stage has the same load pattern and the
     // compiler's own vmcnt waits (for the scale registers) stay static.
-    constexpr int kAfter = kSL + (P - 2) * kLoads;
-    for (int st0 = 0; st0 < n_st; st0 += P) {
-#pragma unroll
-        for (int j = 0; j < P; ++j) {
-            const bool live = st0 + j < n_st;
-            if (live) {
-                wait_vmcnt<kAfter>();
-                __builtin_amdgcn_s_barrier();
-                asm volatile("" ::: "memory");
-            }
+    // Stage st (ring slot j) with `later` stages issued after it; `refill`:
+    // the slot of stage st - 1 takes stage st + P - 1.
+    auto step = [&](int j, int st, int later, bool refill) {
+        const bool live = st < n_st;
+        if (live) {
+            wait_vmcnt_n(kSL + later * kLoads);
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        }
+        if (refill) {
             issue((j + P - 1) % P);
             advance_ld();
-            if (live) {
-                compute(j);
-                if (cp_ku + KS >= cp_end) {
-                    finish_segment(j);
-                    cp_c += 1;
-                    cp_ku = 0;
-                    cp_begin = 0;
-                    cp_end = (cp_c < c_last) ? KU : k1;
-                } else {
-                    cp_ku += KS;
-                }
+        }
+        if (live) {
+            compute(j);
+            if (cp_ku + KS >= cp_end) {
+                finish_segment(j);
+                cp_c += 1;
+                cp_ku = 0;
+                cp_begin = 0;
+                cp_end = (cp_c < c_last) ? KU : k1;
+            } else {
+                cp_ku += KS;
             }
         }
+    };
+    // Groups of P stages.  In the last group only the first step has a stage
+    // left to load (the group's last); the others issue nothing, and stage j
+    // of the group waits with the P - 1 - j stages issued after it behind it.
+    const int st_last = (n_st - 1) / P * P;
+    for (int st0 = 0; st0 < st_last; st0 += P) {
+#pragma unroll
+        for (int j = 0; j < P; ++j) step(j, st0 + j, P - 2, true);
     }
+#pragma unroll
+    for (int j = 0; j < P; ++j) step(j, st_last + j, j == 0 ? P - 2 : P - 1 - j, j == 0);
 
     float4_t last_out[kBlocks];
 #pragma unroll
