@@ -57,6 +57,28 @@ __device__ __forceinline__ void wait_vmcnt_n(int n)
 #undef MARLIN_VMCNT_CASE
 }
 
+// Wait until at most n LDS (and scalar-memory) operations are outstanding;
+// n is clamped to the counter's range (a smaller n only waits longer).  The
+// switch folds to one wait when n is a constant after unrolling.
+__device__ __forceinline__ void wait_lgkmcnt_n(int n)
+{
+#define MARLIN_LGKM_CASE(V)                                                          \
+    case V:                                                                          \
+        __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | ((V) << 8) | (3 << 14));         \
+        break;
+    switch (n < 0 ? 0 : n > 15 ? 15 : n) {
+        MARLIN_LGKM_CASE(0) MARLIN_LGKM_CASE(1) MARLIN_LGKM_CASE(2) MARLIN_LGKM_CASE(3)
+        MARLIN_LGKM_CASE(4) MARLIN_LGKM_CASE(5) MARLIN_LGKM_CASE(6) MARLIN_LGKM_CASE(7)
+        MARLIN_LGKM_CASE(8) MARLIN_LGKM_CASE(9) MARLIN_LGKM_CASE(10) MARLIN_LGKM_CASE(11)
+        MARLIN_LGKM_CASE(12) MARLIN_LGKM_CASE(13) MARLIN_LGKM_CASE(14)
+    default:
+        __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (15 << 8) | (3 << 14));
+        break;
+    }
+#undef MARLIN_LGKM_CASE
+    asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ void wait_lgkmcnt0()
 {
     __builtin_amdgcn_s_waitcnt(63 | (7 << 4) | (0 << 8) | (3 << 14));

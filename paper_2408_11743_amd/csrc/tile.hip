@@ -271,15 +271,23 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
     // One stage (ring slot j): every operand of the KS blocks is read first,
     // then per block the column blocks, each dequantized word feeding the MBW
     // row blocks.
+    // LDS reads of one stage, in the order the MFMAs use them: per block,
+    // column block 0's weights, the activation operands k-step by k-step,
+    // then the other column blocks' weights.  LDS reads complete in order, so
+    // each group of MFMAs waits only for the reads it needs (by counting the
+    // reads issued after them) and the rest of the stage's reads overlap the
+    // first column block's MFMAs.  Each wait "redefines" the registers it
+    // makes available, so that no use is scheduled before it.
+    constexpr int kRB = NBW + 4 * MBW;  // reads per block
+    constexpr int kR = KS * kRB;        // reads per stage
+    auto reads_after = [](int idx) { return kR - 1 - idx; };
     auto compute = [&](int j) {
         u32x4_t wv[KS][NBW];     // [block][column block] this lane's packed weights
         u32x4_t v[KS][MBW][4];   // [block][row block][k-step] activation operands
 #pragma unroll
         for (int kb = 0; kb < KS; ++kb) {
             const uint32_t wj = w_rd + j * kStage + kb * kWBlock;
-#pragma unroll
-            for (int b = 0; b < NBW; ++b)
-                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(wv[kb][b]) : "v"(wj), "i"(b * 1024));
+            asm volatile("ds_read_b128 %0, %1" : "=v"(wv[kb][0]) : "v"(wj));
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const uint32_t aj = a_rd[t] + j * kStage + kb * kABlock;
@@ -287,25 +295,32 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
                 for (int mb = 0; mb < MBW; ++mb)
                     asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v[kb][mb][t]) : "v"(aj), "i"(mb * 4096));
             }
-        }
-        // The wait "redefines" the results: no use is scheduled before it.
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int kb = 0; kb < KS; ++kb) {
-#pragma unroll
-            for (int b = 0; b < NBW; ++b) asm volatile("" : "+v"(wv[kb][b]));
-#pragma unroll
-            for (int mb = 0; mb < MBW; ++mb)
-#pragma unroll
-                for (int t = 0; t < 4; ++t) asm volatile("" : "+v"(v[kb][mb][t]));
+            for (int b = 1; b < NBW; ++b)
+                asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(wv[kb][b]) : "v"(wj), "i"(b * 1024));
         }
 #pragma unroll
         for (int kb = 0; kb < KS; ++kb) {
 #pragma unroll
             for (int b = 0; b < NBW; ++b) {
+                if (b > 0) {
+                    wait_lgkmcnt_n(reads_after(kb * kRB + 4 * MBW + b));
+                    asm volatile("" : "+v"(wv[kb][b]));
+                }
+                // k-step t of column block 0 waits for the step's activation
+                // operands (and, at t = 0, the block's first weights)
+                auto ready_step = [&](int t) {
+                    if (b == 0) {
+                        wait_lgkmcnt_n(reads_after(kb * kRB + t * MBW + MBW));
+                        if (t == 0) asm volatile("" : "+v"(wv[kb][0]));
+#pragma unroll
+                        for (int mb = 0; mb < MBW; ++mb) asm volatile("" : "+v"(v[kb][mb][t]));
+                    }
+                };
                 if constexpr (PER_CHANNEL) {
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
+                        ready_step(t);
                         const half8_t w = dequant_magic(wv[kb][b][t], dq);
 #pragma unroll
                         for (int mb = 0; mb < MBW; ++mb)
@@ -315,6 +330,7 @@ __global__ void __launch_bounds__(64 * WN * WM, 1) w4a16_tile_kernel(GemmProblem
                     float4_t tmp[MBW];
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
+                        ready_step(t);
                         const half8_t w = dequant_magic(wv[kb][b][t], dq);
 #pragma unroll
                         for (int mb = 0; mb < MBW; ++mb)
