@@ -18,9 +18,13 @@ shape timed the same way in the same run (comparison only).  ``roofline``
 covers the GEMM kernel: algorithmic bytes of the timed launches / elapsed
 (HIP events on the launch stream) against 8 TB/s.  ``cpu_baseline`` times
 the fp64 oracle on the host over the whole sweep (and checks the GPU
-outputs against it).
+outputs against it).  Two further sections are reported beside the step,
+outside its timed region: ``sparse_2of4`` (the 2:4 sparse kernel, K = N =
+8192, M sweep) and ``prefill`` (M = 256, 1024, 4096 in one launch per call,
+against the fp16 matrix-core peak and fp16 ``torch.matmul``).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+       [--no-sparse | --sparse-only] [--no-prefill | --prefill-only]
 """
 from __future__ import annotations
 
@@ -59,6 +63,10 @@ def parse():
                     help="skip the 2:4 sparse section (K = N = 8192, g = 128, M sweep)")
     ap.add_argument("--sparse-only", action="store_true",
                     help="run only the 2:4 sparse section and print its JSON (for profiling it alone)")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the large-batch section (M = 256, 1024, 4096 in one launch)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="run only the large-batch section and print its JSON (for profiling it alone)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run plain device-to-device copies of this many MB (outside the timed "
                          "region) so hardware byte counters can be scaled against a known size")
@@ -79,6 +87,9 @@ def measured_traffic():
 
 
 SPARSE_K, SPARSE_N, SPARSE_WID = 8192, 8192, 4
+# large batches: (K, N, synth workload) and the batch sizes
+PREFILL_SHAPES = [(4096, 4096, 1), (28672, 8192, 3)]
+PREFILL_M = [256, 1024, 4096]
 
 
 def graph_time_us(launch, count, stream, reps, torch, np):
@@ -90,8 +101,13 @@ def graph_time_us(launch, count, stream, reps, torch, np):
         with torch.cuda.graph(gr, stream=stream):
             for i in range(count):
                 launch(i)
-        gr.replay()
-        torch.cuda.synchronize()
+        # replays for >= 30 ms first: clocks ramp up after host-side pauses
+        t_end = time.perf_counter() + 0.03
+        while True:
+            gr.replay()
+            torch.cuda.synchronize()
+            if time.perf_counter() >= t_end:
+                break
         times = []
         for _ in range(reps):
             a0 = torch.cuda.Event(enable_timing=True)
@@ -161,6 +177,56 @@ def sparse_section(args, mk, R, synth, torch, np, dev):
             "bound": "hbm", "per_m": rows}
 
 
+def prefill_section(args, mk, R, synth, torch, np, dev):
+    """Large batches in one launch (Section 3.4, Striped Partitioning, on
+    batches well above 64): the Llama-7B attention projection and the
+    70B-class MLP down projection at M = 256, 1024, 4096, g = 128, against
+    fp16 torch.matmul on the dequantized matrix.  MFMA-bound: the roofline is
+    the fp16 matrix-core peak.  Two weight copies alternate (at these M the
+    weights are a small part of the traffic)."""
+    L = mk.lib()
+    stream = torch.cuda.Stream(device=dev)
+    ws = mk.Workspace(dev)
+    rows = []
+    for (K, N, wid) in PREFILL_SHAPES:
+        g = GROUP
+        q, s = synth.weights(wid, K, N, g)
+        qd, sd = torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev)
+        wp, sp = mk.pack(qd, sd, group=g)
+        wps = [wp, wp.clone()]
+        w16 = None
+        if not args.no_fp16:
+            w16 = ((qd.to(torch.float32) - 8.0) * sd.to(torch.float32).repeat_interleave(g, dim=0)).to(torch.float16)
+        del qd, sd
+        wsbuf = ws.ensure(max(mk.marlin_workspace_bytes(M, N, K, g) for M in PREFILL_M))
+        for M in PREFILL_M:
+            A = torch.from_numpy(synth.activations(wid, M, K)).to(dev)
+            C = torch.empty((M, N), dtype=torch.float16, device=dev)
+
+            def launch(i, M=M, A=A, C=C):
+                st = L.marlin_gemm(A.data_ptr(), wps[i % 2].data_ptr(), sp.data_ptr(), C.data_ptr(),
+                                   wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g, stream.cuda_stream)
+                if st != 0:
+                    raise mk.MarlinError("marlin_gemm", st)
+            t = graph_time_us(launch, 4, stream, args.per_m_reps, torch, np)
+            rec = {"K": K, "N": N, "M": M, "us": round(t, 2),
+                   "TFLOPs": round(R.flops(M, N, K) / t / 1e6, 1),
+                   "mfma_frac": round(R.flops(M, N, K) / (t * 1e-6) / R.FP16_MFMA_FLOPS, 4),
+                   "launch": mk.marlin_describe(M, N, K, g)}
+            if w16 is not None:
+                t16 = graph_time_us(lambda i: torch.matmul(A, w16), 4, stream, args.per_m_reps, torch, np)
+                rec["fp16_us"] = round(t16, 2)
+                rec["speedup_vs_fp16"] = round(t16 / t, 3)
+            rows.append(rec)
+            log("prefill %dx%d M=%4d: %.1f us, %.0f TFLOP/s (%.1f%% of the MFMA peak), fp16 %s us" %
+                (K, N, M, t, rec["TFLOPs"], 100 * rec["mfma_frac"], rec.get("fp16_us", "-")))
+            del A, C
+        del wps, wp, sp, w16
+    return {"workload": "W4A16 GEMM, one launch per call, g=%d, (K, N) in %s, M in %s" %
+                        (GROUP, [sh[:2] for sh in PREFILL_SHAPES], PREFILL_M),
+            "bound": "mfma", "peak_TFLOPs": R.FP16_MFMA_FLOPS / 1e12, "per_m": rows}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -191,6 +257,9 @@ def main():
         del src, dst
     if args.sparse_only:
         print(json.dumps({"sparse_2of4": sparse_section(args, mk, R, synth, torch, np, dev)}), flush=True)
+        return
+    if args.prefill_only:
+        print(json.dumps({"prefill": prefill_section(args, mk, R, synth, torch, np, dev)}), flush=True)
         return
     K, N, g = K_DIM, N_DIM, GROUP
 
@@ -369,6 +438,7 @@ def main():
             (tot, threads, ok, worst))
 
     sparse = None if args.no_sparse else sparse_section(args, mk, R, synth, torch, np, dev)
+    prefill = None if args.no_prefill else prefill_section(args, mk, R, synth, torch, np, dev)
 
     small = [r for r in per_m if r["M"] <= 16]
     out = {
@@ -405,6 +475,7 @@ def main():
         "cpu_baseline": cpu,
         "parity": parity,
         "sparse_2of4": sparse,
+        "prefill": prefill,
     }
     print(json.dumps(out), flush=True)
 

@@ -139,9 +139,13 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  *              may overlap (different streams) need separate workspaces.
  *
  * Accumulation is fp32.  Group scales multiply each 128-row fp32 partial
- * product; per-channel scales multiply the final sum once.  M > 128 runs as
- * passes of 128 rows.  Results are bitwise reproducible for a given device,
- * shape and input.
+ * product; per-channel scales multiply the final sum once.  Any M up to 4096
+ * runs in one launch: the rows are cut into segments (32 rows for the stream
+ * kernel, the tile's rows for the tile kernel) and each segment repeats the
+ * weight matrix's tiles in the striped partition, so all segments share one
+ * work split and one combination step (Section 3.4, Striped Partitioning,
+ * on batches well above 64).  Larger M runs as launches of 4096 rows.
+ * Results are bitwise reproducible for a given device, shape and input.
  *
  * The launch configuration comes from a cost model of the device (see
  * marlin_describe).  For tuning and tests, the environment variable
@@ -167,7 +171,7 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
  * visible), as one NUL-terminated line: the kernel's name with its template
  * arguments as a profiler reports it, then "cols=<columns per tile>
  * rg=<row groups> partition=<whole|streamk> grid=<work-groups>", for the
- * first 128-row pass.  The stream kernel's template arguments are
+ * first launch (the first 4096 rows).  The stream kernel's template arguments are
  * <16-row blocks, 16-column blocks, ring depth, activation rows / 4, waves,
  * per-channel>, the tile kernel's <waves along N, waves along M, 16-row
  * blocks per wave, 16-column blocks per wave, 128-row blocks per stage,

@@ -226,7 +226,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.sparse = sparse ? 1 : 0;
     cfg.mb = (M <= 16) ? 1 : 2;
     cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
-    cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32 (at most 4 per 128-row pass)
+    cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32, each a copy of the column tiles
     if (cfg.rg < 1) cfg.rg = 1;
     double best = 1e30;
     cfg.nb = 0;
@@ -329,17 +329,17 @@ size_t workspace_bytes_for(const GemmConfig &cfg, int N)
 }
 
 namespace {
-// Largest workspace over the passes of 128 rows that an M-row call makes,
-// dense or 2:4 sparse (one size serves both entry points).
+// Largest workspace over the passes of at most kPassRows rows that an M-row
+// call makes, dense or 2:4 sparse (one size serves both entry points).
 size_t required_workspace(int64_t M, int N, int K, int gu)
 {
-    const int m_first = M < 128 ? (int)M : 128;
-    const int m_last = (int)(M % 128);
+    const int m_first = M < kPassRows ? (int)M : kPassRows;
+    const int m_last = (int)(M % kPassRows);
     size_t need = 0;
     for (int sp = 0; sp < 2; ++sp) {
         size_t b = workspace_bytes_for(choose_config(m_first, N, K, gu, kMaxCus, sp != 0), N);
         if (b > need) need = b;
-        if (M > 128 && m_last != 0) {
+        if (M > kPassRows && m_last != 0) {
             b = workspace_bytes_for(choose_config(m_last, N, K, gu, kMaxCus, sp != 0), N);
             if (b > need) need = b;
         }
@@ -376,8 +376,8 @@ marlin_status_t gemm_impl(const uint16_t *A, const void *w_packed, const void *s
     const int cus = device_cu_count(device);
     if (cus <= 0) return MARLIN_ERR_HIP;
 
-    for (int64_t m0 = 0; m0 < M; m0 += 128) {
-        const int mp = (M - m0) < 128 ? (int)(M - m0) : 128;
+    for (int64_t m0 = 0; m0 < M; m0 += kPassRows) {
+        const int mp = (M - m0) < kPassRows ? (int)(M - m0) : kPassRows;
         const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus, sparse);
         const size_t counter_bytes = kCounterRegionBytes;
         GemmProblem p;
@@ -428,7 +428,7 @@ marlin_status_t describe_impl(int64_t M, int64_t N, int64_t K, int64_t group, ch
         (void)hipGetLastError();
     }
     const int gu = (group == -1 || group == K) ? 0 : (int)(group / 128);
-    const int mp = M < 128 ? (M > 0 ? (int)M : 1) : 128;
+    const int mp = M < kPassRows ? (M > 0 ? (int)M : 1) : kPassRows;
     const GemmConfig cfg = choose_config(mp, (int)N, (int)K, gu, cus, sparse);
     char name[96];
     kernel_name(cfg, gu == 0, name, sizeof(name));

@@ -90,6 +90,16 @@ constexpr int kCounterStride = 32;
 constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4 * 4;
 static_assert((size_t)kMaxCus * kMaxPerCu * kCounterStride * 4 <= kCounterRegionBytes, "counter region");
 
+// Rows of A per launch.  A launch covers ceil(rows / 32) row groups of the
+// stream kernel, or one row group per tile height of the tile kernel, each a
+// copy of the weight matrix's tiles in the striped partition (the weights
+// replicated virtually, one copy per segment of A: Section 3.4, Striped
+// Partitioning); the copies read the same weights, mostly through L2.  With
+// K * N < 2^32, the units of a launch (N / 16 column blocks times K / 128
+// weight blocks, below 2^21, times at most 128 row groups) stay below 2^28,
+// so every unit index fits in 32 bits; larger M runs as several launches.
+constexpr int kPassRows = 4096;
+
 // Device facts cached per device.
 int device_cu_count(int device);
 

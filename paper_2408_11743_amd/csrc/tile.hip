@@ -1,4 +1,4 @@
-// W4A16 GEMM for gfx950, large batches (33 <= M <= 128 rows per pass):
+// W4A16 GEMM for gfx950 at larger batches (tiles of 16 to 128 rows of A):
 // C[M,N] = A[M,K] * (s * (q - 8)), fp32 accumulation.
 //
 // Where the stream kernel is bound by its per-weight VALU work (it serves at

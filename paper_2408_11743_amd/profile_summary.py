@@ -5,6 +5,11 @@ Usage (after the three profiling runs, see the command block this prints):
     python -m paper_2408_11743_amd.profile_summary --trace DIR --fetch DIR \
         --write DIR --bench BENCH_JSON --out OUT_PREFIX [--copy-mb 256]
 
+or, for bench.py --prefill-only, a kernel trace alone (its CSV, not only the
+statistics: --kernel-trace --stats --output-format csv):
+
+    python -m paper_2408_11743_amd.profile_summary --trace DIR --bench BENCH_JSON --out OUT_PREFIX
+
 Reads
   DIR/*kernel_stats.csv          (rocprofv3 --kernel-trace --stats)
   DIR/*counter_collection.csv    (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)
@@ -76,11 +81,67 @@ def short(name: str) -> str:
     return base.split("::")[-1]
 
 
+def prefill_summary(a, bench: dict) -> None:
+    """Kernel trace of bench.py --prefill-only: one row per (K, N, M) case.
+
+    Cases can share a kernel instantiation, so the per-dispatch trace is
+    used: the replayed GEMM dispatches of one case form one run, which the
+    fp16 comparator's kernels (and the weight set-up between shapes) end; the
+    i-th run belongs to the i-th case of the bench output."""
+    sec = bench["prefill"]
+    cases = sec["per_m"]
+    trace = []
+    with open(_one(os.path.join(a.trace, "**", "*kernel_trace.csv"))) as f:
+        for r in csv.DictReader(f):
+            trace.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), short(r["Kernel_Name"])))
+    trace.sort()
+    runs, cur = [], []
+    for t0, t1, name in trace:
+        if name.startswith("w4a16_"):
+            cur.append((name, (t1 - t0) / 1e3))
+        elif cur:
+            runs.append(cur)
+            cur = []
+    if cur:
+        runs.append(cur)
+    # the graph replays of a case; the one eager launch before each capture
+    # stands alone (the capture's own fill kernels follow it)
+    runs = [r for r in runs if len(r) > 1]
+    if len(runs) != len(cases):
+        raise SystemExit("%d GEMM runs in the trace for %d cases (run with the fp16 comparator)" %
+                         (len(runs), len(cases)))
+    import paper_2408_11743_amd.roofline as R
+    md = ["# Kernel trace: W4A16 GEMM at large batches, one launch per call, g = 128", "",
+          "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
+          "Per case: the kernel the library launched (its own account, `launch`), the",
+          "median kernel duration over the case's dispatches (rocprofv3), the bench's",
+          "event time per launch of an unprofiled run (--bench), the fp16",
+          "`torch.matmul` time beside it, and the fraction of the fp16 matrix-core",
+          "peak (2.5 PFLOP/s) that the kernel duration gives:", "",
+          "| K | N | M | kernel | dispatches | median kernel us | bench us | fp16 us | TFLOP/s (kernel) | MFMA frac |",
+          "|---|---|---|---|---|---|---|---|---|---|"]
+    for case, run in zip(cases, runs):
+        names = {n for n, _ in run}
+        want = case["launch"].split(" cols=")[0]
+        if names != {want}:
+            raise SystemExit("case %s: trace has %s, expected %s" % (case, names, want))
+        med = statistics.median(d for _, d in run)
+        fl = R.flops(case["M"], case["N"], case["K"])
+        md.append("| %d | %d | %d | `%s` | %d | %.1f | %.1f | %s | %.0f | %.3f |" % (
+            case["K"], case["N"], case["M"], want, len(run), med, case["us"],
+            "%.1f" % case["fp16_us"] if "fp16_us" in case else "-", fl / med / 1e6,
+            fl / (med * 1e-6) / R.FP16_MFMA_FLOPS))
+    md += ["", "Configuration per case: " + "; ".join(
+        "%dx%d M=%d: cols=%s" % (c["K"], c["N"], c["M"], c["launch"].split(" cols=")[1]) for c in cases), ""]
+    open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
+    print("wrote", a.out + "_kernel_trace.md")
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", required=True)
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
     ap.add_argument("--bench", required=True)
     ap.add_argument("--out", required=True)
     ap.add_argument("--copy-mb", type=int, default=256)
@@ -92,6 +153,11 @@ def main() -> None:
     import paper_2408_11743_amd as mk
 
     bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
+    if "prefill" in bench and "config" not in bench:  # bench.py --prefill-only
+        prefill_summary(a, bench)
+        return
+    if not a.fetch or not a.write:
+        raise SystemExit("--fetch and --write are required for the M sweeps")
     import paper_2408_11743_amd.roofline as R
     sparse = "config" not in bench  # bench.py --sparse-only
     if sparse:

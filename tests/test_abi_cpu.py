@@ -128,7 +128,8 @@ def test_describe_reports_a_launchable_configuration(L):
     import ctypes
     buf = ctypes.create_string_buffer(256)
     for M, N, K, g in [(1, 4096, 4096, 128), (16, 4096, 4096, 128), (32, 11008, 4096, -1),
-                       (128, 28672, 8192, 128), (200, 1024, 1024, 256)]:
+                       (128, 28672, 8192, 128), (200, 1024, 1024, 256), (1000, 4096, 4096, 128),
+                       (4096, 28672, 8192, -1), (5000, 11008, 4096, 128)]:
         assert L.marlin_describe(M, N, K, g, buf, len(buf)) == 0
         text = buf.value.decode()
         assert text.startswith("w4a16_stream_kernel<") or text.startswith("w4a16_tile_kernel<"), text
@@ -143,7 +144,8 @@ def test_describe_reports_a_launchable_configuration(L):
             assert wn * wm in (4, 8) and cols == wn * 16 * nbw, text
             rows = wm * 16 * mbw
             assert rows >= min(M, 128) or rows == 128, text
-        assert int(text.split("rg=")[1].split()[0]) == -(-min(M, 128) // rows), text
+        # one launch covers up to 4096 rows, in segments of the tile's rows
+        assert int(text.split("rg=")[1].split()[0]) == -(-min(M, 4096) // rows), text
         assert int(text.split("grid=")[1]) >= 1
     assert "rg=1" in B.marlin_describe(32, 4096, 4096, 128)
     small = ctypes.create_string_buffer(8)
@@ -152,6 +154,25 @@ def test_describe_reports_a_launchable_configuration(L):
     assert L.marlin_describe(1, 4096, 4096, 128, None, 0) == 1
     assert L.marlin_describe(1, 4096, 4000, 128, buf, len(buf)) == 2
     assert L.marlin_describe(1, 4096, 4096, 64, buf, len(buf)) == 3
+
+
+def test_large_M_runs_in_one_launch(monkeypatch, L):
+    # Beyond 128 rows the rows are segments of one launch (each a copy of the
+    # column tiles in the striped partition), up to 4096 rows per launch.
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
+    assert "cols=32 rg=32 partition=streamk grid=7" in B.marlin_describe(1000, 1024, 1024, 128)
+    assert "cols=32 rg=128 partition=streamk grid=7" in B.marlin_describe(4096, 1024, 1024, 128)
+    assert "cols=32 rg=128 partition=streamk grid=7" in B.marlin_describe(4097, 1024, 1024, 128)
+    monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=tile,nw=8")
+    assert "rg=8 " in B.marlin_describe(1000, 1024, 1024, 128)
+    assert "rg=32 " in B.marlin_describe(9000, 1024, 1024, 128)
+    monkeypatch.delenv("MARLIN_FORCE_CONFIG")
+    # the workspace of an M-row call serves every launch it makes
+    for N, K in [(4096, 4096), (28672, 8192), (4096, 11008)]:
+        w = L.marlin_workspace_bytes(5000, N, K, 128)
+        assert w >= L.marlin_workspace_bytes(4096, N, K, 128)
+        assert w >= L.marlin_workspace_bytes(904, N, K, 128)
+        assert L.marlin_workspace_bytes(1 << 24, N, K, 128) > 0
 
 
 def test_override_selects_the_kernel(monkeypatch):

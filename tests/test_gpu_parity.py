@@ -166,12 +166,35 @@ def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
 
 
-@pytest.mark.parametrize("M", [130, 200, 256])
-def test_M_above_128_runs_in_passes(mk, M):
+@pytest.mark.parametrize("spec", ["", "kind=tile,nw=8,whole=1", "kind=tile,nw=8,whole=0,grid=7",
+                                  "kind=tile,nw=4,whole=0,grid=96", "kind=stream,whole=1",
+                                  "kind=stream,nb=2,whole=0,grid=7"])
+@pytest.mark.parametrize("M", [130, 200, 256, 511, 1000])
+def test_large_M_in_one_launch(mk, force, spec, M):
+    # Beyond 128 rows the segments of A are tiles of one launch (each segment
+    # a copy of the column tiles in the striped partition): every segment
+    # count, a ragged last segment, whole tiles and Stream-K ranges that cross
+    # from one segment's copy into the next.
     K, N = 1024, 512
+    force(spec)
     q, s = synth.weights(4, K, N, 128)
     A = synth.activations(4, M, K)
-    check_close(run_gemm(mk, A, q, s, 128), oracle.gemm(A, q, s, 128), "M=%d" % M)
+    check_close(run_gemm(mk, A, q, s, 128), oracle.gemm(A, q, s, 128), "%s M=%d" % (spec, M))
+
+
+@pytest.mark.parametrize("M", [4096, 4097, 4500])
+def test_M_beyond_one_launch(mk, M):
+    # 4096 rows per launch; the rest in a second launch (sampled outputs, all
+    # columns of the rows around the boundary and of the last row)
+    K, N, g = 1024, 512, -1
+    q, s = synth.weights(8, K, N, None)
+    A = synth.activations(8, M, K)
+    C = run_gemm(mk, A, q, s, g)
+    mi, ni = _samples(M, N, 4000, [8, M])
+    rows = np.array([4094, 4095, min(4096, M - 1), M - 1])
+    mi = np.concatenate([mi, np.repeat(rows, N)])
+    ni = np.concatenate([ni, np.tile(np.arange(N), rows.size)])
+    check_close(C[mi, ni], oracle.gemm_sampled(A, q, s, g, mi, ni), "M=%d sampled" % M)
 
 
 def test_M_zero(mk):
@@ -317,7 +340,7 @@ def test_full_size_layers_sampled(mk, wid, K, N, g):
     q, s = synth.weights(wid, K, N, None if g == -1 else g)
     wp, sp = mk.pack(dev(q), dev(s), group=g)
     ws = mk.Workspace("cuda")
-    for M in (1, 16, 32, 128):
+    for M in (1, 16, 32, 128, 1000):
         A = synth.activations(wid, M, K)
         C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws).cpu().numpy()
         mi, ni = _samples(M, N, 1500, [wid, K, N, M])

@@ -68,7 +68,7 @@ def test_sparse_pack_matches_layout_reference(mk, K, N, g):
     assert np.array_equal(layout.unpack_sparse(layout.pack_sparse(q), K, N), q)
 
 
-@pytest.mark.parametrize("M", [1, 3, 16, 17, 32, 33, 64, 100, 128])
+@pytest.mark.parametrize("M", [1, 3, 16, 17, 32, 33, 64, 100, 128, 300])
 @pytest.mark.parametrize("K,N,g", [(1024, 1024, 128), (2048, 768, -1), (1024, 512, 256)])
 def test_sparse_gemm(mk, M, K, N, g):
     q, keep, s = synth.sparse24_weights(42, K, N, None if g == -1 else g)
@@ -86,7 +86,7 @@ def force(monkeypatch):
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("spec", ["nb=1,whole=1", "nb=2,whole=0,grid=7", "nb=4,whole=0,grid=96", "whole=0,grid=7",
                                   "nb=4,whole=1"])
-@pytest.mark.parametrize("M", [1, 6, 16, 32, 100])
+@pytest.mark.parametrize("M", [1, 6, 16, 32, 100, 257])
 def test_sparse_each_partition(mk, force, waves, spec, M):
     # eight waves apply up to 16 rows; beyond, the override falls back to four
     force("%s,waves=%d" % (spec, waves))
