@@ -20,11 +20,13 @@ covers the GEMM kernel: algorithmic bytes of the timed launches / elapsed
 the fp64 oracle on the host over the whole sweep (and checks the GPU
 outputs against it).  Two further sections are reported beside the step,
 outside its timed region: ``sparse_2of4`` (the 2:4 sparse kernel, K = N =
-8192, M sweep) and ``prefill`` (M = 256, 1024, 4096 in one launch per call,
-against the fp16 matrix-core peak and fp16 ``torch.matmul``).
+8192, M sweep), ``prefill`` (M = 256, 1024, 4096 in one launch per call,
+against the fp16 matrix-core peak and fp16 ``torch.matmul``) and
+``quantize`` (the weight quantiser, against the fp32 vector lane rate).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
        [--no-sparse | --sparse-only] [--no-prefill | --prefill-only]
+       [--no-quantize | --quantize-only]
 """
 from __future__ import annotations
 
@@ -67,6 +69,10 @@ def parse():
                     help="skip the large-batch section (M = 256, 1024, 4096 in one launch)")
     ap.add_argument("--prefill-only", action="store_true",
                     help="run only the large-batch section and print its JSON (for profiling it alone)")
+    ap.add_argument("--no-quantize", action="store_true",
+                    help="skip the quantiser section")
+    ap.add_argument("--quantize-only", action="store_true",
+                    help="run only the quantiser section and print its JSON (for profiling it alone)")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run plain device-to-device copies of this many MB (outside the timed "
                          "region) so hardware byte counters can be scaled against a known size")
@@ -227,6 +233,39 @@ def prefill_section(args, mk, R, synth, torch, np, dev):
             "bound": "mfma", "peak_TFLOPs": R.FP16_MFMA_FLOPS / 1e12, "per_m": rows}
 
 
+def quantize_section(args, mk, R, synth, torch, np, dev):
+    """The quantiser (symmetric, zero point 8, g = 128, clipping search over
+    the 10 default ratios) on the Llama-7B attention projection and the
+    70B-class MLP down projection.  Bound by fp32 vector work (~75 operations
+    per weight against 3 bytes of HBM traffic): ``alu_frac`` against the fp32
+    vector lane rate, ``hbm_GBps`` for reference."""
+    L = mk.lib()
+    stream = torch.cuda.Stream(device=dev)
+    ratios = list(mk.CLIP_RATIOS)
+    rows = []
+    for (K, N, wid) in PREFILL_SHAPES:
+        g = GROUP
+        W = torch.from_numpy(synth.fp16_weights(wid, K, N)).to(dev)
+        q = torch.empty((K, N), dtype=torch.uint8, device=dev)
+        s = torch.empty((K // g, N), dtype=torch.float16, device=dev)
+
+        def launch(i):
+            mk.marlin_quantize(W, K, N, g, ratios, q, s, stream)
+        t = graph_time_us(launch, 2, stream, args.per_m_reps, torch, np)
+        ops = R.quant_ops(K, N, len(ratios))
+        rec = {"K": K, "N": N, "group": g, "ratios": len(ratios), "us": round(t, 2),
+               "Gweights_per_s": round(K * N / t / 1e3, 2),
+               "alu_frac": round(ops / (t * 1e-6) / R.FP32_LANE_OPS, 4),
+               "hbm_GBps": round(R.quant_bytes(K, N, g) / t / 1e3, 1)}
+        rows.append(rec)
+        log("quantize %dx%d g=%d, %d ratios: %.1f us, %.2f G weights/s, %.1f%% of the fp32 lane rate" %
+            (K, N, g, len(ratios), t, rec["Gweights_per_s"], 100 * rec["alu_frac"]))
+        del W, q, s
+    return {"workload": "quantiser fp16 -> (q, s), g=%d, %d clipping ratios, (K, N) in %s" %
+                        (GROUP, len(mk.CLIP_RATIOS), [sh[:2] for sh in PREFILL_SHAPES]),
+            "bound": "alu", "peak_lane_ops_per_s": R.FP32_LANE_OPS, "per_shape": rows}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -260,6 +299,9 @@ def main():
         return
     if args.prefill_only:
         print(json.dumps({"prefill": prefill_section(args, mk, R, synth, torch, np, dev)}), flush=True)
+        return
+    if args.quantize_only:
+        print(json.dumps({"quantize": quantize_section(args, mk, R, synth, torch, np, dev)}), flush=True)
         return
     K, N, g = K_DIM, N_DIM, GROUP
 
@@ -439,6 +481,7 @@ def main():
 
     sparse = None if args.no_sparse else sparse_section(args, mk, R, synth, torch, np, dev)
     prefill = None if args.no_prefill else prefill_section(args, mk, R, synth, torch, np, dev)
+    quant = None if args.no_quantize else quantize_section(args, mk, R, synth, torch, np, dev)
 
     small = [r for r in per_m if r["M"] <= 16]
     out = {
@@ -476,6 +519,7 @@ def main():
         "parity": parity,
         "sparse_2of4": sparse,
         "prefill": prefill,
+        "quantize": quant,
     }
     print(json.dumps(out), flush=True)
 

@@ -48,7 +48,8 @@ typedef enum {
     MARLIN_ERR_MISALIGNED = 4,        /* a device pointer is not 16-byte aligned    */
     MARLIN_ERR_WORKSPACE_TOO_SMALL = 5, /* workspace_bytes < marlin_workspace_bytes */
     MARLIN_ERR_HIP = 6,               /* a HIP runtime call or launch failed        */
-    MARLIN_ERR_INVALID_SPARSITY = 7   /* reserved for the 2:4 entry points          */
+    MARLIN_ERR_INVALID_SPARSITY = 7,  /* reserved for the 2:4 entry points          */
+    MARLIN_ERR_INVALID_ARGUMENT = 8   /* another argument out of its range          */
 } marlin_status_t;
 
 /* Version of the packed weight / scale layouts described below.  A packed
@@ -255,6 +256,40 @@ marlin_status_t marlin_gemm_sparse(const uint16_t *A, const void *w_packed,
 /* marlin_describe_sparse - as marlin_describe, for marlin_gemm_sparse. */
 marlin_status_t marlin_describe_sparse(int64_t M, int64_t N, int64_t K, int64_t group,
                                        char *buf, size_t buf_bytes);
+
+/*
+ * ---- Quantiser (Section 2.2, Eq. 1, symmetric; Section 3.5 clipping) ----
+ *
+ * marlin_quantize - fp16 weights W [K][N] -> codes q and scales s in the
+ * format of marlin_pack_weights (w = s * (q - 8)).
+ *
+ * Each group of `group` consecutive rows of a column (or the whole column,
+ * group = -1 or K) is quantised uniformly onto [-a, a] with the fixed zero
+ * point 8: s = fp16(2a / 15), q = clamp(rint(v * (1/s)) + 8, 0, 15), the
+ * symmetric form of Eq. 1 (Section 2.2) in the format the kernel decodes.
+ * The clipping threshold a = r * max|v| is chosen per group among the
+ * `n_ratios` ratios r: the one whose reconstruction error
+ * sum (v - s (q - 8))^2 (Section 2.2) is smallest, the first one on ties
+ * (Section 3.5 names this group-wise clipping search as part of its GPTQ
+ * variant; GPTQ's calibration-data updates are not part of this call).
+ * A group whose scale rounds to 0 in fp16 gets s = 0 and every code 8.
+ * All arithmetic is fp32 in a fixed order (sequential sum over the group's
+ * rows, no contracted multiply-adds), so the output is bit-for-bit a
+ * function of the input.
+ *
+ *   W          device, fp16 [K][N] row-major, read only; finite values.
+ *   ratios     HOST, n_ratios fp32 values in (0, 1], read during the call
+ *              (e.g. {1} for plain round-to-nearest, or 1, 0.95, ..., 0.55).
+ *   n_ratios   1..64.
+ *   q          device, uint8 [K][N], written (values 0..15).
+ *   s          device, fp16 [G][N], written (G = K / group).
+ * Shapes and groups as for marlin_pack_weights.  No workspace.
+ * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,
+ * INVALID_ARGUMENT (n_ratios or a ratio out of range), HIP.
+ */
+marlin_status_t marlin_quantize(const uint16_t *W, int64_t K, int64_t N, int64_t group,
+                                const float *ratios, int n_ratios, uint8_t *q, uint16_t *s,
+                                hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -5,9 +5,10 @@ The compute runs in hand-written HIP kernels behind the C ABI of
 ``python -m paper_2408_11743_amd.build``).  This package is the binding:
 
 * ``marlin_*``   one function per C entry point, same names (``_binding``);
-* ``pack``, ``unpack``, ``gemm``, ``Workspace``: tensor helpers that
-  allocate outputs with PyTorch and call the entry points on the current
-  stream (``ops``; ``sparse=True`` selects the 2:4 sparse entry points);
+* ``pack``, ``unpack``, ``gemm``, ``quantize``, ``Workspace``: tensor
+  helpers that allocate outputs with PyTorch and call the entry points on
+  the current stream (``ops``; ``sparse=True`` selects the 2:4 sparse entry
+  points);
 * ``roofline``:  byte / FLOP accounting and MI355X peaks used by the bench.
 
 Importing the package does not load the library; the first call does, and
@@ -27,9 +28,10 @@ from ._binding import (  # noqa: F401
     marlin_packed_scale_bytes,
     marlin_packed_sparse_weight_bytes,
     marlin_packed_weight_bytes,
+    marlin_quantize,
     marlin_status_string,
     marlin_unpack_sparse_weights,
     marlin_unpack_weights,
     marlin_workspace_bytes,
 )
-from .ops import Workspace, gemm, pack, unpack  # noqa: F401
+from .ops import CLIP_RATIOS, Workspace, gemm, pack, quantize, unpack  # noqa: F401

@@ -23,6 +23,7 @@ STATUS = {
     5: "MARLIN_ERR_WORKSPACE_TOO_SMALL",
     6: "MARLIN_ERR_HIP",
     7: "MARLIN_ERR_INVALID_SPARSITY",
+    8: "MARLIN_ERR_INVALID_ARGUMENT",
 }
 LAYOUT_VERSION = 1
 
@@ -43,6 +44,8 @@ SIGNATURES = {
     "marlin_unpack_sparse_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "marlin_gemm_sparse": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _vp]),
     "marlin_describe_sparse": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_char_p, _sz]),
+    "marlin_quantize": (ctypes.c_int, [_vp, _i64, _i64, _i64, ctypes.POINTER(ctypes.c_float), ctypes.c_int,
+                                       _vp, _vp, _vp]),
 }
 
 
@@ -168,3 +171,11 @@ def marlin_describe_sparse(M: int, N: int, K: int, group: int) -> str:
     buf = ctypes.create_string_buffer(256)
     _check("marlin_describe_sparse", lib().marlin_describe_sparse(M, N, K, group, buf, len(buf)))
     return buf.value.decode()
+
+
+def marlin_quantize(W, K, N, group, ratios, q, s, stream=None) -> None:
+    """ratios: a host sequence of floats (copied into a C array here)."""
+    rs = [float(r) for r in ratios]
+    arr = (ctypes.c_float * max(1, len(rs)))(*rs)
+    _check("marlin_quantize", lib().marlin_quantize(_ptr(W), K, N, group, arr, len(rs),
+                                                    _ptr(q), _ptr(s), _stream(stream)))

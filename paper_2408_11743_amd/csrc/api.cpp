@@ -10,6 +10,7 @@
 
 #include "marlin.h"
 #include "internal.h"
+#include "quant.h"
 
 namespace marlin {
 
@@ -455,6 +456,7 @@ const char *marlin_status_string(marlin_status_t status)
     case MARLIN_ERR_WORKSPACE_TOO_SMALL: return "MARLIN_ERR_WORKSPACE_TOO_SMALL";
     case MARLIN_ERR_HIP: return "MARLIN_ERR_HIP";
     case MARLIN_ERR_INVALID_SPARSITY: return "MARLIN_ERR_INVALID_SPARSITY";
+    case MARLIN_ERR_INVALID_ARGUMENT: return "MARLIN_ERR_INVALID_ARGUMENT";
     }
     return "MARLIN_ERR_UNKNOWN";
 }
@@ -488,6 +490,21 @@ marlin_status_t marlin_pack_weights(const uint8_t *q, const uint16_t *s, int64_t
     if (!aligned16(w_packed) || !aligned16(s_packed)) return MARLIN_ERR_MISALIGNED;
     const hipError_t e = launch_pack(q, s, (int)K, (int)N, (int)scale_rows(K, group),
                                      (uint32_t *)w_packed, (uint16_t *)s_packed, stream);
+    return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
+}
+
+marlin_status_t marlin_quantize(const uint16_t *W, int64_t K, int64_t N, int64_t group, const float *ratios,
+                                int n_ratios, uint8_t *q, uint16_t *s, hipStream_t stream)
+{
+    if (!W || !ratios || !q || !s) return MARLIN_ERR_NULL_POINTER;
+    const marlin_status_t st = check_weights(K, N, group);
+    if (st != MARLIN_OK) return st;
+    if (!aligned16(W) || !aligned16(q) || !aligned16(s)) return MARLIN_ERR_MISALIGNED;
+    if (n_ratios < 1 || n_ratios > kMaxQuantRatios) return MARLIN_ERR_INVALID_ARGUMENT;
+    for (int i = 0; i < n_ratios; ++i)
+        if (!(ratios[i] > 0.0f && ratios[i] <= 1.0f)) return MARLIN_ERR_INVALID_ARGUMENT;  // NaN too
+    const int64_t g = (group == -1) ? K : group;
+    const hipError_t e = launch_quantize(W, (int)K, (int)N, (int)g, ratios, n_ratios, q, s, stream);
     return e == hipSuccess ? MARLIN_OK : MARLIN_ERR_HIP;
 }
 

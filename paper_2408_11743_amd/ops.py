@@ -98,3 +98,25 @@ def gemm(A: torch.Tensor, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, gr
     fn = B.marlin_gemm_sparse if sparse else B.marlin_gemm
     fn(A, wp, sp, out, buf, buf.numel(), M, N, K, g, _cur_stream(A))
     return out
+
+
+# Clipping ratios searched by default: 1, 0.95, ..., 0.55 (shrinking the
+# group's range by up to 45% in steps of 5%).
+CLIP_RATIOS = tuple(1.0 - 0.05 * i for i in range(10))
+
+
+def quantize(W: torch.Tensor, group=128, ratios=CLIP_RATIOS):
+    """fp16 W [K, N] -> (q uint8 [K, N], s fp16 [G, N]) by ``marlin_quantize``
+    (symmetric, zero point 8, group-wise clipping search over ``ratios``;
+    ``ratios=(1.0,)`` is plain round-to-nearest).  ``pack(q, s, group)``
+    then gives the GEMM's operands."""
+    if W.dtype != torch.float16 or not W.is_cuda:
+        raise TypeError("quantize: W must be a float16 device tensor")
+    W = W.contiguous()
+    K, N = W.shape
+    g = _group(K, group)
+    G = 1 if g == -1 else K // g
+    q = torch.empty((K, N), dtype=torch.uint8, device=W.device)
+    s = torch.empty((G, N), dtype=torch.float16, device=W.device)
+    B.marlin_quantize(W, K, N, g, ratios, q, s, _cur_stream(W))
+    return q, s

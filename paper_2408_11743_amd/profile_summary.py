@@ -5,8 +5,8 @@ Usage (after the three profiling runs, see the command block this prints):
     python -m paper_2408_11743_amd.profile_summary --trace DIR --fetch DIR \
         --write DIR --bench BENCH_JSON --out OUT_PREFIX [--copy-mb 256]
 
-or, for bench.py --prefill-only, a kernel trace alone (its CSV, not only the
-statistics: --kernel-trace --stats --output-format csv):
+or, for bench.py --prefill-only or --quantize-only, a kernel trace alone (its
+CSV, not only the statistics: --kernel-trace --stats --output-format csv):
 
     python -m paper_2408_11743_amd.profile_summary --trace DIR --bench BENCH_JSON --out OUT_PREFIX
 
@@ -81,6 +81,63 @@ def short(name: str) -> str:
     return base.split("::")[-1]
 
 
+def dispatch_runs(trace_dir: str, prefix: str, gap_ns: int = 20_000_000) -> list:
+    """Runs of consecutive dispatches of kernels named prefix*: a run ends at
+    any other kernel or at an idle gap of more than gap_ns (a case's replays
+    are back to back; the host prepares the next case in between).  Runs of
+    one dispatch (the eager launch before a graph capture, followed by the
+    capture's own fill kernels) are left out."""
+    trace = []
+    with open(_one(os.path.join(trace_dir, "**", "*kernel_trace.csv"))) as f:
+        for r in csv.DictReader(f):
+            trace.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), short(r["Kernel_Name"])))
+    trace.sort()
+    runs, cur, last_end = [], [], None
+    for t0, t1, name in trace:
+        if name.startswith(prefix):
+            if cur and last_end is not None and t0 - last_end > gap_ns:
+                runs.append(cur)
+                cur = []
+            cur.append((name, (t1 - t0) / 1e3))
+            last_end = t1
+        elif cur:
+            runs.append(cur)
+            cur = []
+    if cur:
+        runs.append(cur)
+    return [r for r in runs if len(r) > 1]
+
+
+def quantize_summary(a, bench: dict) -> None:
+    """Kernel trace of bench.py --quantize-only: one row per shape."""
+    import paper_2408_11743_amd.roofline as R
+    cases = bench["quantize"]["per_shape"]
+    runs = dispatch_runs(a.trace, "quantize_kernel")
+    if len(runs) != len(cases):
+        raise SystemExit("%d quantiser runs in the trace for %d cases" % (len(runs), len(cases)))
+    md = ["# Kernel trace: weight quantiser, g = 128, clipping search over %d ratios" % cases[0]["ratios"], "",
+          "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
+          "Per shape: the median kernel duration over the shape's replayed dispatches",
+          "(rocprofv3), the bench's event time per call of an unprofiled run (--bench),",
+          "and the fraction of the fp32 vector lane rate (78.65 T operations/s: the",
+          "published 157.3 TFLOP/s counts a fused multiply-add as two) that the",
+          "quantiser's algorithmic operations (`roofline.quant_ops`) reach in the",
+          "kernel time; HBM GB/s for reference (fp16 read, codes and scales written):", "",
+          "| K | N | kernel | dispatches | median kernel us | bench us | G weights/s | ALU frac | HBM GB/s |",
+          "|---|---|---|---|---|---|---|---|---|"]
+    for case, run in zip(cases, runs):
+        names = sorted({n for n, _ in run})
+        med = statistics.median(d for _, d in run)
+        K, N = case["K"], case["N"]
+        ops = R.quant_ops(K, N, case["ratios"])
+        md.append("| %d | %d | `%s` | %d | %.1f | %.1f | %.2f | %.3f | %.0f |" % (
+            K, N, ", ".join(names), len(run), med, case["us"], K * N / med / 1e3,
+            ops / (med * 1e-6) / R.FP32_LANE_OPS, R.quant_bytes(K, N, case["group"]) / med / 1e3))
+    md.append("")
+    open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
+    print("wrote", a.out + "_kernel_trace.md")
+
+
 def prefill_summary(a, bench: dict) -> None:
     """Kernel trace of bench.py --prefill-only: one row per (K, N, M) case.
 
@@ -90,23 +147,7 @@ def prefill_summary(a, bench: dict) -> None:
     i-th run belongs to the i-th case of the bench output."""
     sec = bench["prefill"]
     cases = sec["per_m"]
-    trace = []
-    with open(_one(os.path.join(a.trace, "**", "*kernel_trace.csv"))) as f:
-        for r in csv.DictReader(f):
-            trace.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), short(r["Kernel_Name"])))
-    trace.sort()
-    runs, cur = [], []
-    for t0, t1, name in trace:
-        if name.startswith("w4a16_"):
-            cur.append((name, (t1 - t0) / 1e3))
-        elif cur:
-            runs.append(cur)
-            cur = []
-    if cur:
-        runs.append(cur)
-    # the graph replays of a case; the one eager launch before each capture
-    # stands alone (the capture's own fill kernels follow it)
-    runs = [r for r in runs if len(r) > 1]
+    runs = dispatch_runs(a.trace, "w4a16_")
     if len(runs) != len(cases):
         raise SystemExit("%d GEMM runs in the trace for %d cases (run with the fp16 comparator)" %
                          (len(runs), len(cases)))
@@ -155,6 +196,9 @@ def main() -> None:
     bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
     if "prefill" in bench and "config" not in bench:  # bench.py --prefill-only
         prefill_summary(a, bench)
+        return
+    if "quantize" in bench and "config" not in bench:  # bench.py --quantize-only
+        quantize_summary(a, bench)
         return
     if not a.fetch or not a.write:
         raise SystemExit("--fetch and --write are required for the M sweeps")

@@ -97,3 +97,26 @@ def ridge_m(g: int = 128, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS, bits: int = 
     """M at which weight bytes / bw equals 2MNK / peak (A and C ignored)."""
     per_weight = bits / 8.0 + 2.0 / g
     return (peak / bw) * per_weight / 2.0
+
+
+# ---- quantiser (symmetric uniform quantisation with a clipping search) ----
+# fp32 vector lanes per CU and clock: the published fp32 vector peak,
+# 157.3 TFLOP/s, counts a fused multiply-add as 2 FLOPs over 256 CUs at
+# 2.4 GHz, i.e. 128 lanes per CU per clock; an operation that is not a fused
+# multiply-add retires at that lane rate.
+FP32_VECTOR_FLOPS = 157.3e12
+FP32_LANE_OPS = FP32_VECTOR_FLOPS / 2
+
+
+def quant_ops(K: int, N: int, n_ratios: int) -> float:
+    """fp32 vector operations the quantiser must perform, K*N weights:
+    per weight one max of magnitudes, then per ratio the code (scale
+    multiply, round, clamp) and its error term (multiply back, subtract,
+    square, accumulate): 7, and the final code (multiply, round, clamp,
+    offset): 4."""
+    return float(K) * N * (1 + 7 * n_ratios + 4)
+
+
+def quant_bytes(K: int, N: int, g) -> float:
+    """HBM bytes: fp16 weights read, one code byte and the fp16 scales written."""
+    return 2.0 * K * N + 1.0 * K * N + 2.0 * num_groups(K, g) * N

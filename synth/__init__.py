@@ -15,6 +15,11 @@ layers the paper benchmarks in Section 5.1):
 * scales: one fp16 scale per group of g consecutive rows of K in each
   column, s = fp16(u / (8 * sqrt(K))), u ~ U[0.5, 1.5]; g = K means one
   scale per output channel.  With these scales Var(C) is O(1).
+* unquantised fp16 weights (input of the quantiser), [K, N]: per column a
+  spread sigma = u / sqrt(K), u ~ U[0.5, 1.5], times N(0, 1) draws, and one
+  entry in 1000 multiplied by 8 (the outlier weights of trained LLM layers,
+  which are what a clipping search trades against); drawn in fp32, rounded
+  to fp16.
 
 Seeds: numpy's PCG64 (``default_rng``) keyed by a tuple, so every draw is
 reproducible from (workload id, shape).  Weights and activations use
@@ -31,6 +36,7 @@ __all__ = [
     "weights",
     "activations",
     "sparse24_weights",
+    "fp16_weights",
     "num_groups",
 ]
 
@@ -99,3 +105,14 @@ def sparse24_weights(wid: int, K: int, N: int, g: int | None):
     u = rng.uniform(0.5, 1.5, size=(G, N))
     s = (u / (8.0 * math.sqrt(K))).astype(np.float16)
     return q, keep, s
+
+
+def fp16_weights(wid: int, K: int, N: int):
+    """Draw W float16 [K, N]: unquantised weights (recipe in the module doc)."""
+    rng = np.random.default_rng([int(wid), 3, int(K), int(N)])
+    sigma = (rng.uniform(0.5, 1.5, size=(1, N)) / math.sqrt(K)).astype(np.float32)
+    w = rng.standard_normal((K, N), dtype=np.float32)
+    w *= sigma
+    outlier = rng.random((K, N), dtype=np.float32) < 1e-3
+    w[outlier] *= 8.0
+    return w.astype(np.float16)

@@ -238,3 +238,24 @@ def test_sparse_entry_points(L):
     for M in (1, 16, 32, 64, 128):
         d = B.marlin_describe_sparse(M, 8192, 8192, 128)
         assert d.startswith("w4a16_sparse_kernel<") and d.endswith(tuple("0123456789")), d
+
+
+def test_quantize_rejects_bad_arguments(L):
+    # every case fails host validation before any HIP call
+    def call(W=FAKE, K=4096, N=4096, g=128, ratios=(1.0,), n=None, q=FAKE, s=FAKE):
+        arr = (ctypes.c_float * max(1, len(ratios)))(*ratios)
+        return L.marlin_quantize(W, K, N, g, arr if ratios is not None else None,
+                                 len(ratios) if n is None else n, q, s, None)
+    ARG = 8
+    assert call(W=None) == NULLP and call(q=None) == NULLP and call(s=None) == NULLP
+    assert L.marlin_quantize(FAKE, 4096, 4096, 128, None, 1, FAKE, FAKE, None) == NULLP
+    assert call(K=4000) == SHAPE and call(N=100) == SHAPE
+    assert call(g=64) == GROUP and call(g=384) == GROUP
+    assert call(W=FAKE + 2) == ALIGN and call(q=FAKE + 8) == ALIGN
+    assert call(n=0) == ARG and call(ratios=(1.0,) * 65) == ARG
+    for bad in [(0.0,), (1.5,), (-0.5,), (float("nan"),), (1.0, 0.9, 1.01)]:
+        assert call(ratios=bad) == ARG, bad
+    assert L.marlin_status_string(ARG).decode() == "MARLIN_ERR_INVALID_ARGUMENT"
+    with pytest.raises(B.MarlinError) as e:
+        B.marlin_quantize(FAKE, 4096, 4096, 128, [2.0], FAKE, FAKE)
+    assert e.value.status == ARG
