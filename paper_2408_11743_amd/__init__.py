@@ -9,6 +9,8 @@ The compute runs in hand-written HIP kernels behind the C ABI of
   helpers that allocate outputs with PyTorch and call the entry points on
   the current stream (``ops``; ``sparse=True`` selects the 2:4 sparse entry
   points);
+* ``MarlinLinear`` and the operator ``torch.ops.marlin_mi355x.gemm``
+  (``torch_op``), registered on import;
 * ``roofline``:  byte / FLOP accounting and MI355X peaks used by the bench.
 
 Importing the package does not load the library; the first call does, and
@@ -35,3 +37,4 @@ from ._binding import (  # noqa: F401
     marlin_workspace_bytes,
 )
 from .ops import CLIP_RATIOS, Workspace, gemm, pack, quantize, unpack  # noqa: F401
+from .torch_op import MarlinLinear  # noqa: F401  (registers torch.ops.marlin_mi355x.gemm)
