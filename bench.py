@@ -269,7 +269,7 @@ def quantize_section(args, mk, R, synth, torch, np, dev):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(the GEMM would shard by columns, or by rows with an RCCL "
               "all-reduce of C). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
