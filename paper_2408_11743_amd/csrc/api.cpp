@@ -141,11 +141,16 @@ TileCost tile_cost(int nw, int wm, int mbw, int nbw)
     return {per4k * nbw, 7.0, 0.5};
 }
 // Fixed cost of a launch (dispatch, prologue, epilogue), the sustained weight
-// stream of the whole chip, and the stream kernel's combination: 3 us with
-// fp32 partial tiles up to 4 KiB per work-group, 4.5 us with 8 KiB.
+// stream of the whole chip, and the stream kernel's combination of a shared
+// tile: 3 us with fp32 partial tiles up to 4 KiB per work-group, 4.5 us with
+// 8 KiB, plus 0.45 us per contributor beyond four (ranges of a few blocks,
+// as on tensor-parallel shards of a layer, give a dozen contributors per
+// tile; fitted to 192 Stream-K timings on layer shapes and such shards).
 constexpr double kFixedUs = 4.0;
 constexpr double kChipBytesPerUs = 7.0e6;
 double stream_tail_us(int slot_kib) { return slot_kib > 4 ? 4.5 : 3.0; }
+constexpr double kStreamFreeContributors = 4.0;
+constexpr double kStreamTailPerExtraContributorUs = 0.45;
 
 // Bytes of weights per microsecond one work-group streams, by rows of A,
 // nb = 4, 2, 1 and waves per work-group (measured; the activation rows arrive
@@ -174,7 +179,8 @@ namespace {
 // Best partition of `tiles` tiles of KU units each over at most `grid`
 // work-groups, given the time of one unit: whole tiles per work-group, or a
 // Stream-K split that pays for combining shared tiles at the end (tail_us,
-// plus tail_per_contributor_us per contributor of a shared tile).  Every
+// plus tail_per_contributor_us per contributor of a shared tile, plus
+// tail_per_extra_contributor_us per contributor beyond free_contributors).  Every
 // launch costs kFixedUs, and no partition streams faster than floor_us.
 struct Partition {
     double t;
@@ -183,7 +189,8 @@ struct Partition {
 };
 
 Partition best_partition(int64_t tiles, int KU, int64_t grid, double unit_us, double tail_us,
-                         double tail_per_contributor_us, double floor_us)
+                         double tail_per_contributor_us, double floor_us, double free_contributors = 0.0,
+                         double tail_per_extra_contributor_us = 0.0)
 {
     Partition best{1e30, 0, 1};
     if (forced().whole != 0) {
@@ -198,7 +205,10 @@ Partition best_partition(int64_t tiles, int KU, int64_t grid, double unit_us, do
         const double per = (double)units / (double)g;  // units per work-group
         const bool split = (units % g) != 0 || (units / g) % KU != 0;
         const double contributors = split ? 1.0 + (double)KU / per : 1.0;
-        const double tail = split ? tail_us + tail_per_contributor_us * contributors : 0.0;
+        const double extra = contributors > free_contributors ? contributors - free_contributors : 0.0;
+        const double tail = split ? tail_us + tail_per_contributor_us * contributors +
+                                        tail_per_extra_contributor_us * extra
+                                  : 0.0;
         const double stream = per * unit_us;
         const double t = kFixedUs + (stream > floor_us ? stream : floor_us) + tail;
         if (t < best.t) best = {t, 0, g};
@@ -251,7 +261,8 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
                 // fp32 partial tile: 16 x 16 x 4 bytes per block
                 const Partition pt = best_partition(tiles, KU, grid, unit_bytes / rate,
                                                     stream_tail_us(nb * cfg.mb), 0.0,
-                                                    layer_bytes / kChipBytesPerUs);
+                                                    layer_bytes / kChipBytesPerUs, kStreamFreeContributors,
+                                                    kStreamTailPerExtraContributorUs);
                 if (pt.t < best) {
                     best = pt.t;
                     cfg.nb = nb;
