@@ -346,3 +346,18 @@ def test_full_size_layers_sampled(mk, wid, K, N, g):
         mi, ni = _samples(M, N, 1500, [wid, K, N, M])
         ref = oracle.gemm_sampled(A, q, s, g, mi, ni)
         check_close(C[mi, ni], ref, "K=%d N=%d g=%d M=%d sampled" % (K, N, g, M))
+
+
+@pytest.mark.parametrize("wid,K,N", [(1, 4096, 4096), (3, 28672, 8192)])
+def test_prefill_bench_configurations_sampled(mk, wid, K, N):
+    # the large-batch cases bench.py times (one launch per call, the library's
+    # own configuration), on sampled outputs
+    g = 128
+    q, s = synth.weights(wid, K, N, g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    ws = mk.Workspace("cuda")
+    for M in (256, 1024, 4096):
+        A = synth.activations(wid, M, K)
+        C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws).cpu().numpy()
+        mi, ni = _samples(M, N, 1500, [wid, K, N, M, 1])
+        check_close(C[mi, ni], oracle.gemm_sampled(A, q, s, g, mi, ni), "prefill K=%d N=%d M=%d sampled" % (K, N, M))

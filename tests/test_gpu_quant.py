@@ -98,7 +98,7 @@ def test_quantize_is_deterministic_and_writes_everything(mk):
 
 
 @pytest.mark.parametrize("wid,K,N,g", [(3, 8192, 28672, 128), (3, 28672, 8192, 128),
-                                       (2, 11008, 4096, -1), (2, 4096, 11008, 128)])
+                                       (2, 11008, 4096, -1), (2, 4096, 11008, 128), (1, 4096, 4096, 128)])
 def test_quantize_full_size_sampled_columns(mk, wid, K, N, g):
     W = synth.fp16_weights(wid, K, N)
     q, s = mk.quantize(dev(W), group=g, ratios=CLIP)
