@@ -98,6 +98,10 @@ PREFILL_SHAPES = [(4096, 4096, 1), (28672, 8192, 3)]
 PREFILL_M = [256, 1024, 4096]
 
 
+def cpu_threads() -> int:
+    return int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+
+
 def graph_time_us(launch, count, stream, reps, torch, np):
     """Median per-launch time of a graph of `count` launches (launch(i))."""
     gr = torch.cuda.CUDAGraph()
@@ -179,8 +183,23 @@ def sparse_section(args, mk, R, synth, torch, np, dev):
         log("sparse 2:4 %dx%d M=%3d: %.3f us (dense W4 %.3f us, fp16 %s us), roofline frac %.3f" %
             (K, N, M, t[True], t[False], "%.3f" % t16 if t16 else "-", troof / t[True]))
     del copies, w16s
+    cpu = None
+    if not args.no_cpu_baseline:
+        # the fp64 oracle over the whole sweep (the sparse product is the dense
+        # definition on the pruned matrix)
+        import oracle
+        tot, flops = 0.0, 0.0
+        for M in M_SWEEP:
+            A_np = synth.activations(SPARSE_WID, M, K)
+            c0 = time.perf_counter()
+            oracle.gemm(A_np, q, s, g)
+            tot += time.perf_counter() - c0
+            flops += R.flops(M, N, K)
+        cpu = {"value": round(flops / tot / 1e12, 6), "unit": "TFLOP/s", "cores": cpu_threads(),
+               "kind": "oracle", "seconds": round(tot, 3), "sample": "the whole M sweep, one run per M"}
+        log("sparse oracle: %.2f s for the sweep" % tot)
     return {"workload": "2:4 sparse W4A16 GEMM, K=%d N=%d g=%d, M sweep %s" % (K, N, g, M_SWEEP),
-            "bound": "hbm", "per_m": rows}
+            "bound": "hbm", "per_m": rows, "cpu_baseline": cpu}
 
 
 def prefill_section(args, mk, R, synth, torch, np, dev):
@@ -193,7 +212,7 @@ def prefill_section(args, mk, R, synth, torch, np, dev):
     L = mk.lib()
     stream = torch.cuda.Stream(device=dev)
     ws = mk.Workspace(dev)
-    rows = []
+    rows, cpu_rows = [], []
     for (K, N, wid) in PREFILL_SHAPES:
         g = GROUP
         q, s = synth.weights(wid, K, N, g)
@@ -228,9 +247,23 @@ def prefill_section(args, mk, R, synth, torch, np, dev):
                 (K, N, M, t, rec["TFLOPs"], 100 * rec["mfma_frac"], rec.get("fp16_us", "-")))
             del A, C
         del wps, wp, sp, w16
+        if not args.no_cpu_baseline:
+            # the fp64 oracle at the smallest batch of the section, in full
+            import oracle
+            M = PREFILL_M[0]
+            A_np = synth.activations(wid, M, K)
+            c0 = time.perf_counter()
+            oracle.gemm(A_np, q, s, g)
+            dt = time.perf_counter() - c0
+            cpu_rows.append({"K": K, "N": N, "M": M, "value": round(R.flops(M, N, K) / dt / 1e12, 6),
+                             "seconds": round(dt, 3), "sample": "all %d x %d outputs" % (M, N)})
+            log("prefill oracle %dx%d M=%d: %.2f s" % (K, N, M, dt))
+    cpu = None
+    if cpu_rows:
+        cpu = {"unit": "TFLOP/s", "cores": cpu_threads(), "kind": "oracle", "per_shape": cpu_rows}
     return {"workload": "W4A16 GEMM, one launch per call, g=%d, (K, N) in %s, M in %s" %
                         (GROUP, [sh[:2] for sh in PREFILL_SHAPES], PREFILL_M),
-            "bound": "mfma", "peak_TFLOPs": R.FP16_MFMA_FLOPS / 1e12, "per_m": rows}
+            "bound": "mfma", "peak_TFLOPs": R.FP16_MFMA_FLOPS / 1e12, "per_m": rows, "cpu_baseline": cpu}
 
 
 def quantize_section(args, mk, R, synth, torch, np, dev):
@@ -242,7 +275,7 @@ def quantize_section(args, mk, R, synth, torch, np, dev):
     L = mk.lib()
     stream = torch.cuda.Stream(device=dev)
     ratios = list(mk.CLIP_RATIOS)
-    rows = []
+    rows, cpu_rows = [], []
     for (K, N, wid) in PREFILL_SHAPES:
         g = GROUP
         W = torch.from_numpy(synth.fp16_weights(wid, K, N)).to(dev)
@@ -260,10 +293,25 @@ def quantize_section(args, mk, R, synth, torch, np, dev):
         rows.append(rec)
         log("quantize %dx%d g=%d, %d ratios: %.1f us, %.2f G weights/s, %.1f%% of the fp32 lane rate" %
             (K, N, g, len(ratios), t, rec["Gweights_per_s"], 100 * rec["alu_frac"]))
+        if not args.no_cpu_baseline:
+            # the quantiser's oracle (numpy, fp32) on all columns, or on the
+            # first 1024 where that takes too long (columns are independent)
+            from oracle import quant as oq
+            cols = N if K * N <= 4096 * 4096 else 1024
+            W_np = np.ascontiguousarray(W[:, :cols].cpu().numpy())
+            c0 = time.perf_counter()
+            oq.quantize(W_np, g, ratios)
+            dt = time.perf_counter() - c0
+            cpu_rows.append({"K": K, "N": N, "value": round(K * cols / dt / 1e9, 6), "unit": "G weights/s",
+                             "seconds": round(dt, 3), "sample": "%d of %d columns" % (cols, N)})
+            log("quantize oracle %dx%d: %.2f s for %d columns" % (K, N, dt, cols))
         del W, q, s
+    cpu = None
+    if cpu_rows:
+        cpu = {"unit": "G weights/s", "cores": cpu_threads(), "kind": "oracle", "per_shape": cpu_rows}
     return {"workload": "quantiser fp16 -> (q, s), g=%d, %d clipping ratios, (K, N) in %s" %
                         (GROUP, len(mk.CLIP_RATIOS), [sh[:2] for sh in PREFILL_SHAPES]),
-            "bound": "alu", "peak_lane_ops_per_s": R.FP32_LANE_OPS, "per_shape": rows}
+            "bound": "alu", "peak_lane_ops_per_s": R.FP32_LANE_OPS, "per_shape": rows, "cpu_baseline": cpu}
 
 
 def main():
@@ -453,7 +501,7 @@ def main():
     parity = None
     if not args.no_cpu_baseline:
         import oracle
-        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+        threads = cpu_threads()
         tot = 0.0
         worst = 0.0
         ok = True
