@@ -73,8 +73,10 @@ size_t marlin_packed_scale_bytes(int64_t K, int64_t N, int64_t group);
 /* Bytes of the workspace marlin_gemm (and marlin_gemm_sparse) needs for
  * this problem (arrival counters plus fp32 partial tiles of the Stream-K
  * style split, Section 3.4 "Striped Partitioning").  Pure host arithmetic:
- * it makes no HIP call and does not depend on the device.  Returns 0 for
- * invalid arguments. */
+ * it makes no HIP call and does not depend on the device (it is the size for
+ * a 256-compute-unit device; on a device with fewer compute units, a launch
+ * whose preferred split would need more is planned to fit it).  Memoised:
+ * a repeated query is a table lookup.  Returns 0 for invalid arguments. */
 size_t marlin_workspace_bytes(int64_t M, int64_t N, int64_t K, int64_t group);
 
 /*
@@ -154,7 +156,9 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  * waves=<4|8>,nw=<4|8>,ks=<1|2|4>" (any subset: kernel, column blocks per
  * tile, partition, work-groups, stream-kernel waves per work-group, tile-kernel
  * waves and 128-row blocks per stage) overrides it where the shape allows,
- * read at every call;
+ * read at every call (parsed again only when its text changes);
+ * configurations are memoised per shape, device and override, so a repeated
+ * call plans in a table lookup;
  * marlin_workspace_bytes follows the same override, so size the workspace
  * under the setting the calls will see.
  * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED,

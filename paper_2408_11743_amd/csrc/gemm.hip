@@ -619,11 +619,6 @@ __global__ void __launch_bounds__(64 * KW, 1) w4a16_sparse_kernel(GemmProblem p)
 
 }  // namespace
 
-int slot_floats(const GemmConfig &cfg)
-{
-    return cfg.kind == kKindTile ? cfg.tile_nw * cfg.nb * cfg.mb * 256 : cfg.nb * cfg.mb * 256;
-}
-
 // Ring depth: stages in flight per wave (weights in registers: NB words of
 // 16 bytes per lane per stage, so narrow tiles afford deep rings).  Eight
 // waves keep as many bytes in flight per work-group with half the depth

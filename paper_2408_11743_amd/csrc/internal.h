@@ -6,44 +6,10 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "marlin.h"
+#include "plan.h"
+
 namespace marlin {
-
-// One launch configuration of the GEMM kernel.
-//   mb   : 16-row blocks of A per row group (1 or 2)
-//   rg   : row groups of 32 rows (M > 32), each a separate set of tiles
-//   nb   : 16-column blocks per column tile (1, 2 or 4)
-//   ar   : 0, or (mb <= 2) the activation rows arrive in LDS, 4 * ar of them
-//   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
-//   grid : work-groups
-//   waves: stream kernel waves per work-group (they split K): 4, or 8 (two per
-//          SIMD) with one 16-row block or one 16-column block
-constexpr int kStreamOcc = 1;    // work-groups per compute unit
-
-constexpr int kKindStream = 0;  // w4a16_stream_kernel (any M; row groups of 32)
-constexpr int kKindTile = 1;    // w4a16_tile_kernel (activation tile shared by the waves)
-
-struct GemmConfig {
-    int kind;
-    int mb;
-    int nb;
-    int ar;
-    int rg;
-    int whole;
-    int grid;
-    int tile_wm;  // tile kernel: waves along M (1: 4x1 waves; 2: 2x2 waves); mb, nb: row and
-                  // column blocks per wave
-    int sparse;   // 2:4 sparse weights (stream kernel only)
-    int tile_ks;  // tile kernel: 128-row blocks of K per work-group stage
-    int tile_nw;  // tile kernel: waves per work-group (4 or 8)
-    int waves;    // stream kernel: waves per work-group (4 or 8)
-};
-
-// Columns and rows of one tile of a configuration.
-inline int tile_cols(const GemmConfig &c)
-{
-    return c.kind == kKindTile ? (c.tile_nw / c.tile_wm) * 16 * c.nb : 16 * c.nb;
-}
-inline int tile_rows(const GemmConfig &c) { return c.kind == kKindTile ? c.tile_wm * 16 * c.mb : 16 * c.mb; }
 
 struct GemmProblem {
     const uint16_t *A;
@@ -68,50 +34,29 @@ struct GemmProblem {
     uint32_t ku_magic;    // ceil(2^32 / KU) where u / KU = mulhi(u, ku_magic) for every unit u, else 0
 };
 
-// ceil(2^32 / d) for 2 <= d: with it, floor(n / d) = floor(n * m / 2^32) for
-// every n with n * d <= 2^32 (m = (2^32 + e) / d, 0 <= e < d, so the error
-// n * e / (d 2^32) stays below 1/d).  0 when d < 2.
-inline uint32_t reciprocal32(uint64_t d)
-{
-    return d < 2 ? 0u : (uint32_t)((((uint64_t)1 << 32) + d - 1) / d);
-}
-
-// Upper bound on compute units used (MI355X has 256).  Workspace sizes are
-// computed with this bound, never with the device's.
-constexpr int kMaxCus = 256;
-constexpr int kMaxPerCu = 2;  // work-groups per compute unit, at most
-// Arrival counters at the start of every workspace.  A shared tile's counter
-// is indexed by the tile's first contributor (a work-group index, below
-// kMaxCus * kMaxPerCu) and sits kCounterStride words (one 128-byte line)
-// from the next.  The region keeps its size of 1 MiB (it held one counter
-// per tile of the finest tiling of the largest N before) so that the
-// workspace layout, and a caller's once-zeroed workspace, stay valid.
-constexpr int kCounterStride = 32;
-constexpr size_t kCounterRegionBytes = ((size_t)1 << 20) / 16 * 4 * 4;
-static_assert((size_t)kMaxCus * kMaxPerCu * kCounterStride * 4 <= kCounterRegionBytes, "counter region");
-
-// Rows of A per launch.  A launch covers ceil(rows / 32) row groups of the
-// stream kernel, or one row group per tile height of the tile kernel, each a
-// copy of the weight matrix's tiles in the striped partition (the weights
-// replicated virtually, one copy per segment of A: Section 3.4, Striped
-// Partitioning); the copies read the same weights, mostly through L2.  With
-// K * N < 2^32, the units of a launch (N / 16 column blocks times K / 128
-// weight blocks, below 2^21, times at most 128 row groups) stay below 2^28,
-// so every unit index fits in 32 bits; larger M runs as several launches.
-constexpr int kPassRows = 4096;
-
 // Device facts cached per device.
 int device_cu_count(int device);
 
-GemmConfig choose_config(int M, int N, int K, int group_units, int grid_cap, bool sparse = false);
-size_t workspace_bytes_for(const GemmConfig &cfg, int N);
+// The host-side checks of a GEMM call's arguments, workspace aside (shape,
+// group, pointers, alignment); MARLIN_OK for M == 0 with any pointers.
+marlin_status_t check_gemm_args(const uint16_t *A, const void *w_packed, const void *s_packed, const uint16_t *C,
+                                int64_t M, int64_t N, int64_t K, int64_t group);
+
+// A validated GEMM call (marlin_gemm, marlin_gemm_sparse and the
+// allocation-free entry point).  Argument checks run first; then each launch
+// of up to kPassRows rows is planned on the current device.  fit = false:
+// the workspace must hold required_workspace (else
+// MARLIN_ERR_WORKSPACE_TOO_SMALL); fit = true: every launch is planned to fit
+// workspace_bytes (whole tiles need none of it).
+marlin_status_t gemm_entry(const uint16_t *A, const void *w_packed, const void *s_packed, uint16_t *C,
+                           void *workspace, size_t workspace_bytes, int64_t M, int64_t N, int64_t K, int64_t group,
+                           hipStream_t stream, bool sparse, bool fit);
 
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 // Name of the kernel instantiation launch_gemm runs for cfg ("" if none).
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
-bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

@@ -481,7 +481,8 @@ hipError_t launch_tile(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 
 // Instantiated shapes (waves along M, row blocks per wave, column blocks per
 // wave, 128-row blocks per stage): 64 x 64 per wave for large batches; for
-// up to 32 rows, 16 or 32 rows per wave over 2 or 4 blocks per stage.
+// up to 32 rows, 16 or 32 rows per wave over 2 or 4 blocks per stage.  One
+// case per entry of kTileConfigs (plan.h), which the planner chooses from.
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     switch (cfg.tile_nw * 10000 + cfg.tile_wm * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.tile_ks) {
@@ -494,14 +495,6 @@ hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStre
     case 41222: return launch_tile<4, 1, 2, 2, 2>(cfg, p, stream);
     case 41214: return launch_tile<4, 1, 2, 1, 4>(cfg, p, stream);
     default: return hipErrorInvalidValue;
-    }
-}
-
-bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks)
-{
-    switch (nw * 10000 + wm * 1000 + mbw * 100 + nbw * 10 + ks) {
-    case 41441: case 42441: case 82441: case 82241: case 41142: case 41124: case 41222: case 41214: return true;
-    default: return false;
     }
 }
 

@@ -30,12 +30,17 @@ def pack(q: torch.Tensor, s: torch.Tensor, group=128, sparse: bool = False):
         raise ValueError("pack: q and s must be device tensors")
     if q.dtype != torch.uint8 or s.dtype != torch.float16:
         raise TypeError("pack: q must be uint8, s float16")
+    if q.dim() != 2 or q.device != s.device:
+        raise ValueError("pack: q must be [K, N] on the device of s")
     K, N = q.shape
     g = _group(K, group)
     wb = B.marlin_packed_sparse_weight_bytes(K, N) if sparse else B.marlin_packed_weight_bytes(K, N)
     sb = B.marlin_packed_scale_bytes(K, N, g)
     if wb == 0 or sb == 0:
         raise B.MarlinError("pack", 2)
+    if tuple(s.shape) != (sb // (2 * N), N):
+        raise ValueError("pack: s has shape %s, expected (%d, %d) for K=%d group=%s"
+                         % (tuple(s.shape), sb // (2 * N), N, K, group))
     q = q.contiguous()
     s = s.contiguous()
     wp = torch.empty(wb, dtype=torch.uint8, device=q.device)
@@ -48,6 +53,7 @@ def pack(q: torch.Tensor, s: torch.Tensor, group=128, sparse: bool = False):
 def unpack(wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128, sparse: bool = False):
     """Inverse of ``pack``: returns (q uint8 [K, N], s fp16 [G, N])."""
     g = _group(K, group)
+    _check_packed("unpack", wp, sp, K, N, g, sparse)
     G = 1 if g == -1 else K // g
     q = torch.empty((K, N), dtype=torch.uint8, device=wp.device)
     s = torch.empty((G, N), dtype=torch.float16, device=wp.device)
@@ -60,20 +66,42 @@ class Workspace:
     """A zero-filled device workspace, grown on demand (never shrunk).
 
     One workspace serves any number of GEMMs issued in order on one stream;
-    each call leaves the counters at zero.
+    each call leaves the counters at zero.  When a call needs more, a larger
+    buffer (at least twice the old size) replaces it, and the superseded
+    buffers are kept alive for the life of the Workspace: a HIP graph
+    captured earlier still holds their addresses, and its replays keep using
+    them safely.
     """
 
     def __init__(self, device=None, nbytes: int = 0):
         self.device = torch.device(device or "cuda")
         self.buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        self._retired: list = []
 
     def ensure(self, nbytes: int) -> torch.Tensor:
         if self.buf.numel() < nbytes:
-            self.buf = torch.zeros(nbytes, dtype=torch.uint8, device=self.device)
+            self._retired.append(self.buf)
+            self.buf = torch.zeros(max(nbytes, 2 * self.buf.numel()), dtype=torch.uint8, device=self.device)
         return self.buf
 
 
 _default_ws: dict = {}
+
+
+def _check_packed(func: str, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, g: int, sparse: bool) -> None:
+    """Packed weights and scales: device tensors of the byte counts K, N and
+    the group imply (a wrong size would make the kernels read past them)."""
+    wb = B.marlin_packed_sparse_weight_bytes(K, N) if sparse else B.marlin_packed_weight_bytes(K, N)
+    sb = B.marlin_packed_scale_bytes(K, N, g)
+    if wb == 0 or sb == 0:
+        raise B.MarlinError(func, 2)
+    if not (wp.is_cuda and sp.is_cuda):
+        raise ValueError("%s: packed weights and scales must be device tensors" % func)
+    if not (wp.is_contiguous() and sp.is_contiguous()):
+        raise ValueError("%s: packed weights and scales must be contiguous" % func)
+    if wp.numel() * wp.element_size() != wb or sp.numel() * sp.element_size() != sb:
+        raise ValueError("%s: packed sizes %d / %d bytes, expected %d / %d for K=%d N=%d"
+                         % (func, wp.numel() * wp.element_size(), sp.numel() * sp.element_size(), wb, sb, K, N))
 
 
 def gemm(A: torch.Tensor, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, group=128,
@@ -83,13 +111,21 @@ def gemm(A: torch.Tensor, wp: torch.Tensor, sp: torch.Tensor, K: int, N: int, gr
     ``sparse=True``: W packed by ``pack(..., sparse=True)``."""
     if A.dtype != torch.float16 or not A.is_cuda:
         raise TypeError("gemm: A must be a float16 device tensor")
+    if A.dim() != 2:
+        raise ValueError("gemm: A must be [M, K]")
     A = A.contiguous()
     M = A.shape[0]
     if A.shape[1] != K:
         raise ValueError("gemm: A has %d columns, expected K=%d" % (A.shape[1], K))
     g = _group(K, group)
+    _check_packed("gemm", wp, sp, K, N, g, sparse)
+    if wp.device != A.device or sp.device != A.device:
+        raise ValueError("gemm: A and the packed weights must be on one device")
     if out is None:
         out = torch.empty((M, N), dtype=torch.float16, device=A.device)
+    elif (tuple(out.shape) != (M, N) or out.dtype != torch.float16 or out.device != A.device
+          or not out.is_contiguous()):
+        raise ValueError("gemm: out must be a contiguous float16 [%d, %d] tensor on %s" % (M, N, A.device))
     need = B.marlin_workspace_bytes(M, N, K, g)
     if workspace is None:
         key = (A.device, torch.cuda.current_stream(A.device).cuda_stream)

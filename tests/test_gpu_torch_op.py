@@ -111,6 +111,55 @@ def test_linear_in_a_captured_graph(mk):
         del junk
 
 
+def test_graph_replay_after_the_workspace_grows(mk):
+    # A graph captured at a small M holds the per-stream workspace's address.
+    # A larger eager call on the same stream then needs a larger workspace
+    # (8192 x 28672: about 3 MB at M = 1, 66 MB at M = 65); the old buffer
+    # must stay alive, so the graph's replays still give the eager bits.
+    K, N, g = 8192, 28672, 128
+    q, s = synth.weights(3, K, N, g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    x1 = dev(synth.activations(36, 1, K))
+    x65 = dev(synth.activations(36, 65, K))
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        want = mk.gemm(x1, wp, sp, K, N, group=g).clone()  # creates the stream's workspace
+        st.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=st):
+            y = mk.gemm(x1, wp, sp, K, N, group=g)
+        big = mk.gemm(x65, wp, sp, K, N, group=g)  # grows the workspace
+        st.synchronize()
+    for i in range(3):
+        with torch.cuda.stream(st):
+            gr.replay()
+            again = mk.gemm(x65, wp, sp, K, N, group=g)
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), want.view(torch.int16)), "replay %d" % i
+        assert torch.equal(again.view(torch.int16), big.view(torch.int16)), "eager after replay %d" % i
+
+
+def test_gemm_checks_its_tensors(mk):
+    K, N, g = 1024, 512, 128
+    q, s = synth.weights(5, K, N, g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    A = dev(synth.activations(5, 4, K))
+    with pytest.raises(ValueError):
+        mk.gemm(A, wp, sp, K, N, out=torch.empty((4, N - 64), dtype=torch.float16, device="cuda"))
+    with pytest.raises(ValueError):
+        mk.gemm(A, wp, sp, K, N, out=torch.empty((4, N), dtype=torch.float32, device="cuda"))
+    with pytest.raises(ValueError):
+        mk.gemm(A, wp, sp, K, N, out=torch.empty((N, 4), dtype=torch.float16, device="cuda").t())
+    with pytest.raises(ValueError):
+        mk.gemm(A, wp[:-16], sp, K, N)
+    with pytest.raises(ValueError):
+        mk.gemm(A, wp, sp, K, N, group=-1)  # scales sized for g = 128
+    with pytest.raises(ValueError):
+        mk.pack(dev(q), dev(s[:-1]), group=g)
+    with pytest.raises(ValueError):
+        mk.unpack(wp, sp[:-8], K, N, group=g)
+
+
 def _samples(M, N, count, seed):
     rng = np.random.default_rng(seed)
     return (np.concatenate([rng.integers(0, M, count), [0, M - 1, M - 1]]),

@@ -1,0 +1,108 @@
+"""The launch planner (csrc/plan.cpp) on the CPU, built alone with g++.
+
+* On any device of fewer compute units than the workspace was sized for, the
+  launch touches no more workspace than marlin_workspace_bytes reports: when
+  the device's preferred Stream-K split would need more (its kernel or tile
+  width differ from the 256-compute-unit choice), the planner takes the best
+  configuration that fits.
+* With a fixed 33 MiB area (the allocation-free entry point's) every shape
+  fits, and splits that fit are kept.
+* On a 256-compute-unit device the sized workspace always holds the
+  preferred configuration (no fallback).
+* Planning a repeated call (override read, workspace size, launch plan) is a
+  table lookup: well under a microsecond.
+"""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2408_11743_amd", "csrc")
+PROBE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "native", "plan_probe.cpp")
+
+SHAPES = [(4096, 4096, 1), (4096, 11008, 1), (11008, 4096, 0), (8192, 28672, 1), (28672, 8192, 1),
+          (1024, 768, 1), (8192, 1280, 1), (2048, 64, 0), (8192, 3584, 1)]
+MS = [1, 3, 8, 16, 17, 24, 32, 33, 64, 65, 97, 128, 200, 1000, 4096]
+SCRATCH = (1 << 20) + (32 << 20)
+
+
+@pytest.fixture(scope="module")
+def probe(tmp_path_factory):
+    out = str(tmp_path_factory.mktemp("plan") / "libplan_probe.so")
+    subprocess.run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-I", CSRC, "-o", out,
+                    os.path.join(CSRC, "plan.cpp"), PROBE], check=True)
+    lib = ctypes.CDLL(out)
+    lib.probe_plan.restype = ctypes.c_uint64
+    lib.probe_plan.argtypes = [ctypes.c_int] * 6 + [ctypes.c_uint64, ctypes.POINTER(ctypes.c_int)]
+    lib.probe_required.restype = ctypes.c_uint64
+    lib.probe_required.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.probe_plan_ns.restype = ctypes.c_double
+    lib.probe_plan_ns.argtypes = [ctypes.c_int]
+    return lib
+
+
+def plan(probe, M, N, K, gu, cus, sparse, ws):
+    out = (ctypes.c_int * 10)()
+    used = probe.probe_plan(M, N, K, gu, cus, sparse, ws, out)
+    return used, list(out)
+
+
+def test_required_size_matches_the_library(probe, monkeypatch):
+    monkeypatch.delenv("MARLIN_FORCE_CONFIG", raising=False)
+    import paper_2408_11743_amd as mk
+    for (K, N, gflag) in SHAPES:
+        gu = 1 if gflag else 0
+        g = 128 if gflag else -1
+        for M in MS + [5000, 12289]:
+            assert probe.probe_required(M, N, K, gu) == mk.marlin_workspace_bytes(M, N, K, g), (K, N, M)
+
+
+@pytest.mark.parametrize("K,N,gflag", SHAPES)
+def test_launch_fits_the_sized_workspace_on_any_cu_count(probe, K, N, gflag):
+    gu = 1 if gflag else 0
+    for M in MS:
+        ws = probe.probe_required(M, N, K, gu)
+        for cus in list(range(1, 65)) + list(range(65, 257, 7)) + [256]:
+            for sparse in (0, 1):
+                used, cfg = plan(probe, M, N, K, gu, cus, sparse, ws)
+                assert used <= ws, (K, N, M, cus, sparse, used, ws, cfg)
+                assert 1 <= cfg[4] <= max(cus, 1) * 2, cfg
+
+
+@pytest.mark.parametrize("K,N,gflag", SHAPES)
+def test_full_device_keeps_its_preferred_choice(probe, K, N, gflag):
+    gu = 1 if gflag else 0
+    for M in MS:
+        ws = probe.probe_required(M, N, K, gu)
+        for sparse in (0, 1):
+            _, sized = plan(probe, M, N, K, gu, 256, sparse, ws)
+            _, free = plan(probe, M, N, K, gu, 256, sparse, 1 << 62)
+            assert sized == free, (K, N, M, sparse)
+
+
+@pytest.mark.parametrize("K,N,gflag", SHAPES)
+def test_fixed_scratch_area_fits_every_shape(probe, K, N, gflag):
+    gu = 1 if gflag else 0
+    for M in MS:
+        for sparse in (0, 1):
+            used, cfg = plan(probe, M, N, K, gu, 256, sparse, SCRATCH)
+            assert used <= SCRATCH, (K, N, M, cfg)
+            pref_used, pref = plan(probe, M, N, K, gu, 256, sparse, 1 << 62)
+            if pref_used <= SCRATCH:
+                assert cfg == pref, (K, N, M, sparse)
+
+
+def test_a_device_with_fewer_cus_needed_the_fallback(probe):
+    # the case the fallback exists for: on 38 compute units, 4096 x 4096 at
+    # M = 97 prefers a split whose slots exceed the 256-compute-unit size
+    ws = probe.probe_required(97, 4096, 4096, 1)
+    used_free, _ = plan(probe, 97, 4096, 4096, 1, 38, 0, 1 << 62)
+    used, _ = plan(probe, 97, 4096, 4096, 1, 38, 0, ws)
+    assert used_free > ws >= used
+
+
+def test_planning_a_repeated_call_is_a_table_lookup(probe):
+    ns = probe.probe_plan_ns(20000)
+    assert ns < 1000.0, ns
