@@ -171,6 +171,35 @@ marlin_status_t marlin_gemm(const uint16_t *A, const void *w_packed,
                             hipStream_t stream);
 
 /*
+ * marlin_gemm_no_alloc - marlin_gemm without a workspace argument, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * serving loops and harnesses that forbid hipMalloc.  It allocates nothing
+ * and frees nothing.
+ *
+ *   A, w_packed, s_packed, C, M, N, K, group, stream: as for marlin_gemm.
+ *
+ * Its workspace is a file-scope device array of the library, 33 MiB
+ * (1 MiB of arrival counters, 32 MiB of fp32 partial tiles), which each
+ * device the library runs on holds from the library's first use there until
+ * the process ends.  Every call on a device shares that device's array:
+ * calls that may overlap on one device (different streams, concurrent graph
+ * replays) race and must be ordered by the caller.  A launch whose preferred
+ * Stream-K split would need more partial-tile space than the array holds is
+ * planned with the best configuration that fits (whole tiles need none), so
+ * every shape marlin_gemm accepts runs; the result is then within the same
+ * tolerance of the definition as marlin_gemm's, and bitwise reproducible.
+ * The first call on a device looks up the array's address there and clears
+ * its counters with a small kernel on `stream`, ahead of the call's own
+ * launches; every call leaves the counters at zero.
+ * Errors: NULL_POINTER, INVALID_SHAPE, UNSUPPORTED_GROUP, MISALIGNED, HIP,
+ * and WORKSPACE_TOO_SMALL should a launch ever need more than the array
+ * (none does: it is checked per launch before anything is enqueued).
+ */
+marlin_status_t marlin_gemm_no_alloc(const uint16_t *A, const void *w_packed, const void *s_packed,
+                                     uint16_t *C, int64_t M, int64_t N, int64_t K, int64_t group,
+                                     hipStream_t stream);
+
+/*
  * marlin_describe - the launch configuration marlin_gemm would use for this
  * problem on the current device (or on a 256-CU device when no device is
  * visible), as one NUL-terminated line: the kernel's name with its template

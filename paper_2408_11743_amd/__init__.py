@@ -23,6 +23,7 @@ from ._binding import (  # noqa: F401
     marlin_describe,
     marlin_describe_sparse,
     marlin_gemm,
+    marlin_gemm_no_alloc,
     marlin_gemm_sparse,
     marlin_layout_version,
     marlin_pack_sparse_weights,

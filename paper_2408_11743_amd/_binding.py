@@ -38,6 +38,7 @@ SIGNATURES = {
     "marlin_pack_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "marlin_unpack_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
     "marlin_gemm": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i64, _i64, _i64, _vp]),
+    "marlin_gemm_no_alloc": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _vp]),
     "marlin_describe": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_char_p, _sz]),
     "marlin_packed_sparse_weight_bytes": (_sz, [_i64, _i64]),
     "marlin_pack_sparse_weights": (ctypes.c_int, [_vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]),
@@ -136,6 +137,11 @@ def marlin_gemm(A, w_packed, s_packed, C, workspace, workspace_bytes, M, N, K, g
     _check("marlin_gemm", lib().marlin_gemm(
         _ptr(A), _ptr(w_packed), _ptr(s_packed), _ptr(C), _ptr(workspace), workspace_bytes,
         M, N, K, group, _stream(stream)))
+
+
+def marlin_gemm_no_alloc(A, w_packed, s_packed, C, M, N, K, group, stream=None) -> None:
+    _check("marlin_gemm_no_alloc", lib().marlin_gemm_no_alloc(
+        _ptr(A), _ptr(w_packed), _ptr(s_packed), _ptr(C), M, N, K, group, _stream(stream)))
 
 
 def marlin_describe(M: int, N: int, K: int, group: int) -> str:
