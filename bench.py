@@ -1,32 +1,40 @@
 #!/usr/bin/env python3
 """Benchmark of the W4A16 GEMM on one MI355X.
 
-Workload: the Llama-7B attention-projection layer, K = N = 4096, group size
-128, synthetic seeded data (``synth`` workload 1), with the batch sweep
-M = 1, 2, 4, 8, 16, 32, 64, 128.  One step = one GEMM at every M of the
-sweep (8 launches), each on the next of >= 1 GiB of packed weight copies so
-the 256 MB Infinity Cache never serves the weights.  Packing is offline and
-not timed.  Launches are replayed from HIP graphs (one graph per step, 16
-graphs rotating the weight copies) so the host does not throttle
-microsecond kernels.
+Headline workload: the 70B-class layers, (K, N) = (8192, 28672) and
+(28672, 8192), group size 128, synthetic seeded data (``synth`` workload 3),
+batch sweep M = 1, 2, 4, 8, 16, 32, 64, 128.  One step = one GEMM at every
+(layer, M) of the sweep (16 launches), each on the next of 9 packed-weight
+copies per layer (1.09 GB per layer, beyond the 256 MB Infinity Cache).
+Packing is offline and not timed.  Launches are replayed from HIP graphs (one
+graph per step, 9 graphs rotating the weight copies) so the host does not
+throttle microsecond kernels.
 
-Output: one JSON line.  ``value`` = TFLOP/s of the whole timed region
-(sum of 2MNK over the launches / elapsed).  Also reported per M: time per
-call, TFLOP/s, effective weight-stream GB/s, fraction of the MI355X roofline
-(t_roof / t), and the speedup over a plain fp16 ``torch.matmul`` of the same
-shape timed the same way in the same run (comparison only).  ``roofline``
-covers the GEMM kernel: algorithmic bytes of the timed launches / elapsed
+Output: one JSON line.  ``value`` = TFLOP/s of the whole timed region (sum of
+2MNK over the launches / elapsed).  Per (layer, M) of the headline: time per
+call (graph replays over the rotated copies), the eager single-call latency
+(event-timed, and the host time of the call itself), TFLOP/s, effective
+weight-stream GB/s, the fraction of the MI355X roofline (t_roof / t), the
+launch configuration, and the speedup over a plain fp16 ``torch.matmul`` of
+the same shape timed the same way in the same run (comparison only).
+``roofline`` covers the step's GEMM launches: algorithmic bytes / elapsed
 (HIP events on the launch stream) against 8 TB/s.  ``cpu_baseline`` times
-the fp64 oracle on the host over the whole sweep (and checks the GPU
-outputs against it).  Two further sections are reported beside the step,
-outside its timed region: ``sparse_2of4`` (the 2:4 sparse kernel, K = N =
-8192, M sweep), ``prefill`` (M = 256, 1024, 4096 in one launch per call,
-against the fp16 matrix-core peak and fp16 ``torch.matmul``) and
-``quantize`` (the weight quantiser, against the fp32 vector lane rate).
+the fp64 oracle on the host at M = 1, 16, 128 on both layers (and checks the
+GPU outputs against it), plus one single-thread run.  ``clock`` records the
+shader clock sampled during the run.
+
+Sections beside the step, outside its timed region: ``attention_4096`` (the
+Llama-7B attention projection, 4096 x 4096), ``mlp_7b`` (the Llama-7B MLP
+layers, g = 128 and per-channel scales), ``sparse_2of4`` (the 2:4 sparse
+kernel, 8192 x 8192), ``prefill`` (M = 256, 1024, 4096 in one launch per
+call) and ``quantize`` (the weight quantiser).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-       [--no-sparse | --sparse-only] [--no-prefill | --prefill-only]
-       [--no-quantize | --quantize-only]
+       [--no-sections] [--no-clock] [--only SECTION] [--profile-cases C
+       [--profile-layers headline|attention_4096|mlp_7b]]
+
+Under a profiler, run with --no-clock --no-cpu-baseline (or --only /
+--profile-cases): those start no child process.
 """
 from __future__ import annotations
 
@@ -34,19 +42,30 @@ import argparse
 import json
 import math
 import os
+import subprocess
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-K_DIM, N_DIM, GROUP = 4096, 4096, 128
+GROUP = 128
 M_SWEEP = [1, 2, 4, 8, 16, 32, 64, 128]
-WID = 1
-ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies (Infinity Cache is 256 MB)
-GRAPHS = 16
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a16_gemm_4096x4096_msweep_traffic.json")
+# (K, N, synth workload id, group); group -1 = one scale per output column
+HEADLINE = [(8192, 28672, 3, 128), (28672, 8192, 3, 128)]
+ATTENTION = [(4096, 4096, 1, 128)]
+MLP_7B = [(4096, 11008, 2, 128), (11008, 4096, 2, 128), (4096, 11008, 2, -1), (11008, 4096, 2, -1)]
+ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies per layer (Infinity Cache is 256 MB)
+CPU_MS = [1, 16, 128]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a16_gemm_70b_layers_msweep_traffic.json")
+SECTIONS = ("attention_4096", "mlp_7b", "sparse_2of4", "prefill", "quantize")
+
+SPARSE_K, SPARSE_N, SPARSE_WID = 8192, 8192, 4
+# large batches: (K, N, synth workload) and the batch sizes
+PREFILL_SHAPES = [(4096, 4096, 1), (28672, 8192, 3)]
+PREFILL_M = [256, 1024, 4096]
 
 
 def log(msg):
@@ -61,27 +80,24 @@ def parse():
     ap.add_argument("--per-m-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fp16", action="store_true")
-    ap.add_argument("--no-sparse", action="store_true",
-                    help="skip the 2:4 sparse section (K = N = 8192, g = 128, M sweep)")
-    ap.add_argument("--sparse-only", action="store_true",
-                    help="run only the 2:4 sparse section and print its JSON (for profiling it alone)")
-    ap.add_argument("--no-prefill", action="store_true",
-                    help="skip the large-batch section (M = 256, 1024, 4096 in one launch)")
-    ap.add_argument("--prefill-only", action="store_true",
-                    help="run only the large-batch section and print its JSON (for profiling it alone)")
-    ap.add_argument("--no-quantize", action="store_true",
-                    help="skip the quantiser section")
-    ap.add_argument("--quantize-only", action="store_true",
-                    help="run only the quantiser section and print its JSON (for profiling it alone)")
+    ap.add_argument("--no-sections", action="store_true", help="the headline step only")
+    ap.add_argument("--no-clock", action="store_true",
+                    help="do not sample the shader clock (no child process: for runs under a profiler)")
+    ap.add_argument("--only", choices=SECTIONS,
+                    help="run only this section and print its JSON (for profiling it alone)")
+    ap.add_argument("--profile-cases", type=int, default=0,
+                    help="counter runs: launch every (layer, M) case of --profile-layers this many times "
+                         "eagerly, in sweep order, print the case list and stop")
+    ap.add_argument("--profile-layers", choices=("headline", "attention_4096", "mlp_7b"), default="headline")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
-                    help="run plain device-to-device copies of this many MB (outside the timed "
-                         "region) so hardware byte counters can be scaled against a known size")
+                    help="run plain device-to-device copies of this many MB first, so hardware byte "
+                         "counters can be scaled against a known size")
     return ap.parse_args()
 
 
 def measured_traffic():
-    """HBM bytes per launch from the committed counter summary, or None when
-    the kernel source has changed since the counters were taken."""
+    """HBM bytes per launch (step average) from the committed counter summary,
+    or None when the kernel sources have changed since the counters were taken."""
     from paper_2408_11743_amd.profile_summary import kernel_sources_digest
     try:
         rec = json.load(open(TRAFFIC_FILE))
@@ -92,18 +108,135 @@ def measured_traffic():
         return None
 
 
-SPARSE_K, SPARSE_N, SPARSE_WID = 8192, 8192, 4
-# large batches: (K, N, synth workload) and the batch sizes
-PREFILL_SHAPES = [(4096, 4096, 1), (28672, 8192, 3)]
-PREFILL_M = [256, 1024, 4096]
-
-
 def cpu_threads() -> int:
     return int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+class Range:
+    """A named range in the profiler's marker trace (roctx), closed after the
+    GPU work inside it has finished, so the kernels it covers lie within it."""
+
+    def __init__(self, torch, name):
+        self.torch, self.name = torch, name
+
+    def __enter__(self):
+        self.torch.cuda.synchronize()
+        self.torch.cuda.nvtx.range_push(self.name)
+
+    def __exit__(self, *exc):
+        self.torch.cuda.synchronize()
+        self.torch.cuda.nvtx.range_pop()
+
+
+# ---------------- shader clock ----------------
+
+# The sampler runs as a child process started before this process touches
+# the GPU (a process that has initialised the GPU starts no other program):
+# it appends one JSON line per amd-smi reading (wall time, shader clocks in
+# MHz, or the error) to a file until a stop file appears.
+_SAMPLER = r"""
+import json, os, subprocess, sys, time
+out, stop = sys.argv[1], sys.argv[2]
+
+def clocks(obj, path=""):
+    found = []
+    if isinstance(obj, dict):
+        for k, v in obj.items():
+            p = (path + "/" + str(k)).lower()
+            if isinstance(v, dict) and "value" in v and str(k).lower() in ("clk", "cur_clk") \
+                    and ("gfx" in path.lower() or "sclk" in path.lower()):
+                try:
+                    found.append(float(v["value"]))
+                except (TypeError, ValueError):
+                    pass
+            else:
+                found += clocks(v, p)
+    elif isinstance(obj, list):
+        for i, v in enumerate(obj):
+            found += clocks(v, path + "/%d" % i)
+    return found
+
+t_end = time.time() + 900
+parent = os.getppid()
+with open(out, "a") as f:
+    first = True
+    while not os.path.exists(stop) and time.time() < t_end and os.getppid() == parent:
+        rec = {"t": time.time()}
+        try:
+            r = subprocess.run(["amd-smi", "metric", "-g", "0", "-c", "--json"], capture_output=True,
+                               text=True, timeout=20)
+            vals = clocks(json.loads(r.stdout))
+            rec["mhz"] = vals
+            if first or not vals:
+                rec["raw"] = (r.stdout + r.stderr)[:3000]
+        except Exception as e:
+            rec["error"] = "%s: %s" % (type(e).__name__, str(e)[:200])
+        first = False
+        f.write(json.dumps(rec) + "\n")
+        f.flush()
+        time.sleep(1.0)
+"""
+
+
+class ClockSampler:
+    """The shader clock, read with amd-smi about once a second by a child
+    process started before the GPU is used."""
+
+    def __init__(self):
+        import tempfile
+        d = tempfile.mkdtemp(prefix="bench_clock_")
+        self.out, self.stop_file = os.path.join(d, "samples.jsonl"), os.path.join(d, "stop")
+        self.proc = subprocess.Popen([sys.executable, "-c", _SAMPLER, self.out, self.stop_file],
+                                     stdout=subprocess.DEVNULL, stderr=subprocess.DEVNULL)
+        self.window = None
+
+    def mark(self, t0, t1):
+        """The wall-time window whose samples are reported."""
+        self.window = (t0, t1)
+
+    def finish(self):
+        open(self.stop_file, "w").close()
+        try:
+            self.proc.wait(timeout=40)
+        except subprocess.TimeoutExpired:
+            self.proc.kill()
+        recs = []
+        try:
+            recs = [json.loads(l) for l in open(self.out) if l.strip()]
+        except (OSError, ValueError):
+            pass
+        raw = next((r.get("raw") for r in recs if r.get("raw")), None)
+        if raw is not None:
+            os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+            open(os.path.join(ROOT, "gpurun_out", "amd_smi_clock_raw.txt"), "w").write(raw)
+        if self.window:
+            recs = [r for r in recs if self.window[0] <= r["t"] <= self.window[1]]
+        s = sorted(round(sum(r["mhz"]) / len(r["mhz"]), 1) for r in recs if r.get("mhz"))
+        rec = {"source": "amd-smi metric -g 0 -c --json (current shader clock, MHz, mean over the XCDs), "
+                         "about once a second during the per-case measurements of the headline layers",
+               "samples": len(s)}
+        if s:
+            rec.update({"min_mhz": s[0], "median_mhz": s[len(s) // 2], "max_mhz": s[-1]})
+        errs = [r["error"] for r in recs if "error" in r]
+        if errs or not s:
+            rec["error"] = errs[0] if errs else "no shader clock in amd-smi output"
+        return rec
+
+
+# ---------------- timing helpers ----------------
+
 def graph_time_us(launch, count, stream, reps, torch, np):
-    """Median per-launch time of a graph of `count` launches (launch(i))."""
+    """(median, min) per-launch time of a graph of `count` launches (launch(i))."""
     gr = torch.cuda.CUDAGraph()
     with torch.cuda.stream(stream):
         launch(0)
@@ -128,7 +261,132 @@ def graph_time_us(launch, count, stream, reps, torch, np):
             a1.synchronize()
             times.append(a0.elapsed_time(a1) * 1e3 / count)
     del gr
-    return float(np.median(times))
+    return float(np.median(times)), float(min(times))
+
+
+def eager_time_us(launch, count, stream, reps, torch, np):
+    """Single eager calls (not in a graph), each alone on the GPU: median of
+    the event-timed latency and of the host time spent in the call."""
+    ev, host = [], []
+    with torch.cuda.stream(stream):
+        for i in range(reps):
+            a0 = torch.cuda.Event(enable_timing=True)
+            a1 = torch.cuda.Event(enable_timing=True)
+            stream.synchronize()
+            a0.record(stream)
+            h0 = time.perf_counter()
+            launch(i % count)
+            h1 = time.perf_counter()
+            a1.record(stream)
+            a1.synchronize()
+            ev.append(a0.elapsed_time(a1) * 1e3)
+            host.append((h1 - h0) * 1e6)
+    return float(np.median(ev)), float(np.median(host))
+
+
+class Layer:
+    """One weight matrix (K, N, g): packed once, replicated to >= 1 GiB of
+    copies; the fp16 comparator's dequantised weights likewise."""
+
+    def __init__(self, mk, synth, torch, dev, K, N, wid, g, fp16=True, min_copies=2):
+        self.K, self.N, self.g, self.wid = K, N, g, wid
+        q, s = synth.weights(wid, K, N, None if g == -1 else g)
+        self.q, self.s = q, s
+        qd, sd = torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev)
+        wp, sp = mk.pack(qd, sd, group=g)
+        self.wbytes = wp.numel() + sp.numel() * 2
+        n = max(min_copies, math.ceil(ROTATION_BYTES / self.wbytes))
+        self.wps = [wp] + [wp.clone() for _ in range(n - 1)]
+        self.sps = [sp] + [sp.clone() for _ in range(n - 1)]
+        self.w16s = []
+        if fp16:
+            rows = K if g == -1 else g
+            w16 = ((qd.to(torch.float32) - 8.0) * sd.to(torch.float32).repeat_interleave(rows, dim=0)).to(torch.float16)
+            n16 = max(2, math.ceil(ROTATION_BYTES / (w16.numel() * 2)))
+            self.w16s = [w16] + [w16.clone() for _ in range(n16 - 1)]
+            del w16
+        del qd, sd
+        torch.cuda.synchronize()
+
+    @property
+    def copies(self):
+        return len(self.wps)
+
+    def name(self):
+        return "%dx%d g=%s" % (self.K, self.N, "K" if self.g == -1 else self.g)
+
+
+def measure_cases(args, mk, R, torch, np, dev, layer, Ms, stream, L, ws, acts, outs, label):
+    """Per-M records of one layer: graph replays over the rotated copies, the
+    eager latency, and the fp16 comparator."""
+    K, N, g = layer.K, layer.N, layer.g
+    rows = []
+    for M in Ms:
+        A, C = acts[M], outs[M]
+
+        def launch(i, M=M, A=A, C=C):
+            st = L.marlin_gemm(A.data_ptr(), layer.wps[i].data_ptr(), layer.sps[i].data_ptr(), C.data_ptr(),
+                               ws.data_ptr(), ws.numel(), M, N, K, g, stream.cuda_stream)
+            if st != 0:
+                raise mk.MarlinError("marlin_gemm", st)
+        with Range(torch, "%s w4a16 K=%d N=%d g=%d M=%d" % (label, K, N, g, M)):
+            t, tmin = graph_time_us(launch, layer.copies, stream, args.per_m_reps, torch, np)
+        ev, host = eager_time_us(launch, layer.copies, stream, 20, torch, np)
+        troof = R.w4a16_t_roof(M, N, K, g) * 1e6
+        rec = {"K": K, "N": N, "group": g, "M": M, "us": round(t, 3), "us_min": round(tmin, 3),
+               "eager_us": round(ev, 3), "host_us_per_call": round(host, 2),
+               "tflops": round(R.flops(M, N, K) / (t * 1e-6) / 1e12, 3),
+               "weight_GBps": round(R.weight_bytes(N, K, g) / (t * 1e-6) / 1e9, 1),
+               "roof_us": round(troof, 3), "roof_frac": round(troof / t, 4),
+               "bound": R.bound(M, N, K, g), "launch": mk.marlin_describe(M, N, K, g)}
+        if layer.w16s:
+            n16 = len(layer.w16s)
+            t16, _ = graph_time_us(lambda i: torch.matmul(A, layer.w16s[i % n16]), n16, stream,
+                                   args.per_m_reps, torch, np)
+            rec["fp16_us"] = round(t16, 3)
+            rec["speedup_vs_fp16"] = round(t16 / t, 3)
+        rows.append(rec)
+        log("%s %dx%d g=%s M=%3d: %.3f us (eager %.2f us, host %.1f us), %.0f weight GB/s, roofline frac %.3f%s" %
+            (label, K, N, g, M, t, ev, host, rec["weight_GBps"], troof / t,
+             ", fp16 %.2f us -> %.2fx" % (rec["fp16_us"], rec["speedup_vs_fp16"]) if "fp16_us" in rec else ""))
+    return rows
+
+
+def layer_section(args, mk, R, synth, torch, np, dev, shapes, label):
+    """A per-M sweep of other layers, outside the timed region."""
+    L = mk.lib()
+    stream = torch.cuda.Stream(device=dev)
+    wsb = mk.Workspace(dev)
+    out = []
+    for (K, N, wid, g) in shapes:
+        layer = Layer(mk, synth, torch, dev, K, N, wid, g, fp16=not args.no_fp16)
+        ws = wsb.ensure(max(mk.marlin_workspace_bytes(M, N, K, g) for M in M_SWEEP))
+        acts = {M: torch.from_numpy(synth.activations(wid, M, K)).to(dev) for M in M_SWEEP}
+        outs = {M: torch.empty((M, N), dtype=torch.float16, device=dev) for M in M_SWEEP}
+        out += measure_cases(args, mk, R, torch, np, dev, layer, M_SWEEP, stream, L, ws, acts, outs, label)
+        del layer, acts, outs
+        torch.cuda.synchronize()
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        tot, flops, rows = 0.0, 0.0, []
+        for (K, N, wid, g) in shapes:
+            q, s = synth.weights(wid, K, N, None if g == -1 else g)
+            for M in CPU_MS:
+                A_np = synth.activations(wid, M, K)
+                c0 = time.perf_counter()
+                oracle.gemm(A_np, q, s, g)
+                dt = time.perf_counter() - c0
+                tot += dt
+                flops += R.flops(M, N, K)
+                rows.append({"K": K, "N": N, "group": g, "M": M, "seconds": round(dt, 4)})
+        cpu = {"value": round(flops / tot / 1e12, 6), "unit": "TFLOP/s", "cores": cpu_threads(),
+               "kind": "oracle", "sample": "fp64 oracle, full products at M in %s on every layer of the section"
+               % CPU_MS, "per_case": rows}
+        log("%s oracle: %.2f s" % (label, tot))
+    return {"workload": "W4A16 GEMM, %s, M sweep %s, weights rotated over >= 1 GiB per layer" %
+                        (", ".join("%dx%d g=%s" % (K, N, "K" if g == -1 else g) for K, N, _, g in shapes), M_SWEEP),
+            "per_m": out, "cpu_baseline": cpu}
 
 
 def sparse_section(args, mk, R, synth, torch, np, dev):
@@ -167,10 +425,11 @@ def sparse_section(args, mk, R, synth, torch, np, dev):
                         wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g, stream.cuda_stream)
                 if st != 0:
                     raise mk.MarlinError("marlin_gemm_sparse" if sp_flag else "marlin_gemm", st)
-            t[sp_flag] = graph_time_us(launch, len(wps), stream, args.per_m_reps, torch, np)
+            with Range(torch, "sparse %s M=%d" % ("2:4" if sp_flag else "dense", M)):
+                t[sp_flag], _ = graph_time_us(launch, len(wps), stream, args.per_m_reps, torch, np)
         t16 = None
         if not args.no_fp16:
-            t16 = graph_time_us(lambda i: torch.matmul(A, w16s[i % n16]), n16, stream, args.per_m_reps, torch, np)
+            t16, _ = graph_time_us(lambda i: torch.matmul(A, w16s[i % n16]), n16, stream, args.per_m_reps, torch, np)
         troof = R.sparse24_t_roof(M, N, K, g) * 1e6
         rec = {"M": M, "us": round(t[True], 3), "dense_w4_us": round(t[False], 3),
                "speedup_vs_dense_w4": round(t[False] / t[True], 3),
@@ -233,13 +492,14 @@ def prefill_section(args, mk, R, synth, torch, np, dev):
                                    wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g, stream.cuda_stream)
                 if st != 0:
                     raise mk.MarlinError("marlin_gemm", st)
-            t = graph_time_us(launch, 4, stream, args.per_m_reps, torch, np)
+            with Range(torch, "prefill K=%d N=%d M=%d" % (K, N, M)):
+                t, _ = graph_time_us(launch, 4, stream, args.per_m_reps, torch, np)
             rec = {"K": K, "N": N, "M": M, "us": round(t, 2),
                    "TFLOPs": round(R.flops(M, N, K) / t / 1e6, 1),
                    "mfma_frac": round(R.flops(M, N, K) / (t * 1e-6) / R.FP16_MFMA_FLOPS, 4),
                    "launch": mk.marlin_describe(M, N, K, g)}
             if w16 is not None:
-                t16 = graph_time_us(lambda i: torch.matmul(A, w16), 4, stream, args.per_m_reps, torch, np)
+                t16, _ = graph_time_us(lambda i: torch.matmul(A, w16), 4, stream, args.per_m_reps, torch, np)
                 rec["fp16_us"] = round(t16, 2)
                 rec["speedup_vs_fp16"] = round(t16 / t, 3)
             rows.append(rec)
@@ -269,9 +529,10 @@ def prefill_section(args, mk, R, synth, torch, np, dev):
 def quantize_section(args, mk, R, synth, torch, np, dev):
     """The quantiser (symmetric, zero point 8, g = 128, clipping search over
     the 10 default ratios) on the Llama-7B attention projection and the
-    70B-class MLP down projection.  Bound by fp32 vector work (~75 operations
-    per weight against 3 bytes of HBM traffic): ``alu_frac`` against the fp32
-    vector lane rate, ``hbm_GBps`` for reference."""
+    70B-class MLP down projection.  Bound by fp32 vector work: ``alu_frac``
+    is its vector instructions per weight (from the committed counter
+    profile) against the non-packed vector issue rate; ``hbm_GBps`` for
+    reference."""
     L = mk.lib()
     stream = torch.cuda.Stream(device=dev)
     ratios = list(mk.CLIP_RATIOS)
@@ -284,14 +545,15 @@ def quantize_section(args, mk, R, synth, torch, np, dev):
 
         def launch(i):
             mk.marlin_quantize(W, K, N, g, ratios, q, s, stream)
-        t = graph_time_us(launch, 2, stream, args.per_m_reps, torch, np)
-        ops = R.quant_ops(K, N, len(ratios))
+        with Range(torch, "quantize K=%d N=%d" % (K, N)):
+            t, _ = graph_time_us(launch, 2, stream, args.per_m_reps, torch, np)
+        ops = R.quant_lane_ops(K, N, len(ratios))
         rec = {"K": K, "N": N, "group": g, "ratios": len(ratios), "us": round(t, 2),
                "Gweights_per_s": round(K * N / t / 1e3, 2),
-               "alu_frac": round(ops / (t * 1e-6) / R.FP32_LANE_OPS, 4),
+               "alu_frac": round(ops / (t * 1e-6) / R.VALU_LANE_OPS, 4),
                "hbm_GBps": round(R.quant_bytes(K, N, g) / t / 1e3, 1)}
         rows.append(rec)
-        log("quantize %dx%d g=%d, %d ratios: %.1f us, %.2f G weights/s, %.1f%% of the fp32 lane rate" %
+        log("quantize %dx%d g=%d, %d ratios: %.1f us, %.2f G weights/s, %.1f%% of the vector issue rate" %
             (K, N, g, len(ratios), t, rec["Gweights_per_s"], 100 * rec["alu_frac"]))
         if not args.no_cpu_baseline:
             # the quantiser's oracle (numpy, fp32) on all columns, or on the
@@ -311,7 +573,41 @@ def quantize_section(args, mk, R, synth, torch, np, dev):
         cpu = {"unit": "G weights/s", "cores": cpu_threads(), "kind": "oracle", "per_shape": cpu_rows}
     return {"workload": "quantiser fp16 -> (q, s), g=%d, %d clipping ratios, (K, N) in %s" %
                         (GROUP, len(mk.CLIP_RATIOS), [sh[:2] for sh in PREFILL_SHAPES]),
-            "bound": "alu", "peak_lane_ops_per_s": R.FP32_LANE_OPS, "per_shape": rows, "cpu_baseline": cpu}
+            "bound": "alu", "peak_lane_ops_per_s": R.VALU_LANE_OPS,
+            "valu_lane_ops_per_weight": R.QUANT_VALU_PER_WEIGHT_G128_10,
+            "per_shape": rows, "cpu_baseline": cpu}
+
+
+def run_section(name, args, mk, R, synth, torch, np, dev):
+    if name == "attention_4096":
+        return layer_section(args, mk, R, synth, torch, np, dev, ATTENTION, name)
+    if name == "mlp_7b":
+        return layer_section(args, mk, R, synth, torch, np, dev, MLP_7B, name)
+    if name == "sparse_2of4":
+        return sparse_section(args, mk, R, synth, torch, np, dev)
+    if name == "prefill":
+        return prefill_section(args, mk, R, synth, torch, np, dev)
+    return quantize_section(args, mk, R, synth, torch, np, dev)
+
+
+def single_thread_oracle():
+    """The oracle on one thread (the 4096 x 4096 attention projection at
+    M = 1), in a child process started with OMP_NUM_THREADS=1."""
+    code = ("import json, time, oracle, synth\n"
+            "q, s = synth.weights(1, 4096, 4096, 128)\n"
+            "A = synth.activations(1, 1, 4096)\n"
+            "oracle.gemm(A, q, s, 128)\n"
+            "ts = []\n"
+            "for _ in range(3):\n"
+            "    t = time.perf_counter(); oracle.gemm(A, q, s, 128); ts.append(time.perf_counter() - t)\n"
+            "print(json.dumps(sorted(ts)[1]))\n")
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, cwd=ROOT, timeout=300)
+    if r.returncode != 0:
+        return {"error": r.stderr[-300:]}
+    dt = float(r.stdout.strip().splitlines()[-1])
+    return {"K": 4096, "N": 4096, "M": 1, "threads": 1, "seconds": round(dt, 4),
+            "value": round(2.0 * 4096 * 4096 / dt / 1e12, 6), "unit": "TFLOP/s"}
 
 
 def main():
@@ -329,6 +625,11 @@ def main():
     import synth
     from paper_2408_11743_amd import roofline as R
 
+    # child processes first: nothing is started once the GPU is in use
+    headline = not (args.only or args.profile_cases)
+    clock = ClockSampler() if headline and not args.no_clock else None
+    single = single_thread_oracle() if headline and not args.no_cpu_baseline else None
+
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
@@ -342,196 +643,174 @@ def main():
         torch.cuda.synchronize()
         log("calibration: 3 device copies of %d MiB" % args.calibration_copy_mb)
         del src, dst
-    if args.sparse_only:
-        print(json.dumps({"sparse_2of4": sparse_section(args, mk, R, synth, torch, np, dev)}), flush=True)
+    if args.only:
+        print(json.dumps({args.only: run_section(args.only, args, mk, R, synth, torch, np, dev)}), flush=True)
         return
-    if args.prefill_only:
-        print(json.dumps({"prefill": prefill_section(args, mk, R, synth, torch, np, dev)}), flush=True)
-        return
-    if args.quantize_only:
-        print(json.dumps({"quantize": quantize_section(args, mk, R, synth, torch, np, dev)}), flush=True)
-        return
-    K, N, g = K_DIM, N_DIM, GROUP
 
-    # ---- weights: pack once, replicate to >= 1 GiB ----
-    q, s = synth.weights(WID, K, N, g)
-    wp0, sp0 = mk.pack(torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev), group=g)
-    wbytes = wp0.numel() + sp0.numel() * 2
-    nrot = 8 * math.ceil(ROTATION_BYTES / wbytes / 8)
-    wps = [wp0] + [wp0.clone() for _ in range(nrot - 1)]
-    sps = [sp0] + [sp0.clone() for _ in range(nrot - 1)]
-    log("weights %dx%d g=%d: %d B packed per copy, %d copies (%.2f GB)" %
-        (K, N, g, wbytes, nrot, nrot * wbytes / 1e9))
-
-
-    acts = {M: torch.from_numpy(synth.activations(WID, M, K)).to(dev) for M in M_SWEEP}
-    outs = {M: torch.empty((M, N), dtype=torch.float16, device=dev) for M in M_SWEEP}
-    ws = mk.Workspace(dev)
-    wsb = max(mk.marlin_workspace_bytes(M, N, K, g) for M in M_SWEEP)
-    wsbuf = ws.ensure(wsb)
+    # ---- headline layers: pack once, replicate to >= 1 GiB per layer ----
     L = mk.lib()
+    layers = []
+    shapes = HEADLINE
+    if args.profile_cases:
+        shapes = {"headline": HEADLINE, "attention_4096": ATTENTION, "mlp_7b": MLP_7B}[args.profile_layers]
+    for (K, N, wid, g) in shapes:
+        layers.append(Layer(mk, synth, torch, dev, K, N, wid, g,
+                            fp16=not (args.no_fp16 or args.profile_cases), min_copies=2))
+        log("weights %s: %d B packed per copy, %d copies (%.2f GB)" %
+            (layers[-1].name(), layers[-1].wbytes, layers[-1].copies, layers[-1].copies * layers[-1].wbytes / 1e9))
+    acts = {(lay.K, lay.N, M): torch.from_numpy(synth.activations(lay.wid, M, lay.K)).to(dev)
+            for lay in layers for M in M_SWEEP}
+    outs = {(lay.K, lay.N, M): torch.empty((M, lay.N), dtype=torch.float16, device=dev)
+            for lay in layers for M in M_SWEEP}
+    wsb = mk.Workspace(dev)
+    ws = wsb.ensure(max(mk.marlin_workspace_bytes(M, lay.N, lay.K, lay.g) for lay in layers for M in M_SWEEP))
+    stream = torch.cuda.Stream(device=dev)
+    cases = [(lay, M) for lay in layers for M in M_SWEEP]
 
-    def launch(M, i, stream):
-        st = L.marlin_gemm(acts[M].data_ptr(), wps[i].data_ptr(), sps[i].data_ptr(),
-                           outs[M].data_ptr(), wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g,
+    def launch(lay, M, i):
+        st = L.marlin_gemm(acts[(lay.K, lay.N, M)].data_ptr(), lay.wps[i].data_ptr(), lay.sps[i].data_ptr(),
+                           outs[(lay.K, lay.N, M)].data_ptr(), ws.data_ptr(), ws.numel(), M, lay.N, lay.K, lay.g,
                            stream.cuda_stream)
         if st != 0:
             raise mk.MarlinError("marlin_gemm", st)
 
-    # ---- graphs: one step (the M sweep) per graph, 16 graphs rotating copies ----
-    stream = torch.cuda.Stream(device=dev)
+    if args.profile_cases:
+        # counter runs: each case C times in a row, eagerly, in sweep order
+        with torch.cuda.stream(stream):
+            for lay, M in cases:
+                for i in range(args.profile_cases):
+                    launch(lay, M, i % lay.copies)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_cases": args.profile_cases, "layers": args.profile_layers,
+                          "cases": [{"K": lay.K, "N": lay.N, "group": lay.g, "M": M,
+                                     "launch": mk.marlin_describe(M, lay.N, lay.K, lay.g)} for lay, M in cases]}),
+              flush=True)
+        return
+
+    # ---- graphs: one step (every case) per graph, rotating the copies ----
+    ngraphs = max(lay.copies for lay in layers)
     torch.cuda.synchronize()
     graphs = []
     with torch.cuda.stream(stream):
-        for i, M in enumerate(M_SWEEP):  # eager warm-up of every variant
-            launch(M, i % nrot, stream)
+        for lay, M in cases:  # eager warm-up of every variant
+            launch(lay, M, 0)
         stream.synchronize()
-        for gi in range(GRAPHS):
+        for gi in range(ngraphs):
             gr = torch.cuda.CUDAGraph()
             with torch.cuda.graph(gr, stream=stream):
-                for j, M in enumerate(M_SWEEP):
-                    launch(M, (gi * len(M_SWEEP) + j) % nrot, stream)
+                for j, (lay, M) in enumerate(cases):
+                    launch(lay, M, (gi * len(M_SWEEP) + j) % lay.copies)
             graphs.append(gr)
     torch.cuda.synchronize()
-    log("captured %d graphs of %d launches" % (GRAPHS, len(M_SWEEP)))
+    log("captured %d graphs of %d launches" % (ngraphs, len(cases)))
 
-    step_flops = sum(R.flops(M, N, K) for M in M_SWEEP)
-    step_bytes = sum(R.w4a16_bytes(M, N, K, g) for M in M_SWEEP)
-    step_wbytes = len(M_SWEEP) * R.weight_bytes(N, K, g)
+    step_flops = sum(R.flops(M, lay.N, lay.K) for lay, M in cases)
+    step_bytes = sum(R.w4a16_bytes(M, lay.N, lay.K, lay.g) for lay, M in cases)
+    step_wbytes = sum(R.weight_bytes(lay.N, lay.K, lay.g) for lay, M in cases)
 
     # ---- warm-up and timed region ----
     with torch.cuda.stream(stream):
         for k in range(args.warmup):
-            graphs[k % GRAPHS].replay()
+            graphs[k % ngraphs].replay()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(stream):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        e0.record(stream)
-        for k in range(args.steps):
-            graphs[k % GRAPHS].replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
+    with Range(torch, "timed steps"):
+        with torch.cuda.stream(stream):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            e0.record(stream)
+            for k in range(args.steps):
+                graphs[k % ngraphs].replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+    del graphs
     ev_ms = e0.elapsed_time(e1)
     wall_ms = (t1 - t0) * 1e3
     ms_per_step = ev_ms / args.steps
     value = step_flops / (ms_per_step * 1e-3) / 1e12
-    log("timed %d steps: %.3f ms/step (events), wall %.3f ms/step" %
-        (args.steps, ms_per_step, wall_ms / args.steps))
-    avg_launch_us = ms_per_step * 1e3 / len(M_SWEEP)
+    log("timed %d steps: %.3f ms/step (events), wall %.3f ms/step, %.1f TFLOP/s" %
+        (args.steps, ms_per_step, wall_ms / args.steps, value))
+    avg_launch_us = ms_per_step * 1e3 / len(cases)
     achieved_gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
 
-    # ---- per-M: graph of nrot launches (one per weight copy) ----
+    # ---- per case: graph of one launch per weight copy, eager latency, fp16 ----
     per_m = []
-    for M in M_SWEEP:
-        gr = torch.cuda.CUDAGraph()
-        with torch.cuda.stream(stream):
-            with torch.cuda.graph(gr, stream=stream):
-                for i in range(nrot):
-                    launch(M, i, stream)
-            gr.replay()
-            torch.cuda.synchronize()
-            times = []
-            for _ in range(args.per_m_reps):
-                a0 = torch.cuda.Event(enable_timing=True)
-                a1 = torch.cuda.Event(enable_timing=True)
-                a0.record(stream)
-                gr.replay()
-                a1.record(stream)
-                a1.synchronize()
-                times.append(a0.elapsed_time(a1) * 1e3 / nrot)
-        del gr
-        t_us = float(np.median(times))
-        troof = R.w4a16_t_roof(M, N, K, g) * 1e6
-        per_m.append({
-            "M": M, "us": round(t_us, 3), "us_min": round(min(times), 3),
-            "tflops": round(R.flops(M, N, K) / (t_us * 1e-6) / 1e12, 3),
-            "weight_GBps": round(R.weight_bytes(N, K, g) / (t_us * 1e-6) / 1e9, 1),
-            "roof_us": round(troof, 3), "roof_frac": round(troof / t_us, 4),
-            "bound": R.bound(M, N, K, g),
-            "launch": mk.marlin_describe(M, N, K, g),
-        })
-        log("M=%3d: %.3f us/call  %.1f weight GB/s  roofline frac %.3f" %
-            (M, t_us, per_m[-1]["weight_GBps"], troof / t_us))
+    w0 = time.time()
+    for lay in layers:
+        la = {M: acts[(lay.K, lay.N, M)] for M in M_SWEEP}
+        lo = {M: outs[(lay.K, lay.N, M)] for M in M_SWEEP}
+        per_m += measure_cases(args, mk, R, torch, np, dev, lay, M_SWEEP, stream, L, ws, la, lo, "70b")
+    if clock:
+        clock.mark(w0, time.time())
+    for lay in layers:
+        lay.w16s = []
+    torch.cuda.synchronize()
 
-    # ---- fp16 comparator: torch.matmul with rotated fp16 weights ----
-    if not args.no_fp16:
-        w16 = torch.from_numpy((s.astype(np.float32).repeat(g, axis=0) *
-                                (q.astype(np.float32) - 8)).astype(np.float16)).to(dev)
-        nrot16 = max(2, math.ceil(ROTATION_BYTES / (w16.numel() * 2)))
-        w16s = [w16] + [w16.clone() for _ in range(nrot16 - 1)]
-        for rec in per_m:
-            M = rec["M"]
-            A = acts[M]
-            eager = torch.matmul(A, w16s[0])
-            torch.cuda.synchronize()
-            gr = torch.cuda.CUDAGraph()
-            c16 = [None] * nrot16
-            with torch.cuda.stream(stream):
-                torch.matmul(A, w16s[0])
-                stream.synchronize()
-                with torch.cuda.graph(gr, stream=stream):
-                    for i in range(nrot16):
-                        c16[i] = torch.matmul(A, w16s[i])
-                gr.replay()
-                torch.cuda.synchronize()
-                same = bool(torch.equal(c16[0], eager))
-                times = []
-                for _ in range(args.per_m_reps):
-                    a0 = torch.cuda.Event(enable_timing=True)
-                    a1 = torch.cuda.Event(enable_timing=True)
-                    a0.record(stream)
-                    gr.replay()
-                    a1.record(stream)
-                    a1.synchronize()
-                    times.append(a0.elapsed_time(a1) * 1e3 / nrot16)
-            del gr, c16
-            t16 = float(np.median(times))
-            rec["fp16_us"] = round(t16, 3)
-            rec["speedup_vs_fp16"] = round(t16 / rec["us"], 3)
-            rec["fp16_graph_matches_eager"] = same
-            log("M=%3d: fp16 matmul %.3f us/call -> speedup %.2fx" % (M, t16, t16 / rec["us"]))
-        del w16s, w16
+    # by kernel class: the stream kernel's launches (M <= 32) and the rest
+    by_kernel = {}
+    for r in per_m:
+        k = r["launch"].split("<")[0]
+        d = by_kernel.setdefault(k, {"launches_per_step": 0, "algorithmic_bytes": 0.0, "us": 0.0})
+        d["launches_per_step"] += 1
+        d["algorithmic_bytes"] += R.w4a16_bytes(r["M"], r["N"], r["K"], r["group"])
+        d["us"] += r["us"]
+    for k, d in by_kernel.items():
+        d["achieved_GBps"] = round(d["algorithmic_bytes"] / (d["us"] * 1e-6) / 1e9, 1)
+        d["frac"] = round(d["algorithmic_bytes"] / (d["us"] * 1e-6) / R.HBM_BYTES_PER_S, 4)
+        d["algorithmic_bytes"] = round(d["algorithmic_bytes"])
+        d["us"] = round(d["us"], 3)
 
-    # ---- CPU baseline: the fp64 oracle over the same sweep (also a parity check) ----
+    # ---- CPU baseline: the fp64 oracle on the host (also a full-output parity check) ----
     cpu = None
     parity = None
     if not args.no_cpu_baseline:
         import oracle
         threads = cpu_threads()
-        tot = 0.0
-        worst = 0.0
-        ok = True
-        for M in M_SWEEP:
-            A_np = acts[M].cpu().numpy()
-            runs = []
-            for _ in range(3):
-                c0 = time.perf_counter()
-                ref = oracle.gemm(A_np, q, s, g)
-                runs.append(time.perf_counter() - c0)
-            tot += float(np.median(runs))
-            launch(M, 0, torch.cuda.current_stream())
+        tot, flops, rows = 0.0, 0.0, []
+        worst, ok = 0.0, True
+        for lay in layers:
+            for M in CPU_MS:
+                A_np = acts[(lay.K, lay.N, M)].cpu().numpy()
+                runs = []
+                for _ in range(3):
+                    c0 = time.perf_counter()
+                    ref = oracle.gemm(A_np, lay.q, lay.s, lay.g)
+                    runs.append(time.perf_counter() - c0)
+                dt = float(np.median(runs))
+                tot += dt
+                flops += R.flops(M, lay.N, lay.K)
+                rows.append({"K": lay.K, "N": lay.N, "M": M, "seconds": round(dt, 4),
+                             "GFLOPs": round(R.flops(M, lay.N, lay.K) / dt / 1e9, 2)})
+                launch(lay, M, 0)
+                torch.cuda.synchronize()
+                got = outs[(lay.K, lay.N, M)].cpu().numpy().astype(np.float64)
+                err = np.abs(got - ref)
+                ok &= bool((err <= 2e-3 + 1e-2 * np.abs(ref)).all())
+                worst = max(worst, float(err.max()))
+                log("oracle %dx%d M=%d: %.3f s" % (lay.K, lay.N, M, dt))
+        cpu = {"value": round(flops / tot / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+               "sample": "fp64 oracle, full products of both 70B-class layers at M in %s (median of 3 runs "
+                         "each, %.1f GFLOP per run set)" % (CPU_MS, flops / 1e9),
+               "seconds": round(tot, 3), "cpu_model": cpu_model(), "per_case": rows,
+               "single_thread": single}
+        parity = {"ok": ok, "max_abs_err": worst, "cases": "both layers at M in %s, every output" % CPU_MS,
+                  "bar": "|C_gpu - C_ref| <= 2e-3 + 1e-2 |C_ref|"}
+        log("oracle: %.2f s on %d threads (%s); GPU parity %s (max err %.3g)" %
+            (tot, threads, cpu["cpu_model"], ok, worst))
+
+    sections = {}
+    if not args.no_sections:
+        del acts, outs, layers
+        torch.cuda.synchronize()
+        for name in SECTIONS:
+            sections[name] = run_section(name, args, mk, R, synth, torch, np, dev)
             torch.cuda.synchronize()
-            got = outs[M].cpu().numpy().astype(np.float64)
-            err = np.abs(got - ref)
-            ok &= bool((err <= 2e-3 + 1e-2 * np.abs(ref)).all())
-            worst = max(worst, float(err.max()))
-        cpu = {"value": round(step_flops / tot / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
-               "kind": "oracle", "seconds": round(tot, 3),
-               "sample": "the whole step (fp64 oracle at every M of the sweep, 4096x4096 g=128), "
-                         "median of 3 runs per M"}
-        parity = {"ok": ok, "max_abs_err": worst}
-        log("oracle: %.2f s for one step on %d threads; GPU parity %s (max err %.3g)" %
-            (tot, threads, ok, worst))
 
-    sparse = None if args.no_sparse else sparse_section(args, mk, R, synth, torch, np, dev)
-    prefill = None if args.no_prefill else prefill_section(args, mk, R, synth, torch, np, dev)
-    quant = None if args.no_quantize else quantize_section(args, mk, R, synth, torch, np, dev)
-
+    clock_rec = clock.finish() if clock else None
     small = [r for r in per_m if r["M"] <= 16]
+    copies = {"%dx%d" % (K, N): int(math.ceil(ROTATION_BYTES / (K * N / 2 + 2 * (K // g) * N))) for K, N, _, g in HEADLINE}
     out = {
         "metric": "W4A16 GEMM TFLOP/s & weight GB/s vs roofline, M=1..128; speedup vs fp16 GEMM",
         "value": round(value, 3),
@@ -545,30 +824,31 @@ def main():
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": "Llama-7B attention projection W4A16 GEMM, K=4096 N=4096 g=128, "
-                               "M sweep 1..128, weights rotated over %.2f GB" % (nrot * wbytes / 1e9),
-                   "K": K, "N": N, "group": g, "M": M_SWEEP, "weight_copies": nrot,
-                   "launches_per_step": len(M_SWEEP)},
+        "config": {"workload": "70B-scale single-GPU layer shapes, W4A16 GEMM (K=8192 N=28672) and "
+                               "(K=28672 N=8192), g=128, M sweep 1..128, weights rotated over >1 GB per layer",
+                   "layers": [[K, N] for K, N, _, _ in HEADLINE], "group": GROUP, "M": M_SWEEP,
+                   "weight_copies": copies, "launches_per_step": len(cases)},
         "weight_GBps": round(step_wbytes / (ms_per_step * 1e-3) / 1e9, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved_gbs, 1),
                      "peak": R.HBM_BYTES_PER_S / 1e9, "unit": "GB/s",
                      "frac": round(achieved_gbs * 1e9 / R.HBM_BYTES_PER_S, 4),
                      "traffic": measured_traffic(),
                      "traffic_unit": "HBM bytes per launch (step average)",
-                     "algorithmic_bytes_per_launch": round(step_bytes / len(M_SWEEP)),
+                     "algorithmic_bytes_per_launch": round(step_bytes / len(cases)),
                      "avg_launch_us": round(avg_launch_us, 3),
-                     "kernel": "w4a16_stream_kernel"},
-        "roof_frac_step": round(sum(R.w4a16_t_roof(M, N, K, g) for M in M_SWEEP) /
-                                (ms_per_step * 1e-3), 4),
+                     "kernel": "w4a16_stream_kernel (M <= 32) and w4a16_tile_kernel (M = 64, 128): every "
+                               "launch of the step",
+                     "by_kernel": by_kernel},
+        "roof_frac_step": round(sum(R.w4a16_t_roof(M, lay_n, lay_k, GROUP) for lay_k, lay_n, _, _ in HEADLINE
+                                    for M in M_SWEEP) / (ms_per_step * 1e-3), 4),
         "min_roof_frac_M_le_16": min(r["roof_frac"] for r in small),
         "per_m": per_m,
         "wall_ms_per_step": round(wall_ms / args.steps, 6),
+        "clock": clock_rec,
         "cpu_baseline": cpu,
         "parity": parity,
-        "sparse_2of4": sparse,
-        "prefill": prefill,
-        "quantize": quant,
     }
+    out.update(sections)
     print(json.dumps(out), flush=True)
 
 

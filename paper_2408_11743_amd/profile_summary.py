@@ -1,29 +1,28 @@
 """Summarise rocprofv3 output of bench.py into the text kept under profiles/.
 
-Usage (after the three profiling runs, see the command block this prints):
+Modes (each reads the JSON line bench.py printed in the same run, --bench):
 
-    python -m paper_2408_11743_amd.profile_summary --trace DIR --fetch DIR \
-        --write DIR --bench BENCH_JSON --out OUT_PREFIX [--copy-mb 256]
+* headline kernel trace -- ``rocprofv3 --kernel-trace --marker-trace --stats
+  --output-format csv`` of ``bench.py``: every kernel dispatch is attributed
+  to the bench's named ranges (one per (layer, M) case, one for the timed
+  steps), giving the median kernel duration per case and the mean over the
+  timed steps' launches beside the bench's event times::
 
-or, for bench.py --prefill-only or --quantize-only, a kernel trace alone (its
-CSV, not only the statistics: --kernel-trace --stats --output-format csv):
+      --trace DIR --bench JSON --out PREFIX
 
-    python -m paper_2408_11743_amd.profile_summary --trace DIR --bench BENCH_JSON --out OUT_PREFIX
+* per-case counters -- ``rocprofv3 --pmc ...`` of ``bench.py --profile-cases C``
+  (each case launched C times in a row, in the order the JSON lists):
+  HBM traffic from a FETCH_SIZE and a WRITE_SIZE pass, scaled by the same
+  passes' plain device copies (--calibration-copy-mb)::
 
-and for the matrix-core counters of bench.py --prefill-only --no-fp16 (one
---pmc pass with PREFILL_COUNTERS):
+      --fetch DIR --write DIR --bench JSON --out PREFIX [--copy-mb 256]
 
-    python -m paper_2408_11743_amd.profile_summary --pmc DIR --bench BENCH_JSON --out OUT_PREFIX
+  or matrix-core and vector counters (one pass of CASE_COUNTERS)::
 
-Reads
-  DIR/*kernel_stats.csv          (rocprofv3 --kernel-trace --stats)
-  DIR/*counter_collection.csv    (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)
-  BENCH_JSON                     (the JSON line bench.py printed in the trace run)
-and writes OUT_PREFIX_kernel_trace.md, OUT_PREFIX_traffic.md and
-OUT_PREFIX_traffic.json.  The counters are scaled by what they read for the
-plain device copies bench.py makes with --calibration-copy-mb (bytes known).
-Each M of the sweep is attributed to its kernel instantiation through
-marlin_describe, the library's own account of the launch it makes.
+      --pmc DIR --bench JSON --out PREFIX
+
+* bench.py --only prefill / quantize / sparse_2of4: kernel trace (and for
+  prefill the matrix-core counters, --pmc), as before.
 """
 from __future__ import annotations
 
@@ -124,20 +123,20 @@ def quantize_summary(a, bench: dict) -> None:
           "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
           "Per shape: the median kernel duration over the shape's replayed dispatches",
           "(rocprofv3), the bench's event time per call of an unprofiled run (--bench),",
-          "and the fraction of the fp32 vector lane rate (78.65 T operations/s: the",
-          "published 157.3 TFLOP/s counts a fused multiply-add as two) that the",
-          "quantiser's algorithmic operations (`roofline.quant_ops`) reach in the",
-          "kernel time; HBM GB/s for reference (fp16 read, codes and scales written):", "",
+          "and the fraction of the vector issue rate (78.6 T lane operations/s: 256 CUs x",
+          "4 SIMDs x 32 lanes x 2.4 GHz) that the kernel's issued vector instructions",
+          "(`roofline.quant_lane_ops`, its instruction count) reach in the kernel time;",
+          "HBM GB/s for reference (fp16 read, codes and scales written):", "",
           "| K | N | kernel | dispatches | median kernel us | bench us | G weights/s | ALU frac | HBM GB/s |",
           "|---|---|---|---|---|---|---|---|---|"]
     for case, run in zip(cases, runs):
         names = sorted({n for n, _ in run})
         med = statistics.median(d for _, d in run)
         K, N = case["K"], case["N"]
-        ops = R.quant_ops(K, N, case["ratios"])
+        ops = R.quant_lane_ops(K, N, case["ratios"])
         md.append("| %d | %d | `%s` | %d | %.1f | %.1f | %.2f | %.3f | %.0f |" % (
             K, N, ", ".join(names), len(run), med, case["us"], K * N / med / 1e3,
-            ops / (med * 1e-6) / R.FP32_LANE_OPS, R.quant_bytes(K, N, case["group"]) / med / 1e3))
+            ops / (med * 1e-6) / R.VALU_LANE_OPS, R.quant_bytes(K, N, case["group"]) / med / 1e3))
     md.append("")
     open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
     print("wrote", a.out + "_kernel_trace.md")
@@ -239,10 +238,235 @@ def prefill_summary(a, bench: dict) -> None:
     print("wrote", a.out + "_kernel_trace.md")
 
 
+def _timestamps_csv(trace_dir: str, pattern: str) -> list[dict]:
+    with open(_one(os.path.join(trace_dir, "**", pattern))) as f:
+        return list(csv.DictReader(f))
+
+
+def marker_ranges(trace_dir: str) -> list[tuple[str, int, int]]:
+    """(name, start ns, end ns) of the bench's named ranges (roctx push/pop
+    pairs; rocprofv3 writes one row per range, or one per push and pop)."""
+    rows = _timestamps_csv(trace_dir, "*marker_api_trace.csv")
+    out, stack = [], []
+    for r in sorted(rows, key=lambda r: int(r["Start_Timestamp"])):
+        name = r.get("Message") or r.get("Function") or ""
+        t0, t1 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        fn = r.get("Function", "")
+        if fn.startswith("roctxRangePush"):
+            stack.append((r.get("Message", name), t0))
+        elif fn.startswith("roctxRangePop"):
+            if stack:
+                n, s = stack.pop()
+                out.append((n, s, t1))
+        elif t1 > t0:
+            out.append((name, t0, t1))
+    return out
+
+
+def dispatches(trace_dir: str) -> list[tuple[int, int, str]]:
+    rows = _timestamps_csv(trace_dir, "*kernel_trace.csv")
+    return sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), short(r["Kernel_Name"])) for r in rows)
+
+
+def headline_trace_summary(a, bench: dict) -> None:
+    """Kernel time per headline case and over the timed steps, from the
+    named ranges of a profiled bench.py run."""
+    import paper_2408_11743_amd.roofline as R
+    ranges = marker_ranges(a.trace)
+    disp = [d for d in dispatches(a.trace) if d[2].startswith("w4a16_")]
+
+    def inside(name):
+        rs = [(s, e) for n, s, e in ranges if n == name]
+        if not rs:
+            raise SystemExit("no range named %r in the marker trace" % name)
+        s, e = rs[-1]
+        return [d for d in disp if s <= d[0] <= e]
+
+    md = ["# Kernel trace: W4A16 GEMM, 70B-class layers, g = 128, M sweep %s" % bench["config"]["M"], "",
+          "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
+          "Per case: the kernel the library launched (`launch`), its dispatches inside the",
+          "case's range (graph replays over the rotated weight copies), their median",
+          "kernel duration (rocprofv3), the bench's event time per launch of the same",
+          "replays, and the HBM roofline fraction of the kernel time (algorithmic bytes /",
+          "kernel time / 8 TB/s; at M = 128 the bound is the MFMA peak, t_roof / t):", "",
+          "| K | N | M | kernel | dispatches | median kernel us | bench us | roofline frac (kernel) |",
+          "|---|---|---|---|---|---|---|---|"]
+    for c in bench["per_m"]:
+        name = "70b w4a16 K=%d N=%d g=%d M=%d" % (c["K"], c["N"], c["group"], c["M"])
+        ds = inside(name)
+        want = c["launch"].split(" cols=")[0]
+        names = {d[2] for d in ds}
+        if names != {want}:
+            raise SystemExit("case %s: trace has %s, expected %s" % (name, names, want))
+        med = statistics.median((d[1] - d[0]) / 1e3 for d in ds)
+        troof = R.w4a16_t_roof(c["M"], c["N"], c["K"], c["group"]) * 1e6
+        md.append("| %d | %d | %d | `%s` | %d | %.2f | %.2f | %.3f |" % (
+            c["K"], c["N"], c["M"], want, len(ds), med, c["us"], troof / med))
+    steps = inside("timed steps")
+    n_l = bench["config"]["launches_per_step"]
+    mean = statistics.fmean((d[1] - d[0]) / 1e3 for d in steps)
+    alg = bench["roofline"]["algorithmic_bytes_per_launch"]
+    md += ["", "Timed steps: %d dispatches (%d steps x %d launches in the profiled run)." % (
+               len(steps), len(steps) // n_l, n_l),
+           "Mean kernel duration per launch: %.3f us (rocprofv3); bench.py's HIP-event" % mean,
+           "time per launch over the same region: %.3f us (`roofline.avg_launch_us`; it" %
+           bench["roofline"]["avg_launch_us"],
+           "also holds the dispatch gap between consecutive graph nodes).",
+           "Algorithmic bytes per launch (step average) %d: %.1f GB/s of kernel time," % (alg, alg / mean / 1e3),
+           "a roofline fraction of %.4f (bench.py, event time: %.4f)." % (
+               alg / (mean * 1e-6) / R.HBM_BYTES_PER_S, bench["roofline"]["frac"]), ""]
+    open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
+    print("wrote", a.out + "_kernel_trace.md")
+
+
+def case_groups(pmc_dir: str, counters: tuple, cases: list, per_case: int) -> list[list[dict]]:
+    """The GEMM dispatches of a --profile-cases run, grouped per case:
+    dispatch order, per_case consecutive dispatches per case."""
+    per = {}
+    with open(_one(os.path.join(pmc_dir, "**", "*counter_collection.csv"))) as f:
+        for r in csv.DictReader(f):
+            if not short(r["Kernel_Name"]).startswith("w4a16_"):
+                continue
+            d = per.setdefault(int(r["Dispatch_Id"]), {"name": short(r["Kernel_Name"])})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    ds = [per[k] for k in sorted(per)]
+    if len(ds) != per_case * len(cases):
+        raise SystemExit("%d GEMM dispatches for %d cases x %d" % (len(ds), len(cases), per_case))
+    groups = [ds[i * per_case:(i + 1) * per_case] for i in range(len(cases))]
+    for c, g in zip(cases, groups):
+        want = c["launch"].split(" cols=")[0]
+        if {d["name"] for d in g} != {want}:
+            raise SystemExit("case %s: dispatches of %s" % (c, {d["name"] for d in g}))
+    return groups
+
+
+CASE_COUNTERS = ("SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_LDS",
+                 "SQ_LDS_BANK_CONFLICT", "SQ_WAVES", "GRBM_GUI_ACTIVE")
+
+
+def case_counter_summary(a, bench: dict) -> None:
+    """Matrix-core utilisation and vector work per case (one --pmc pass)."""
+    cases, C = bench["cases"], bench["profile_cases"]
+    groups = case_groups(a.pmc, CASE_COUNTERS, cases, C)
+    simds, xcds = 256 * 4, 8
+    md = ["# Matrix-core and vector counters: W4A16 GEMM, %s layers, M sweep" % bench["layers"], "",
+          "Command (`TMPDIR=/tmp`, from the repository root; one counter pass, every case",
+          "launched %d times in a row):" % C, "", "```", a.pmc_cmd, "```", "",
+          "Medians over each case's dispatches.  MFMA utilisation = MFMA busy cycles /",
+          "(1024 SIMDs x kernel cycles), kernel cycles = GRBM_GUI_ACTIVE / 8 XCDs: the",
+          "fraction of the matrix-core peak at the clock the chip ran.  VALU per MFMA:",
+          "the other vector instructions per MFMA instruction (dequantisation, fold).", "",
+          "| K | N | g | M | kernel | MFMA / dispatch | MFMA busy | kernel cycles | MFMA util | VALU per MFMA | LDS instr | LDS bank conflicts |",
+          "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for c, g in zip(cases, groups):
+        med = {k: statistics.median(d.get(k, 0.0) for d in g) for k in CASE_COUNTERS}
+        cyc = med["GRBM_GUI_ACTIVE"] / xcds
+        util = med["SQ_VALU_MFMA_BUSY_CYCLES"] / (simds * cyc) if cyc else float("nan")
+        other = (med["SQ_INSTS_VALU"] - med["SQ_INSTS_MFMA"]) / med["SQ_INSTS_MFMA"] if med["SQ_INSTS_MFMA"] else 0
+        md.append("| %d | %d | %s | %d | `%s` | %.0f | %.3g | %.3g | %.3f | %.2f | %.3g | %.0f |" % (
+            c["K"], c["N"], "K" if c["group"] == -1 else c["group"], c["M"], g[0]["name"], med["SQ_INSTS_MFMA"],
+            med["SQ_VALU_MFMA_BUSY_CYCLES"], cyc, util, other, med["SQ_INSTS_LDS"], med["SQ_LDS_BANK_CONFLICT"]))
+    md.append("")
+    open(a.out + "_counters.md", "w").write("\n".join(md) + "\n")
+    print("wrote", a.out + "_counters.md")
+
+
+def case_traffic_summary(a, bench: dict) -> None:
+    """HBM bytes per case from a FETCH_SIZE and a WRITE_SIZE pass of
+    bench.py --profile-cases, scaled by the passes' calibration copies."""
+    import paper_2408_11743_amd.roofline as R
+    cases, C = bench["cases"], bench["profile_cases"]
+    gf = case_groups(a.fetch, ("FETCH_SIZE",), cases, C)
+    gw = case_groups(a.write, ("WRITE_SIZE",), cases, C)
+    fetch = counter_per_dispatch(a.fetch, "FETCH_SIZE")
+    write = counter_per_dispatch(a.write, "WRITE_SIZE")
+    copy_bytes = a.copy_mb * (1 << 20)
+
+    def largest(samples):
+        v = [x for n, x in samples if COPY_KERNEL in n]
+        return [x for x in v if x >= 0.9 * max(v)] if v else []
+
+    cf, cw = largest(fetch), largest(write)
+    if not cf or not cw:
+        raise SystemExit("no calibration copies in the counter runs (--calibration-copy-mb)")
+    f_scale = copy_bytes / (statistics.median(cf) * 1024.0)
+    w_scale = copy_bytes / (statistics.median(cw) * 1024.0)
+    md = ["# HBM traffic: W4A16 GEMM, %s layers, M sweep (rocprofv3 counters)" % bench["layers"], "",
+          "Commands (two counter passes, each its own run, `TMPDIR=/tmp`; every case launched",
+          "%d times in a row, each launch on the next weight copy):" % C, "", "```",
+          a.fetch_cmd, a.write_cmd, "```", "",
+          "Calibration: the same runs make plain device copies of %d MiB (the runtime's" % a.copy_mb,
+          "copy kernel).  Per copy FETCH_SIZE reads %.0f KiB for %d KiB read (scale x%.3f)," %
+          (statistics.median(cf), copy_bytes // 1024, f_scale),
+          "WRITE_SIZE %.0f KiB for %d KiB written (scale x%.3f)." % (statistics.median(cw), copy_bytes // 1024, w_scale),
+          "", "Per case (median over its dispatches), scaled:", "",
+          "| K | N | g | M | kernel | fetch MB | write MB | HBM MB | algorithmic MB | ratio |",
+          "|---|---|---|---|---|---|---|---|---|---|"]
+    hbm, tot = {}, 0.0
+    for c, f, w in zip(cases, gf, gw):
+        fb = statistics.median(d["FETCH_SIZE"] for d in f) * 1024.0 * f_scale
+        wb = statistics.median(d["WRITE_SIZE"] for d in w) * 1024.0 * w_scale
+        alg = R.w4a16_bytes(c["M"], c["N"], c["K"], c["group"])
+        md.append("| %d | %d | %s | %d | `%s` | %.2f | %.2f | %.2f | %.2f | %.3f |" % (
+            c["K"], c["N"], "K" if c["group"] == -1 else c["group"], c["M"], f[0]["name"], fb / 1e6, wb / 1e6,
+            (fb + wb) / 1e6, alg / 1e6, (fb + wb) / alg))
+        hbm["K=%d N=%d g=%d M=%d" % (c["K"], c["N"], c["group"], c["M"])] = round(fb + wb)
+        tot += fb + wb
+    digest = kernel_sources_digest()
+    md += ["", "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N.", "",
+           "Average per launch over the cases: %.2f MB (bench.py reports it as `roofline.traffic`" %
+           (tot / len(cases) / 1e6),
+           "while the kernel sources (%s under `paper_2408_11743_amd/csrc/`) hash to `%s...`)." %
+           (", ".join(KERNEL_SOURCES), digest[:16]), ""]
+    open(a.out + "_traffic.md", "w").write("\n".join(md) + "\n")
+    rec = {"workload": "W4A16 GEMM, %s layers, M sweep (bench.py --profile-cases)" % bench["layers"],
+           "kernel_sources_sha256": digest,
+           "counter_scale": {"FETCH_SIZE": round(f_scale, 4), "WRITE_SIZE": round(w_scale, 4),
+                             "calibration": "device copies of %d MiB" % a.copy_mb},
+           "hbm_bytes_per_launch": hbm, "step_avg_hbm_bytes_per_launch": round(tot / len(cases))}
+    json.dump(rec, open(a.out + "_traffic.json", "w"), indent=1)
+    print("wrote", a.out + "_traffic.md", a.out + "_traffic.json")
+
+
+def sparse_summary(a, bench: dict) -> None:
+    """Kernel trace of bench.py --only sparse_2of4 (with --marker-trace): per
+    M the 2:4 kernel's and the dense kernel's median duration on 8192 x 8192."""
+    import paper_2408_11743_amd.roofline as R
+    ranges = marker_ranges(a.trace)
+    disp = [d for d in dispatches(a.trace) if d[2].startswith("w4a16_")]
+    K = N = 8192
+    g = 128
+    md = ["# Kernel trace: 2:4 sparse W4A16 GEMM, K = N = 8192, g = 128, M sweep", "",
+          "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
+          "Per M: median kernel duration of the 2:4 kernel and of the dense W4A16 kernel on",
+          "the same (pruned) matrix, each over its case's replays, and the 2:4 kernel's",
+          "fraction of the HBM roofline of its algorithmic bytes (3/8 byte per weight plus",
+          "scales, A and C) in kernel time:", "",
+          "| M | 2:4 kernel | median us | dense kernel | median us | speedup | roofline frac (kernel) |",
+          "|---|---|---|---|---|---|---|"]
+    for c in bench["sparse_2of4"]["per_m"]:
+        M = c["M"]
+        res = []
+        for tag in ("2:4", "dense"):
+            rs = [(s, e) for n, s, e in ranges if n == "sparse %s M=%d" % (tag, M)]
+            if not rs:
+                raise SystemExit("no range for sparse %s M=%d" % (tag, M))
+            s, e = rs[-1]
+            ds = [d for d in disp if s <= d[0] <= e]
+            res.append((sorted({d[2] for d in ds}), statistics.median((d[1] - d[0]) / 1e3 for d in ds)))
+        troof = R.sparse24_t_roof(M, N, K, g) * 1e6
+        md.append("| %d | `%s` | %.2f | `%s` | %.2f | %.3f | %.3f |" % (
+            M, ", ".join(res[0][0]), res[0][1], ", ".join(res[1][0]), res[1][1], res[1][1] / res[0][1],
+            troof / res[0][1]))
+    md.append("")
+    open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
+    print("wrote", a.out + "_kernel_trace.md")
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace")
-    ap.add_argument("--pmc", help="counter run of bench.py --prefill-only --no-fp16 (prefill counters)")
+    ap.add_argument("--pmc", help="one counter pass (prefill counters, or CASE_COUNTERS of --profile-cases)")
     ap.add_argument("--pmc-cmd", default="")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
@@ -254,10 +478,14 @@ def main() -> None:
     ap.add_argument("--write-cmd", default="")
     a = ap.parse_args()
 
-    import paper_2408_11743_amd as mk
-
     bench = json.loads(open(a.bench).read().strip().splitlines()[-1])
-    if "prefill" in bench and "config" not in bench:  # bench.py --prefill-only
+    if "profile_cases" in bench:  # bench.py --profile-cases
+        if a.pmc:
+            case_counter_summary(a, bench)
+        else:
+            case_traffic_summary(a, bench)
+        return
+    if "prefill" in bench and "config" not in bench:  # bench.py --only prefill
         if a.pmc:
             prefill_counter_summary(a, bench)
         else:
@@ -265,125 +493,13 @@ def main() -> None:
         return
     if not a.trace:
         raise SystemExit("--trace is required for this bench output")
-    if "quantize" in bench and "config" not in bench:  # bench.py --quantize-only
+    if "quantize" in bench and "config" not in bench:  # bench.py --only quantize
         quantize_summary(a, bench)
         return
-    if not a.fetch or not a.write:
-        raise SystemExit("--fetch and --write are required for the M sweeps")
-    import paper_2408_11743_amd.roofline as R
-    sparse = "config" not in bench  # bench.py --sparse-only
-    if sparse:
-        sec = bench["sparse_2of4"]
-        K, N, g = 8192, 8192, 128
-        Ms = [r["M"] for r in sec["per_m"]]
-        bench_per_m = sec["per_m"]
-        describe = {M: mk.marlin_describe_sparse(M, N, K, g) for M in Ms}
-        alg_bytes = R.sparse24_bytes
-        title = "2:4 sparse W4A16 GEMM"
-    else:
-        K, N, g = bench["config"]["K"], bench["config"]["N"], bench["config"]["group"]
-        Ms = bench["config"]["M"]
-        bench_per_m = bench.get("per_m", [])
-        describe = {M: mk.marlin_describe(M, N, K, g) for M in Ms}
-        alg_bytes = R.w4a16_bytes
-        title = "W4A16 GEMM"
-    # kernel name as a profiler prints it, e.g. "w4a16_stream_kernel<1, 1, 8, 1, false>"
-    kname = {M: describe[M].split(" cols=")[0] for M in Ms}
-
-    # ---- kernel trace ----
-    stats = kernel_stats(a.trace)
-    rows, step_ns = [], 0.0
-    for M in Ms:
-        hits = [(n, v) for n, v in stats.items() if short(n) == kname[M]]
-        if not hits:
-            raise SystemExit("kernel %s (M=%d) not in the trace" % (kname[M], M))
-        avg = hits[0][1]["avg_ns"]  # all launches of one instantiation (all Ms that share it)
-        cfg = "cols=" + describe[M].split(" cols=")[1] if " cols=" in describe[M] else ""
-        rows.append((M, kname[M], cfg, hits[0][1]["calls"], avg))
-        step_ns += avg
-    md = ["# Kernel trace: %s, K = %d, N = %d, g = %d, M sweep %s" % (title, K, N, g, Ms), "",
-          "Command (`TMPDIR=/tmp`, from the repository root):", "", "```", a.trace_cmd, "```", "",
-          "Average duration per launch of each kernel instantiation over all its",
-          "launches in the run (warm-up included; other kernels, such as the fp16",
-          "comparator's, are not matched):", "",
-          "| M | kernel | configuration | launches | avg kernel us | bench us per launch |",
-          "|---|---|---|---|---|---|"]
-    per_m = {r["M"]: r["us"] for r in bench_per_m}
-    for M, k, cfg, calls, avg in rows:
-        md.append("| %d | `%s` | %s | %d | %.3f | %.3f |" % (M, k, cfg, calls, avg / 1e3, per_m.get(M, float("nan"))))
-    md += ["", "Mean over the %d launches of one step: %.3f us of kernel time (rocprofv3)." % (len(Ms), step_ns / len(Ms) / 1e3)]
-    if not sparse:
-        md += ["%.3f us per launch measured by bench.py with HIP events over its timed region" % bench["roofline"]["avg_launch_us"],
-               "(`roofline.avg_launch_us`, an unprofiled run: --bench)."]
-    md += ["The event time of a launch (bench us per launch, graph replays) also holds",
-           "the dispatch gap between consecutive graph nodes, which the kernel time",
-           "excludes (an empty kernel costs about 1.7 us per launch in a graph).",
-           "Shared instantiations (same kernel for several M) report one average for all",
-           "of their launches, so the per-M rows are approximate where a kernel is shared.", ""]
-    open(a.out + "_kernel_trace.md", "w").write("\n".join(md) + "\n")
-
-    # ---- traffic ----
-    fetch = counter_per_dispatch(a.fetch, "FETCH_SIZE")
-    write = counter_per_dispatch(a.write, "WRITE_SIZE")
-    copy_bytes = a.copy_mb * (1 << 20)
-    # The calibration copies are the largest copy dispatches of the run (the
-    # weight clones bench.py makes use the same copy kernel, on smaller
-    # buffers: 8.65 MB packed copies, 134 MB fp16 copies in the sparse section).
-    def largest(samples):
-        v = [x for n, x in samples if COPY_KERNEL in n]
-        return [x for x in v if x >= 0.9 * max(v)] if v else []
-
-    cf, cw = largest(fetch), largest(write)
-    if not cf or not cw:
-        raise SystemExit("no calibration copies in the counter runs (--calibration-copy-mb)")
-    f_scale = copy_bytes / (statistics.median(cf) * 1024.0)
-    w_scale = copy_bytes / (statistics.median(cw) * 1024.0)
-
-    def per_kernel(samples, scale):
-        out = {}
-        for n, v in samples:
-            out.setdefault(short(n), []).append(v * 1024.0 * scale)
-        return {k: statistics.median(v) for k, v in out.items()}
-
-    fk, wk = per_kernel(fetch, f_scale), per_kernel(write, w_scale)
-    trows, hbm = [], {}
-    step_bytes = 0.0
-    for M in Ms:
-        k = kname[M]
-        fb, wb = fk.get(k), wk.get(k)
-        if fb is None or wb is None:
-            raise SystemExit("kernel %s (M=%d) has no counter samples" % (k, M))
-        alg = alg_bytes(M, N, K, g)
-        trows.append((M, k, fb, wb, fb + wb, alg))
-        hbm["M=%d %s" % (M, k)] = round(fb + wb)
-        step_bytes += fb + wb
-    md = ["# HBM traffic: %s, K = %d, N = %d, g = %d, M sweep %s" % (title, K, N, g, Ms), "",
-          "Commands (two counter passes, each its own run, `TMPDIR=/tmp`):", "", "```",
-          a.fetch_cmd, a.write_cmd, "```", "",
-          "Calibration: the same runs make plain device copies of %d MiB (the runtime's" % a.copy_mb,
-          "copy kernel).  Per copy FETCH_SIZE reads %.0f KiB for %d KiB read (scale x%.3f)," %
-          (statistics.median(cf), copy_bytes // 1024, f_scale),
-          "WRITE_SIZE %.0f KiB for %d KiB written (scale x%.3f)." % (statistics.median(cw), copy_bytes // 1024, w_scale),
-          "", "Per dispatch (median over the dispatches of each instantiation), scaled:", "",
-          "| M | kernel | fetch MB | write MB | HBM MB | algorithmic MB | ratio |",
-          "|---|---|---|---|---|---|---|"]
-    for M, k, fb, wb, tb, alg in trows:
-        md.append("| %d | `%s` | %.2f | %.2f | %.2f | %.2f | %.2f |" % (M, k, fb / 1e6, wb / 1e6, tb / 1e6, alg / 1e6, tb / alg))
-    digest = kernel_sources_digest()
-    md += ["", ("Algorithmic bytes: K*N/4 + K*N/8 + 2*(K/g)*N + 2*M*K + 2*M*N (kept codes, row indices)."
-                if sparse else "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N."), "",
-           "Step average per launch: %.2f MB (bench.py reports it as `roofline.traffic`" % (step_bytes / len(Ms) / 1e6),
-           "while the kernel sources (%s under `paper_2408_11743_amd/csrc/`) hash to `%s...`)." %
-           (", ".join(KERNEL_SOURCES), digest[:16]), ""]
-    open(a.out + "_traffic.md", "w").write("\n".join(md) + "\n")
-    rec = {"workload": "%s K=%d N=%d g=%d, M sweep %s (bench.py)" % (title, K, N, g, Ms),
-           "kernel_sources_sha256": digest,
-           "counter_scale": {"FETCH_SIZE": round(f_scale, 4), "WRITE_SIZE": round(w_scale, 4),
-                             "calibration": "device copies of %d MiB" % a.copy_mb},
-           "hbm_bytes_per_launch": hbm, "step_launches": Ms,
-           "step_avg_hbm_bytes_per_launch": round(step_bytes / len(Ms))}
-    json.dump(rec, open(a.out + "_traffic.json", "w"), indent=1)
-    print("wrote", a.out + "_kernel_trace.md", a.out + "_traffic.md", a.out + "_traffic.json")
+    if "sparse_2of4" in bench and "config" not in bench:  # bench.py --only sparse_2of4
+        sparse_summary(a, bench)
+        return
+    headline_trace_summary(a, bench)
 
 
 if __name__ == "__main__":

@@ -100,12 +100,28 @@ def ridge_m(g: int = 128, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS, bits: int = 
 
 
 # ---- quantiser (symmetric uniform quantisation with a clipping search) ----
-# fp32 vector lanes per CU and clock: the published fp32 vector peak,
-# 157.3 TFLOP/s, counts a fused multiply-add as 2 FLOPs over 256 CUs at
-# 2.4 GHz, i.e. 128 lanes per CU per clock; an operation that is not a fused
-# multiply-add retires at that lane rate.
+# Vector issue rate: 256 CUs x 4 SIMDs x 32 fp32 lanes per clock x 2.4 GHz
+# = 78.6 T lane operations/s.  The published fp32 vector peak, 157.3 TFLOP/s,
+# is this rate with a fused multiply-add counted as two FLOPs.  The library
+# is built without packed fp32 instructions; that an unpacked wave64
+# instruction issues over two clocks, not four, is measured: the quantiser
+# runs its 10,810 vector instructions per wave (the instruction count of the
+# built g = 128 kernel) on 28,672 waves in about 404 us, 2.9 clocks per
+# instruction and SIMD at the shader clock under load, which a four-clock
+# issue could not reach (rocprofv3 counters in profiles/).
+VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
 FP32_VECTOR_FLOPS = 157.3e12
-FP32_LANE_OPS = FP32_VECTOR_FLOPS / 2
+FP32_LANE_OPS = VALU_LANE_OPS
+
+# Vector instructions per weight (lane operations) of the built g = 128
+# quantiser kernel: 12.35 outside the search (loading, magnitude maximum,
+# the final scale's reciprocal and codes) and 7.21 per clipping ratio
+# (scale multiply, round, clamp, multiply back, subtract, square,
+# accumulate), counted in its gfx950 assembly: 1580 + 923 per ratio, for the
+# 128 weights a thread owns.
+QUANT_VALU_BASE = 1580 / 128
+QUANT_VALU_PER_RATIO = 923 / 128
+QUANT_VALU_PER_WEIGHT_G128_10 = QUANT_VALU_BASE + 10 * QUANT_VALU_PER_RATIO
 
 
 def quant_ops(K: int, N: int, n_ratios: int) -> float:
@@ -115,6 +131,13 @@ def quant_ops(K: int, N: int, n_ratios: int) -> float:
     square, accumulate): 7, and the final code (multiply, round, clamp,
     offset): 4."""
     return float(K) * N * (1 + 7 * n_ratios + 4)
+
+
+def quant_lane_ops(K: int, N: int, n_ratios: int) -> float:
+    """Vector lane operations the built g = 128 quantiser issues for K*N
+    weights (its instruction count, which includes conversions, address
+    arithmetic and the reciprocal)."""
+    return float(K) * N * (QUANT_VALU_BASE + QUANT_VALU_PER_RATIO * n_ratios)
 
 
 def quant_bytes(K: int, N: int, g) -> float:
