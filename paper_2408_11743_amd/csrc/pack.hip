@@ -7,8 +7,9 @@
 //   word (((c*KU + ku)*4 + nb)*64 + l)*4 + t holds column n = 64c + 16nb + l%16,
 //   rows k = 128ku + 32t + 8(l/16) + j (j = 0..7), code j in nibble
 //   (j >> 1) + 4(j & 1).
-// The nibble order puts codes j and j+1 sixteen bits apart, so one mask-and-or
-// yields two fp16 values at once (see dequant8 in gemm.hip).
+// The nibble order puts codes j and j+1 sixteen bits apart, so one mask (and
+// an or with the magic number) yields two fp16 values at once (dequant_sub in
+// gemm.hip, dequant_magic in device.h).
 //
 // Scales (fp16), r = scale row, lg = n-row group of the MFMA output, i = 0..3:
 //   index (((c*G + r)*4 + lg)*4 + nb)*4 + i holds s[r][64c + 16nb + 4lg + i],

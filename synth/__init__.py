@@ -15,6 +15,10 @@ layers the paper benchmarks in Section 5.1):
 * scales: one fp16 scale per group of g consecutive rows of K in each
   column, s = fp16(u / (8 * sqrt(K))), u ~ U[0.5, 1.5]; g = K means one
   scale per output channel.  With these scales Var(C) is O(1).
+* non-centred and outlier activations for the parity tests: A ~ U[0, 8]
+  (every product of a column has one sign, so the sums are large next to
+  their signed parts), and A ~ N(0, 1) with 1% of the K columns (the same in
+  every row) multiplied by 64;
 * unquantised fp16 weights (input of the quantiser), [K, N]: per column a
   spread sigma = u / sqrt(K), u ~ U[0.5, 1.5], times N(0, 1) draws, and one
   entry in 1000 multiplied by 8 (the outlier weights of trained LLM layers,
@@ -35,6 +39,8 @@ __all__ = [
     "WORKLOADS",
     "weights",
     "activations",
+    "activations_uniform",
+    "activations_outlier_columns",
     "sparse24_weights",
     "fp16_weights",
     "num_groups",
@@ -81,6 +87,24 @@ def activations(wid: int, M: int, K: int):
     """Draw A float16 [M, K], A ~ N(0, 1) rounded to fp16."""
     rng = np.random.default_rng([int(wid), 0, int(M), int(K)])
     return rng.standard_normal((M, K)).astype(np.float16)
+
+
+def activations_uniform(wid: int, M: int, K: int, lo: float = 0.0, hi: float = 8.0):
+    """Draw A float16 [M, K], A ~ U[lo, hi) rounded to fp16 (non-centred
+    activations: every product of a column has the same sign)."""
+    rng = np.random.default_rng([int(wid), 4, int(M), int(K)])
+    return rng.uniform(lo, hi, size=(M, K)).astype(np.float16)
+
+
+def activations_outlier_columns(wid: int, M: int, K: int, frac: float = 0.01, factor: float = 64.0):
+    """Draw A float16 [M, K]: N(0, 1), with a random `frac` of the K columns
+    (the same columns in every row) multiplied by `factor` -- the outlier
+    features of LLM activations."""
+    rng = np.random.default_rng([int(wid), 5, int(M), int(K)])
+    a = rng.standard_normal((M, K))
+    cols = rng.random(K) < frac
+    a[:, cols] *= factor
+    return a.astype(np.float16)
 
 
 def sparse24_weights(wid: int, K: int, N: int, g: int | None):

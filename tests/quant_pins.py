@@ -19,8 +19,18 @@ the same pins run on the oracle and on planted-mistake copies of it.
 * ``scaling``: multiplying W by 4 multiplies s by 4 and keeps q (powers of two
   commute with every rounding step away from under/overflow).
 * ``per_channel``: group -1 and group K agree.
+* ``exact_rounding``: every code is the exact quotient v/s of the fp16 inputs
+  rounded to the nearest integer (half to even) and clamped to -8..7, checked
+  with exact rationals for every weight whose quotient is not within 2^-16 of
+  a half-integer.  That window is the tie set: the oracle (and the kernel)
+  divide by multiplying with the fp32 reciprocal of s, which is within
+  2^-22 of v/s for |v/s| < 16, so outside the window both roundings agree
+  and inside it either neighbour may be taken.
 """
 from __future__ import annotations
+
+import math
+from fractions import Fraction
 
 import numpy as np
 
@@ -115,7 +125,33 @@ def pin_per_channel(quantize):
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[1].shape == (1, 16)
 
 
-PINS = [pin_representable, pin_rtn_bound, pin_search, pin_zero, pin_scaling, pin_per_channel]
+def pin_exact_rounding(quantize):
+    K, N, g = 256, 12, 128
+    W = _weights(21, K, N)
+    q, s = quantize(W, g, CLIP)
+    window = Fraction(1, 1 << 16)
+    checked = ties = 0
+    for j in range(K // g):
+        for n in range(N):
+            sv = Fraction(float(s[j, n]))
+            rows = range(j * g, (j + 1) * g)
+            if sv == 0:
+                assert all(q[k, n] == 8 for k in rows)
+                continue
+            for k in rows:
+                x = Fraction(float(W[k, n])) / sv
+                fl = math.floor(x)
+                frac = x - fl
+                if abs(frac - Fraction(1, 2)) <= window:
+                    ties += 1
+                    continue
+                code = min(max(fl + (1 if frac > Fraction(1, 2) else 0), -8), 7) + 8
+                assert int(q[k, n]) == code, ("code", k, n, float(x), int(q[k, n]), code)
+                checked += 1
+    assert checked >= 0.99 * K * N and ties <= 0.01 * K * N, (checked, ties)
+
+
+PINS = [pin_representable, pin_rtn_bound, pin_search, pin_zero, pin_scaling, pin_per_channel, pin_exact_rounding]
 
 
 def run_all(quantize):

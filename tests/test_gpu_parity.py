@@ -3,8 +3,11 @@
 Bar (elementwise tolerance of the hot path): |C_gpu - C_ref| <= 2e-3 + 1e-2*|C_ref|,
 with C_ref the unrounded fp64 oracle value.  Packing and unpacking are
 bit-exact; closed-form cases (zero weights, power-of-two scales, every code
-in every nibble slot) are bit-exact; identity weights reproduce A within the
-bar (the zero point is a separate fp32 product; see that test).
+in every nibble slot) are bit-exact; identity weights reproduce A bit-exactly
+on the tile and 2:4 sparse kernels, which decode q - 8 exactly, and within
+the bar on the stream kernel (its zero point is a separate fp32 product; see
+that test).  Non-centred and outlier activations check that separate product
+where its cancellation is largest.
 
 Inputs are the seeded workloads of ``synth``; large shapes are compared on
 sampled outputs computed one by one by the oracle, in the same launch
@@ -225,6 +228,68 @@ def test_identity_weights_reproduce_A(mk, M):
         assert (err <= 2e-3 + 1e-2 * np.abs(A.astype(np.float64))).all(), (M, g, float(err.max()))
 
 
+_TILE_IDENTITY = ([(spec, M) for M in (1, 16, 32, 64, 128)
+                   for spec in ("kind=tile", "kind=tile,whole=1", "kind=tile,whole=0,grid=7")]
+                  + [("kind=tile,nw=8", 64), ("kind=tile,nw=8", 128), ("kind=tile,nw=8,whole=0,grid=7", 128),
+                     ("kind=tile,nb=2,ks=4", 1), ("kind=tile,nb=4,ks=2,whole=0,grid=7", 16),
+                     ("kind=tile,nb=1,ks=4", 32), ("kind=tile,nb=2,ks=2,whole=0,grid=7", 32)])
+
+
+@pytest.mark.parametrize("spec,M", _TILE_IDENTITY)
+def test_identity_weights_bit_exact_on_the_tile_kernel(mk, force, spec, M):
+    # The tile kernel decodes q - 8 exactly (the magic-number subtraction),
+    # so identity weights with s = 1 give C == A bit for bit: one product
+    # A[m][n] * 1 per output, exact in the fp32 accumulation, the fold and the
+    # fp16 rounding (Section 3.4, "Dequantization and Tensor Cores").
+    force(spec)
+    K = N = 512
+    q = np.full((K, N), 8, dtype=np.uint8) + np.eye(K, dtype=np.uint8)
+    A = synth.activations(6, M, K)
+    for g in (128, -1):
+        s = np.ones((1 if g == -1 else K // g, N), dtype=np.float16)
+        assert mk.marlin_describe(M, N, K, g).startswith("w4a16_tile_kernel<")
+        C = run_gemm(mk, A, q, s, g)
+        assert np.array_equal(C.view(np.uint16), A.view(np.uint16)), (spec, M, g)
+
+
+@pytest.mark.parametrize("M", [1, 16, 32, 64, 128])
+def test_identity_weights_bit_exact_on_the_sparse_kernel(mk, M):
+    # The identity has one non-zero weight per group of 4 rows: it is 2:4
+    # sparse, and the sparse kernel decodes its kept codes exactly.
+    K = N = 512
+    q = np.full((K, N), 8, dtype=np.uint8) + np.eye(K, dtype=np.uint8)
+    A = synth.activations(6, M, K)
+    for g in (128, -1):
+        s = np.ones((1 if g == -1 else K // g, N), dtype=np.float16)
+        wp, sp = mk.pack(dev(q), dev(s), group=g, sparse=True)
+        C = mk.gemm(dev(A), wp, sp, K, N, group=g, sparse=True).cpu().numpy()
+        assert np.array_equal(C.view(np.uint16), A.view(np.uint16)), (M, g)
+
+
+@pytest.mark.parametrize("dist", ["uniform_0_8", "outlier_columns"])
+@pytest.mark.parametrize("g", [128, -1])
+@pytest.mark.parametrize("K", [4096, 28672])
+@pytest.mark.parametrize("spec", ["", "kind=stream"])
+def test_non_centred_and_outlier_activations(mk, force, dist, g, K, spec):
+    # The stream kernel's zero point is a separate fp32 product, 8 * sum A,
+    # subtracted from sum A * q: with A >= 0 both sums are large next to their
+    # difference, and with outlier columns a few terms dominate them.  Every
+    # output against the oracle, the stream kernel forced and in the library's
+    # own choice, at M = 1, 16, 32, 128.
+    force(spec)
+    N = 1024
+    q, s = synth.weights(14, K, N, None if g == -1 else g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    ws = mk.Workspace("cuda")
+    for M in (1, 16, 32, 128):
+        A = (synth.activations_uniform(14, M, K) if dist == "uniform_0_8"
+             else synth.activations_outlier_columns(14, M, K))
+        if spec:
+            assert mk.marlin_describe(M, N, K, g).startswith("w4a16_stream_kernel<")
+        C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws).cpu().numpy()
+        check_close(C, oracle.gemm(A, q, s, g), "%s g=%d K=%d M=%d %s" % (dist, g, K, M, spec))
+
+
 @pytest.mark.parametrize("M", [1, 32, 128])
 def test_zero_weights(mk, M):
     K, N = 1024, 256
@@ -340,7 +405,7 @@ def test_full_size_layers_sampled(mk, wid, K, N, g):
     q, s = synth.weights(wid, K, N, None if g == -1 else g)
     wp, sp = mk.pack(dev(q), dev(s), group=g)
     ws = mk.Workspace("cuda")
-    for M in (1, 16, 32, 128, 1000):
+    for M in (1, 2, 4, 8, 16, 32, 64, 128, 1000):
         A = synth.activations(wid, M, K)
         C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws).cpu().numpy()
         mi, ni = _samples(M, N, 1500, [wid, K, N, M])

@@ -10,6 +10,10 @@ activation loads of a stage, and reading rows before their load had landed
 gave wrong outputs), so the kernels pin the order; this test compiles the
 kernel sources for gfx950 and checks, for every instantiation, that the
 buffer loads form identical stage groups of the size the waits assume.
+
+The same assembly pins the memory-coherence bits the cross-work-group
+combination relies on (device-coherent slot stores and loads, a returning
+atomic for the arrival count, no whole-cache maintenance).
 """
 import os
 import re
@@ -80,3 +84,31 @@ def test_every_kernel_issues_its_loads_in_stage_groups(assembly):
                 bad.append("%s: expected groups %s, got %s" % (name, group, seq))
     assert n >= 100, "kernels not found in the assembly (%d)" % n
     assert not bad, "\n".join(bad)
+
+
+def test_combination_uses_device_coherent_accesses(assembly):
+    # Tiles shared by several work-groups are combined through fp32 slots in
+    # the workspace and one arrival counter per tile.  The slots are written
+    # and read with relaxed agent-scope atomics, which must come out as plain
+    # dword stores and loads carrying the device-coherence bit (sc1), so they
+    # bypass the per-XCD L2s' incoherence without any whole-cache writeback or
+    # invalidate; the arrival is an atomic add that returns the old count
+    # (sc0), which decides the reducer.  Nothing else in the kernels uses
+    # dword global stores or loads (C is written as 8-byte stores).
+    n = 0
+    bad = []
+    for src, text in assembly.items():
+        for name, kind, ints, pc, body in _kernels(text):
+            n += 1
+            lines = [l.strip() for l in body.splitlines() if l.strip() and not l.strip().startswith(";")]
+            stores = [l for l in lines if l.startswith("global_store_dword ")]
+            loads = [l for l in lines if l.startswith("global_load_dword ")]
+            atomics = [l for l in lines if "atomic" in l.split()[0]]
+            if not stores or not loads or not atomics:
+                bad.append("%s: no combination code found" % name)
+            bad += ["%s: %s" % (name, l) for l in stores + loads if not l.endswith(" sc1")]
+            bad += ["%s: %s" % (name, l) for l in atomics
+                    if not (l.startswith("global_atomic_add ") and l.endswith(" sc0"))]
+            bad += ["%s: %s" % (name, l) for l in lines if l.split()[0] in ("buffer_wbl2", "buffer_inv")]
+    assert n >= 100, "kernels not found in the assembly (%d)" % n
+    assert not bad, "\n".join(bad[:20])

@@ -2,7 +2,8 @@
 
 Each mutant is a plausible slip in writing the definition (symmetric uniform
 quantisation with zero point 8, Section 2.2 Eq. 1, and the group-wise
-clipping search, Section 3.5): a wrong zero point, step count or rounding, a
+clipping search, Section 3.5): a wrong zero point, step count or rounding
+(floor, truncation), a
 clamp that loses the code 0, a search that keeps the worst ratio or ignores
 the ratio, a dropped or sign-flipped error term, a range taken without the
 magnitude.  Each copy of ``oracle/quant.py`` must fail at least one pin; the
@@ -24,6 +25,7 @@ MUTANTS = {
     "sixteen_steps": [("s16 = ((a + a) / _F(15))", "s16 = ((a + a) / _F(16))")],
     "step_a_over_8": [("s16 = ((a + a) / _F(15))", "s16 = (a / _F(8))")],
     "floor_rounding": [("t = np.clip(np.rint(v * inv)", "t = np.clip(np.floor(v * inv)")],
+    "truncation": [("t = np.clip(np.rint(v * inv)", "t = np.clip(np.trunc(v * inv)")],
     "clamp_loses_code_0": [("_F(-8), _F(7))", "_F(-7), _F(7))")],
     "keeps_worst_ratio": [("better = err < best_err", "better = (err > best_err) | np.isinf(best_err)")],
     "ratio_ignored": [("a = r * amax", "a = amax")],
