@@ -142,6 +142,55 @@ def quantize_summary(a, bench: dict) -> None:
     print("wrote", a.out + "_kernel_trace.md")
 
 
+QUANT_COUNTERS = ("SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES",
+                  "GRBM_GUI_ACTIVE")
+
+
+def quantize_counter_summary(a, bench: dict) -> None:
+    """Vector-instruction counters of bench.py --only quantize (one --pmc pass
+    of QUANT_COUNTERS): issued vector instructions per weight and the issue
+    rate per SIMD, which fixes the lane rate the quantiser is measured
+    against."""
+    import paper_2408_11743_amd.roofline as R
+    cases = bench["quantize"]["per_shape"]
+    per = {}
+    with open(_one(os.path.join(a.pmc, "**", "*counter_collection.csv"))) as f:
+        for r in csv.DictReader(f):
+            if not short(r["Kernel_Name"]).startswith("quantize_kernel"):
+                continue
+            d = per.setdefault(int(r["Dispatch_Id"]), {"grid": int(r["Grid_Size"])})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    simds, xcds = 256 * 4, 8
+    md = ["# Vector-instruction counters: weight quantiser, g = 128, %d clipping ratios" % cases[0]["ratios"], "",
+          "Command (`TMPDIR=/tmp`, from the repository root; one counter pass):", "", "```", a.pmc_cmd, "```", "",
+          "Medians over each shape's dispatches (a shape is recognised by its grid: one",
+          "thread per (group, column)).  VALU per weight = SQ_INSTS_VALU x 64 lanes /",
+          "weights.  Kernel cycles = GRBM_GUI_ACTIVE / 8 XCDs.  Clocks per VALU",
+          "instruction and SIMD = kernel cycles / (SQ_INSTS_VALU / 1024 SIMDs): below 4,",
+          "an unpacked wave64 vector instruction cannot take four clocks, so the issue",
+          "rate is taken as 32 lanes per SIMD and clock (`roofline.VALU_LANE_OPS`, 78.6",
+          "T lane operations/s at 2.4 GHz); the issue utilisation is 2 / that ratio.", "",
+          "| K | N | dispatches | VALU / wave | VALU per weight | kernel cycles | clocks per VALU instr and SIMD | issue utilisation |",
+          "|---|---|---|---|---|---|---|---|"]
+    for c in cases:
+        K, N, g = c["K"], c["N"], c["group"]
+        grid = (K // g) * ((N + 255) // 256) * 256
+        ds = [d for d in per.values() if d["grid"] == grid]
+        if not ds:
+            raise SystemExit("no quantiser dispatches of grid %d" % grid)
+        med = {k: statistics.median(d.get(k, 0.0) for d in ds) for k in QUANT_COUNTERS}
+        cyc = med["GRBM_GUI_ACTIVE"] / xcds
+        per_simd = med["SQ_INSTS_VALU"] / simds
+        md.append("| %d | %d | %d | %.0f | %.2f | %.3g | %.2f | %.3f |" % (
+            K, N, len(ds), med["SQ_INSTS_VALU"] / med["SQ_WAVES"], med["SQ_INSTS_VALU"] * 64 / (K * N), cyc,
+            cyc / per_simd, 2 * per_simd / cyc))
+    md += ["", "The library's account of the same kernel (`roofline.quant_lane_ops`, from its",
+           "gfx950 assembly): %.2f lane operations per weight at %d ratios." % (
+               R.QUANT_VALU_BASE + R.QUANT_VALU_PER_RATIO * cases[0]["ratios"], cases[0]["ratios"]), ""]
+    open(a.out + "_counters.md", "w").write("\n".join(md) + "\n")
+    print("wrote", a.out + "_counters.md")
+
+
 PREFILL_COUNTERS = ("SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_LDS",
                     "SQ_LDS_BANK_CONFLICT", "SQ_WAVES", "GRBM_GUI_ACTIVE")
 
@@ -491,10 +540,13 @@ def main() -> None:
         else:
             prefill_summary(a, bench)
         return
-    if not a.trace:
+    if not a.trace and not ("quantize" in bench and a.pmc):
         raise SystemExit("--trace is required for this bench output")
     if "quantize" in bench and "config" not in bench:  # bench.py --only quantize
-        quantize_summary(a, bench)
+        if a.pmc:
+            quantize_counter_summary(a, bench)
+        else:
+            quantize_summary(a, bench)
         return
     if "sparse_2of4" in bench and "config" not in bench:  # bench.py --only sparse_2of4
         sparse_summary(a, bench)

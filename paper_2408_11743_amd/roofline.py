@@ -104,11 +104,11 @@ def ridge_m(g: int = 128, bw=HBM_BYTES_PER_S, peak=FP16_MFMA_FLOPS, bits: int = 
 # = 78.6 T lane operations/s.  The published fp32 vector peak, 157.3 TFLOP/s,
 # is this rate with a fused multiply-add counted as two FLOPs.  The library
 # is built without packed fp32 instructions; that an unpacked wave64
-# instruction issues over two clocks, not four, is measured: the quantiser
-# runs its 10,810 vector instructions per wave (the instruction count of the
-# built g = 128 kernel) on 28,672 waves in about 404 us, 2.9 clocks per
-# instruction and SIMD at the shader clock under load, which a four-clock
-# issue could not reach (rocprofv3 counters in profiles/).
+# instruction issues in two clocks, not four, is measured: on 28672 x 8192
+# the quantiser issues 307 M wave instructions (SQ_INSTS_VALU) over 1024
+# SIMDs in 0.94 M kernel clocks (GRBM_GUI_ACTIVE per XCD), 3.1 clocks per
+# instruction and SIMD, which four-clock issue could not reach
+# (profiles/quantize_g128_clip10_counters.md).
 VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
 FP32_VECTOR_FLOPS = 157.3e12
 FP32_LANE_OPS = VALU_LANE_OPS
@@ -118,7 +118,8 @@ FP32_LANE_OPS = VALU_LANE_OPS
 # the final scale's reciprocal and codes) and 7.21 per clipping ratio
 # (scale multiply, round, clamp, multiply back, subtract, square,
 # accumulate), counted in its gfx950 assembly: 1580 + 923 per ratio, for the
-# 128 weights a thread owns.
+# 128 weights a thread owns.  The counters give 83.7 per weight at 10 ratios
+# (branches skip a few), against 84.5 by this count.
 QUANT_VALU_BASE = 1580 / 128
 QUANT_VALU_PER_RATIO = 923 / 128
 QUANT_VALU_PER_WEIGHT_G128_10 = QUANT_VALU_BASE + 10 * QUANT_VALU_PER_RATIO
