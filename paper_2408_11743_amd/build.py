@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libmarlin_mi355x.so")
-SOURCES = ["api.cpp", "plan.cpp", "gemm.hip", "tile.hip", "pack.hip", "quant.hip", "noalloc.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "gemm.hip", "tile.hip", "wide.hip", "pack.hip", "quant.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 instructions are disabled for all device code: plain float code
@@ -29,6 +29,9 @@ ARCH = "gfx950"
 # stage reads them without accumulator-register moves.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                 "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+# The wide kernel's accumulators are written by MFMAs only, so it lets the
+# compiler place them in the accumulation registers.
+SOURCE_FLAGS = {"wide.hip": ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]}
 _NOISE = "is not a recognized feature for this target"
 
 
@@ -48,13 +51,13 @@ def _run(cmd, verbose):
 def build(verbose: bool = False, out: str = LIB, extra: list[str] | None = None) -> str:
     tmpdir = tempfile.mkdtemp(prefix="marlin_build_")
     try:
-        common = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
-                  "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS, *(extra or [])]
+        common = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC]
         objs, cmds = [], []
         for s in SOURCES:
             obj = os.path.join(tmpdir, s + ".o")
             objs.append(obj)
-            cmds.append([hipcc(), *common, "-c", "-o", obj, os.path.join(CSRC, s)])
+            flags = SOURCE_FLAGS.get(s, DEVICE_FLAGS)
+            cmds.append([hipcc(), *common, *flags, *(extra or []), "-c", "-o", obj, os.path.join(CSRC, s)])
         jobs = min(len(cmds), max(1, min(16, os.cpu_count() or 1)))
         with ThreadPoolExecutor(jobs) as ex:
             results = list(ex.map(lambda c: _run(c, verbose), cmds))

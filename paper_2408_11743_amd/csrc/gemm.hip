@@ -125,7 +125,8 @@ __device__ __forceinline__ float4_t smfmac2(half8_t w0, half8_t w1, const half8_
 // ---------------------------------------------------------------------------
 // Register-streaming kernel.
 //
-// A work-group owns a column tile of 16*NB columns (NB 16-column blocks) over
+// A work-group owns a column tile of 16*NB columns (NB 16-column blocks; NB = 8
+// spans two 64-column tiles of the packed layout) over
 // a range of 128-row blocks of K (the striped partition); its KW waves take
 // consecutive 128-row blocks of each stage (waves split K), so no weight or
 // activation byte is shared between waves: each lane loads exactly its MFMA
@@ -248,6 +249,11 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     const uint32_t w_bytes = SPARSE ? (uint32_t)p.K / 8u * (uint32_t)p.N * 3u : (uint32_t)p.K * (uint32_t)(p.N / 2);
 
     const uint32_t s_bytes = (uint32_t)p.G * (uint32_t)p.N * 2u;
+    // NB = 8: the wave's column blocks 4..7 lie in the next 64-column tile of
+    // the packed layout, KU * 4 KiB further on (weights) and G * 128 bytes
+    // further on (scales)
+    const uint32_t w_next = (uint32_t)KU * 4096u;
+    const uint32_t s_next = (uint32_t)p.G * 128u;
 
     u32x4_t wr[SPARSE ? 1 : D][NB];   // dense weights
     SparseWords<NB> sw[SPARSE ? D : 1];  // sparse codes and row indices
@@ -290,7 +296,8 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
 #pragma unroll
             for (int b = 0; b < NB; ++b)
                 wr[j][b] = __builtin_bit_cast(
-                    u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + b * 1024, ld_w, kAuxNonTemporal));
+                    u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rw, w_lane + (b & 3) * 1024,
+                                                                   ld_w + (b >> 2) * w_next, kAuxNonTemporal));
         }
         if constexpr (!PER_CHANNEL) {
             const __amdgpu_buffer_rsrc_t rs =
@@ -307,7 +314,8 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
 #pragma unroll
                 for (int i = 0; i < kSLoads; ++i)
                     sr[j][i] = __builtin_bit_cast(
-                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + i * 16, s_off, 0));
+                        half8_t, __builtin_amdgcn_raw_buffer_load_b128(rs, s_lane + (i & 1) * 16,
+                                                                       s_off + (i >> 1) * s_next, 0));
             }
         }
         issue_order_point();  // stages do not interleave
@@ -449,31 +457,40 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
                 }
             }
         } else {
-            // k-step outer, column block inner: consecutive MFMAs are independent.
+            // k-step outer, column block inner: consecutive MFMAs are
+            // independent.  Column blocks go in passes of at most four (NB = 8:
+            // two passes), which bounds the temporaries; the zero-point
+            // product of the first pass serves both.
+            constexpr int kCB = NB < 4 ? NB : 4;
             float4_t tb[MB];
-            float4_t tmp[NB][MB];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
+            for (int c0 = 0; c0 < NB; c0 += kCB) {
+                float4_t tmp[kCB][MB];
 #pragma unroll
-                for (int mb = 0; mb < MB; ++mb) tb[mb] = mfma(kb, a[mb * 4 + t], t == 0 ? zero4 : tb[mb]);
+                for (int t = 0; t < 4; ++t) {
+                    if (c0 == 0) {
 #pragma unroll
-                for (int b = 0; b < NB; ++b) {
-                    const half8_t w = dequant_sub(wr[j][b][t]);
+                        for (int mb = 0; mb < MB; ++mb) tb[mb] = mfma(kb, a[mb * 4 + t], t == 0 ? zero4 : tb[mb]);
+                    }
+#pragma unroll
+                    for (int b = 0; b < kCB; ++b) {
+                        const half8_t w = dequant_sub(wr[j][c0 + b][t]);
+#pragma unroll
+                        for (int mb = 0; mb < MB; ++mb)
+                            tmp[b][mb] = mfma(w, a[mb * 4 + t], t == 0 ? zero4 : tmp[b][mb]);
+                    }
+                }
+#pragma unroll
+                for (int b = 0; b < kCB; ++b) {
+                    // scales of block c0 + b: halves 4(c0 + b) .. +3 of this lane's runs
+                    const half8_t sv = sr[j][(c0 + b) >> 1];
 #pragma unroll
                     for (int mb = 0; mb < MB; ++mb)
-                        tmp[b][mb] = mfma(w, a[mb * 4 + t], t == 0 ? zero4 : tmp[b][mb]);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            acc[c0 + b][mb][i] = __builtin_fmaf(tmp[b][mb][i] - tb[mb][i],
+                                                                (float)sv[(b & 1) * 4 + i], acc[c0 + b][mb][i]);
                 }
-            }
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                // scales of block b: halves 4b .. 4b+3 of this lane's run
-                const half8_t sv = sr[j][b >> 1];
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        acc[b][mb][i] = __builtin_fmaf(tmp[b][mb][i] - tb[mb][i], (float)sv[(b & 1) * 4 + i],
-                                                       acc[b][mb][i]);
             }
         }
     };
@@ -627,13 +644,13 @@ template <int MB, int NB, int AR, int KW>
 constexpr int stream_depth()
 {
     if constexpr (MB == 1) {
-        constexpr int d = NB == 4 ? 4 : NB == 2 ? 5 : 8;
+        constexpr int d = NB == 8 ? 3 : NB == 4 ? 4 : NB == 2 ? 5 : 8;
         return KW == 8 ? (d + 1) / 2 : d;
     }
     // LDS ring of 32 rows: 8 KiB per wave-stage (eight waves: 16-column
     // tiles only, two stages, 128 KiB)
     if constexpr (KW == 8) return 2;
-    return NB == 4 ? 3 : 4;
+    return NB == 8 ? 2 : NB == 4 ? 3 : 4;
 }
 
 template <int MB, int NB, int AR, int KW>
@@ -643,10 +660,15 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
     GemmProblem arg = p;
     void *args[] = {&arg};
     const bool pc = p.group_units == 0;
-    const void *fn = cfg.sparse ? (pc ? (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, true>
-                                      : (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, false>)
-                                : (pc ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, true>
-                                      : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, false>);
+    const void *fn = pc ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, true>
+                        : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, false>;
+    if constexpr (NB <= 4) {  // the 2:4 layout has 64-column tiles at most
+        if (cfg.sparse)
+            fn = pc ? (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, true>
+                    : (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, false>;
+    } else if (cfg.sparse) {
+        return hipErrorInvalidValue;
+    }
     return hipLaunchKernel(fn, dim3(cfg.grid), dim3(64 * KW), args, 0, stream);
 }
 
@@ -654,6 +676,10 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 {
     if (cfg.kind == kKindTile) {
         tile_kernel_name(cfg, per_channel, buf, n);
+        return;
+    }
+    if (cfg.kind == kKindWide) {
+        wide_kernel_name(cfg, per_channel, buf, n);
         return;
     }
     int d = 0;
@@ -680,6 +706,13 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
     case 8142: d = stream_depth<1, 4, 2, 8>(); break;
     case 8144: d = stream_depth<1, 4, 4, 8>(); break;
     case 8218: d = stream_depth<2, 1, 8, 8>(); break;
+    case 4181: d = stream_depth<1, 8, 1, 4>(); break;
+    case 4182: d = stream_depth<1, 8, 2, 4>(); break;
+    case 4184: d = stream_depth<1, 8, 4, 4>(); break;
+    case 4288: d = stream_depth<2, 8, 8, 4>(); break;
+    case 8181: d = stream_depth<1, 8, 1, 8>(); break;
+    case 8182: d = stream_depth<1, 8, 2, 8>(); break;
+    case 8184: d = stream_depth<1, 8, 4, 8>(); break;
     default: break;
     }
     if (d == 0) {
@@ -693,6 +726,7 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
 hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     if (cfg.kind == kKindTile) return launch_tile_gemm(cfg, p, stream);
+    if (cfg.kind == kKindWide) return launch_wide_gemm(cfg, p, stream);
     switch (cfg.waves * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
     case 4111: return launch_stream<1, 1, 1, 4>(cfg, p, stream);
     case 4112: return launch_stream<1, 1, 2, 4>(cfg, p, stream);
@@ -716,6 +750,13 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
     case 8142: return launch_stream<1, 4, 2, 8>(cfg, p, stream);
     case 8144: return launch_stream<1, 4, 4, 8>(cfg, p, stream);
     case 8218: return launch_stream<2, 1, 8, 8>(cfg, p, stream);
+    case 4181: return launch_stream<1, 8, 1, 4>(cfg, p, stream);
+    case 4182: return launch_stream<1, 8, 2, 4>(cfg, p, stream);
+    case 4184: return launch_stream<1, 8, 4, 4>(cfg, p, stream);
+    case 4288: return launch_stream<2, 8, 8, 4>(cfg, p, stream);
+    case 8181: return launch_stream<1, 8, 1, 8>(cfg, p, stream);
+    case 8182: return launch_stream<1, 8, 2, 8>(cfg, p, stream);
+    case 8184: return launch_stream<1, 8, 4, 8>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

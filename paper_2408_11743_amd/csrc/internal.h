@@ -57,6 +57,8 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
+hipError_t launch_wide_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
+void wide_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

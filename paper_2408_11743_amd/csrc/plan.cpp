@@ -26,6 +26,7 @@ Override parse_override(const char *e)
     if (q) f.whole = atoi(q + 6) ? 1 : 0;
     if (strstr(e, "kind=stream")) f.kind = kKindStream;
     if (strstr(e, "kind=tile")) f.kind = kKindTile;
+    if (strstr(e, "kind=wide")) f.kind = kKindWide;
     q = strstr(e, "ks=");
     if (q) f.ks = atoi(q + 3);
     q = strstr(e, "nw=");
@@ -33,7 +34,7 @@ Override parse_override(const char *e)
     q = strstr(e, "waves=");
     if (q) f.waves = atoi(q + 6);
     if (f.waves != 4 && f.waves != 8) f.waves = 0;
-    if (f.nb != 1 && f.nb != 2 && f.nb != 4) f.nb = 0;
+    if (f.nb != 1 && f.nb != 2 && f.nb != 4 && f.nb != 8) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
 }
@@ -55,7 +56,9 @@ Override current_override()
 
 int slot_floats(const GemmConfig &cfg)
 {
-    return cfg.kind == kKindTile ? cfg.tile_nw * cfg.nb * cfg.mb * 256 : cfg.nb * cfg.mb * 256;
+    if (cfg.kind == kKindTile) return cfg.tile_nw * cfg.nb * cfg.mb * 256;
+    if (cfg.kind == kKindWide) return 4 * cfg.nb * cfg.mb * 256;
+    return cfg.nb * cfg.mb * 256;
 }
 
 // The counter region never moves, whatever the shape, so any sequence of
@@ -114,23 +117,26 @@ constexpr double kStreamFreeContributors = 4.0;
 constexpr double kStreamTailPerExtraContributorUs = 0.45;
 
 // Bytes of weights per microsecond one work-group streams, by rows of A,
-// nb = 4, 2, 1 and waves per work-group (measured; the activation rows arrive
-// in LDS in every class).
+// nb = 8, 4, 2, 1 and waves per work-group (measured; the activation rows
+// arrive in LDS in every class).  nb = 8 (two packed 64-column tiles per
+// wave) holds twice the weight bytes in flight per wave and reads each
+// activation block for twice the columns: fitted to whole-tile and Stream-K
+// timings on the 70B-class layers (8192 x 28672, 28672 x 8192) at M = 1..32.
 double wg_rate(int mb, int ar, int nb, int waves)
 {
-    static const double r4[4][3] = {
-        {31.8e3, 22.3e3, 13.3e3},  // M <= 4
-        {32.5e3, 20.8e3, 13.0e3},  // M <= 8
-        {25.2e3, 16.6e3, 10.7e3},  // M <= 16
-        {17.6e3, 11.6e3, 7.1e3},   // M <= 32 (also each row group of 32 for larger M)
+    static const double r4[4][4] = {
+        {28.0e3, 31.8e3, 22.3e3, 13.3e3},  // M <= 4
+        {28.0e3, 32.5e3, 20.8e3, 13.0e3},  // M <= 8
+        {26.0e3, 25.2e3, 16.6e3, 10.7e3},  // M <= 16
+        {21.5e3, 17.6e3, 11.6e3, 7.1e3},   // M <= 32 (also each row group of 32 for larger M)
     };
-    static const double r8[3][3] = {
-        {38.8e3, 34.2e3, 20.2e3},  // M <= 4
-        {32.7e3, 22.1e3, 15.6e3},  // M <= 8
-        {26.0e3, 16.4e3, 11.0e3},  // M <= 16
+    static const double r8[3][4] = {
+        {30.0e3, 38.8e3, 34.2e3, 20.2e3},  // M <= 4
+        {29.0e3, 32.7e3, 22.1e3, 15.6e3},  // M <= 8
+        {27.0e3, 26.0e3, 16.4e3, 11.0e3},  // M <= 16
     };
     const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : 3;
-    const int col = (nb == 4) ? 0 : (nb == 2) ? 1 : 2;
+    const int col = (nb == 8) ? 0 : (nb == 4) ? 1 : (nb == 2) ? 2 : 3;
     if (waves == 8) return row < 3 ? r8[row][col] : (nb == 1 ? 7.4e3 : 0.0);
     return r4[row][col];
 }
@@ -206,13 +212,13 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.nb = 0;
     cfg.whole = 0;
     int64_t best_grid = grid;
-    if (ov.kind != kKindTile) {
+    if (ov.kind != kKindTile && ov.kind != kKindWide) {
         // eight waves exist for one 16-row block, or two with one 16-column
         // block; an override to eight applies where they do
         const int forced_waves = (ov.waves == 8 && cfg.mb != 1 && ov.nb > 1) ? 4 : ov.waves;
         for (int waves = 8; waves >= 4; waves -= 4) {
             if (forced_waves && waves != forced_waves) continue;
-            for (int nb = 4; nb >= 1; nb >>= 1) {
+            for (int nb = sparse ? 4 : 8; nb >= 1; nb >>= 1) {
                 const double rate = wg_rate(cfg.mb, cfg.ar, nb, waves);
                 if (tiles16 % nb != 0 || rate <= 0.0) continue;
                 if (ov.nb && nb != ov.nb) continue;
@@ -242,7 +248,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     // 128-row block per stage; up to 32 rows, 4x1 waves of 16 or 32 rows over
     // 2 or 4 blocks per stage (measured to win only where whole 128-column
     // tiles fill the chip at 17..32 rows, e.g. N = 28672).
-    if (!sparse && ov.kind != kKindStream) {
+    if (!sparse && ov.kind != kKindStream && ov.kind != kKindWide) {
         for (int nw = 8; nw >= 4; nw -= 4) {
             if (ov.nw && nw != ov.nw) continue;
             // rows per tile: 64*wm with 64-row waves; eight waves at 33..64
@@ -276,6 +282,40 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
                         best_grid = pt.grid;
                     }
                 }
+            }
+        }
+    }
+    // wide kernel: four waves along N, each 64 x 128 or 128 x 64 outputs,
+    // weights in registers, activations and group scales shared in LDS.  One
+    // wave per SIMD: its dequantization and its MFMAs do not overlap, so it
+    // wins only where each dequantized weight feeds 128 rows, beyond 128 rows
+    // (measured per 128-row block of a tile: 1.92 us for 128 x 256 tiles,
+    // 2.15 us for 64 x 512; the combination reads 128 KiB fp32 slots).
+    if (!sparse && ov.kind != kKindStream && ov.kind != kKindTile && (M > 128 || ov.kind == kKindWide)) {
+        const int shapes[2][2] = {{8, 4}, {4, 8}};  // 16-row blocks, 16-column blocks per wave
+        for (const auto &sh : shapes) {
+            const int mbw = sh[0], nbw = sh[1];
+            if (ov.nb && nbw != ov.nb) continue;
+            const int cols = 64 * nbw, rows = 16 * mbw;
+            if (N % cols != 0) continue;
+            const int64_t tiles = (int64_t)(N / cols) * ((M + rows - 1) / rows);
+            const size_t slot_bytes = (size_t)2 * 4 * nbw * mbw * 256 * sizeof(float);
+            const double unit_us = mbw == 8 ? 1.92 : 2.15;
+            const Partition pt =
+                best_partition(ov, tiles, KU, grid, unit_us, 8.0, 2.0, 0.0, slot_bytes, partial_budget);
+            if (pt.t < best) {
+                best = pt.t;
+                cfg.kind = kKindWide;
+                cfg.tile_nw = 4;
+                cfg.tile_wm = 1;
+                cfg.tile_ks = 1;
+                cfg.waves = 0;
+                cfg.nb = nbw;
+                cfg.mb = mbw;
+                cfg.ar = 0;
+                cfg.rg = (M + rows - 1) / rows;
+                cfg.whole = pt.whole;
+                best_grid = pt.grid;
             }
         }
     }

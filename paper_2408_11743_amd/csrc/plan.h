@@ -14,6 +14,7 @@ constexpr int kStreamOcc = 1;  // stream kernel work-groups per compute unit
 
 constexpr int kKindStream = 0;  // w4a16_stream_kernel (any M; row groups of 32)
 constexpr int kKindTile = 1;    // w4a16_tile_kernel (activation tile shared by the waves)
+constexpr int kKindWide = 2;    // w4a16_wide_kernel (four waves along N, weights in registers)
 
 // One launch configuration of the GEMM kernel.
 //   mb   : 16-row blocks of A per row group (1 or 2)
@@ -43,7 +44,7 @@ struct GemmConfig {
 // Columns and rows of one tile of a configuration.
 inline int tile_cols(const GemmConfig &c)
 {
-    return c.kind == kKindTile ? (c.tile_nw / c.tile_wm) * 16 * c.nb : 16 * c.nb;
+    return c.kind == kKindTile ? (c.tile_nw / c.tile_wm) * 16 * c.nb : c.kind == kKindWide ? 64 * c.nb : 16 * c.nb;
 }
 inline int tile_rows(const GemmConfig &c) { return c.kind == kKindTile ? c.tile_wm * 16 * c.mb : 16 * c.mb; }
 
@@ -94,7 +95,7 @@ inline bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks)
 
 // Tuning and test override of the configuration (the cost model is the
 // default): MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>,
-// kind=<stream|tile>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>" forces the column-tile
+// kind=<stream|tile|wide>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>" forces the column-tile
 // width, the work-group count, the partition, the kernel, the stream kernel's
 // waves per work-group and the tile kernel's waves and blocks per stage where
 // the shape allows it.  Fields left out are free (0, or -1 for whole/kind).

@@ -132,13 +132,17 @@ def test_describe_reports_a_launchable_configuration(L):
                        (4096, 28672, 8192, -1), (5000, 11008, 4096, 128)]:
         assert L.marlin_describe(M, N, K, g, buf, len(buf)) == 0
         text = buf.value.decode()
-        assert text.startswith("w4a16_stream_kernel<") or text.startswith("w4a16_tile_kernel<"), text
+        assert text.startswith(("w4a16_stream_kernel<", "w4a16_tile_kernel<", "w4a16_wide_kernel<")), text
         assert ("true>" in text) == (g == -1 or g == K), text
         assert "partition=whole" in text or "partition=streamk" in text, text
         cols = int(text.split("cols=")[1].split()[0])
-        assert cols in (16, 32, 64, 128, 256) and N % cols == 0, text
+        assert cols in (16, 32, 64, 128, 256, 512) and N % cols == 0, text
         if text.startswith("w4a16_stream_kernel<"):
             rows = 32
+        elif text.startswith("w4a16_wide_kernel<"):  # <row blocks, column blocks per wave, ring, ...>, 4 waves
+            mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:2])
+            assert mbw * nbw == 32 and cols == 4 * 16 * nbw, text
+            rows = 16 * mbw
         else:  # w4a16_tile_kernel<waves along N, waves along M, row blocks, column blocks per wave, ks, ...>
             wn, wm, mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:4])
             assert wn * wm in (4, 8) and cols == wn * 16 * nbw, text
@@ -269,5 +273,5 @@ def test_cost_model_avoids_many_contributor_splits():
     d = B.marlin_describe(8, 1280, 8192, 128)
     assert d.startswith("w4a16_stream_kernel<1, 1, ") and "partition=whole grid=80" in d, d
     # the 7B / 70B layer shapes keep their measured-best choices
-    assert "cols=64 rg=1 partition=whole" in B.marlin_describe(16, 28672, 8192, 128)
+    assert "cols=128 rg=1 partition=whole" in B.marlin_describe(16, 28672, 8192, 128)
     assert "cols=64 rg=1 partition=streamk" in B.marlin_describe(32, 4096, 11008, 128)

@@ -148,14 +148,32 @@ def test_each_kernel_and_partition(mk, force, spec, M, K, N, g):
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
 
 
+@pytest.mark.parametrize("spec", ["kind=wide,nb=8", "kind=wide,nb=4", "kind=wide,nb=8,whole=1", "kind=wide,nb=4,whole=1",
+                                  "kind=wide,nb=8,whole=0,grid=7", "kind=wide,nb=4,whole=0,grid=96",
+                                  "kind=wide,nb=8,whole=0,grid=96"])
+@pytest.mark.parametrize("M", [1, 17, 33, 64, 65, 100, 128, 200])
+@pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1536, 512, -1), (1024, 1024, 256)])
+def test_wide_kernel(mk, force, spec, M, K, N, g):
+    # The wide kernel (four waves along N, 64 x 128 or 128 x 64 outputs per
+    # wave, group scales on the fp16 weights) under whole tiles and Stream-K
+    # splits with several contributors per tile, ragged row groups and
+    # several row groups per launch, grouped and per-channel scales.
+    force(spec)
+    assert mk.marlin_describe(M, N, K, g).startswith("w4a16_wide_kernel<"), mk.marlin_describe(M, N, K, g)
+    q, s = synth.weights(15, K, N, None if g == -1 else g)
+    A = synth.activations(15, M, K)
+    check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
+
+
 @pytest.mark.parametrize("waves", [4, 8])
-@pytest.mark.parametrize("nb", [1, 2, 4])
+@pytest.mark.parametrize("nb", [1, 2, 4, 8])
 @pytest.mark.parametrize("part", ["whole=1", "whole=0,grid=7", "whole=0,grid=96"])
 @pytest.mark.parametrize("M", [1, 6, 13, 20, 32, 70])
 @pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1)])
 def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
     # The stream kernel with four and with eight waves per work-group, every
-    # column-tile width and activation-row class (4, 8, 16, 32 rows in LDS;
+    # column-tile width (nb = 8: two packed 64-column tiles per wave) and
+    # activation-row class (4, 8, 16, 32 rows in LDS;
     # 70 rows: three row groups), whole tiles and Stream-K splits (7
     # work-groups: long ranges over several tiles; 96: several contributors
     # per tile), grouped and per-channel.  Eight waves with two row blocks

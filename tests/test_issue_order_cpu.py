@@ -3,7 +3,8 @@ operations issued after them (which complete in order): the stream and
 sparse kernels wait for a stage's activation rows while its weight and scale
 loads and D - 1 later stages may still be in flight; the tile kernel waits
 for a stage's activation and weight blocks while its scale loads and P - 2
-later stages may be.  That holds only if the compiler emits each stage's
+later stages may be; the wide kernel waits for a stage's activation rows and
+scales while its weight loads and P - 2 later stages may be.  That holds only if the compiler emits each stage's
 loads as one group, direct-to-LDS loads first, in issue order.  The compiler
 may interleave independent loads (it once moved a weight load between the
 activation loads of a stage, and reading rows before their load had landed
@@ -39,11 +40,12 @@ def assembly(tmp_path_factory):
         pytest.skip("hipcc not available")
     d = tmp_path_factory.mktemp("asm")
     procs = {}
-    for src in ("gemm", "tile"):
+    from paper_2408_11743_amd import build as B
+    for src in ("gemm", "tile", "wide"):
         out = str(d / (src + ".s"))
+        flags = B.SOURCE_FLAGS.get(src + ".hip", B.DEVICE_FLAGS)
         cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form=1",
-               "--cuda-device-only", "-S", "-o", out, os.path.join(CSRC, src + ".hip")]
+               *flags, "--cuda-device-only", "-S", "-o", out, os.path.join(CSRC, src + ".hip")]
         procs[src] = (subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE), out)
     text = {}
     for src, (pr, out) in procs.items():
@@ -54,13 +56,16 @@ def assembly(tmp_path_factory):
 
 
 def _kernels(text):
-    for m in re.finditer(r"^(_ZN6marlin\S*(w4a16_(?:stream|sparse|tile)_kernel)I((?:Li\d+E)+)Lb(\d)E\S*):", text, re.M):
+    for m in re.finditer(r"^(_ZN6marlin\S*(w4a16_(?:stream|sparse|tile|wide)_kernel)I((?:Li\d+E)+)Lb(\d)E\S*):", text, re.M):
         body = text[m.end():text.index(".Lfunc_end", m.end())]
         ints = [int(x) for x in re.findall(r"Li(\d+)E", m.group(3))]
         yield m.group(1), m.group(2), ints, m.group(4) == "1", body
 
 
 def _expected_group(kind, ints, per_channel):
+    if kind == "w4a16_wide_kernel":
+        MBW, NBW, P = ints
+        return "L" * (MBW + (0 if per_channel else 1)) + "R" * NBW
     if kind == "w4a16_tile_kernel":
         WN, WM, MBW, NBW, KS = ints
         NW, TR = WN * WM, 16 * MBW * WM
