@@ -8,7 +8,9 @@ batch sweep M = 1, 2, 4, 8, 16, 32, 64, 128.  One step = one GEMM at every
 copies per layer (1.09 GB per layer, beyond the 256 MB Infinity Cache).
 Packing is offline and not timed.  Launches are replayed from HIP graphs (one
 graph per step, 9 graphs rotating the weight copies) so the host does not
-throttle microsecond kernels.
+throttle microsecond kernels.  Before the W warm-up steps, the step graphs are
+replayed for 0.15 s (untimed) so that the shader clock has ramped up: a
+timed region of 20 steps lasts only about 11 ms.
 
 Output: one JSON line.  ``value`` = TFLOP/s of the whole timed region (sum of
 2MNK over the launches / elapsed).  Per (layer, M) of the headline: time per
@@ -59,6 +61,7 @@ ATTENTION = [(4096, 4096, 1, 128)]
 MLP_7B = [(4096, 11008, 2, 128), (11008, 4096, 2, 128), (4096, 11008, 2, -1), (11008, 4096, 2, -1)]
 ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies per layer (Infinity Cache is 256 MB)
 CPU_MS = [1, 16, 128]
+RAMP_S = 0.15  # untimed step replays before the warm-up steps (clock ramp)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a16_gemm_70b_layers_msweep_traffic.json")
 SECTIONS = ("attention_4096", "mlp_7b", "sparse_2of4", "prefill", "quantize")
 
@@ -708,11 +711,22 @@ def main():
     step_bytes = sum(R.w4a16_bytes(M, lay.N, lay.K, lay.g) for lay, M in cases)
     step_wbytes = sum(R.weight_bytes(lay.N, lay.K, lay.g) for lay, M in cases)
 
-    # ---- warm-up and timed region ----
+    # ---- clock ramp, warm-up and timed region ----
+    # The shader clock ramps up over tens of milliseconds of load, while the
+    # timed region of a short run lasts about ten: the step graphs are first
+    # replayed for RAMP_S seconds (untimed), then the W warm-up steps.
+    ramp_steps = 0
+    t_ramp = time.perf_counter()
     with torch.cuda.stream(stream):
+        while time.perf_counter() - t_ramp < RAMP_S:
+            for _ in range(8):
+                graphs[ramp_steps % ngraphs].replay()
+                ramp_steps += 1
+            stream.synchronize()
         for k in range(args.warmup):
             graphs[k % ngraphs].replay()
     torch.cuda.synchronize()
+    log("clock ramp: %d untimed steps in %.0f ms" % (ramp_steps, (time.perf_counter() - t_ramp) * 1e3))
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     with Range(torch, "timed steps"):
@@ -844,6 +858,7 @@ def main():
         "min_roof_frac_M_le_16": min(r["roof_frac"] for r in small),
         "per_m": per_m,
         "wall_ms_per_step": round(wall_ms / args.steps, 6),
+        "clock_ramp_steps": ramp_steps,
         "clock": clock_rec,
         "cpu_baseline": cpu,
         "parity": parity,

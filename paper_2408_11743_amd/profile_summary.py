@@ -35,9 +35,9 @@ import os
 import statistics
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-# Device sources the GEMM kernels are built from: a counter summary holds
-# for the kernels only while these are unchanged.
-KERNEL_SOURCES = ("gemm.hip", "tile.hip", "device.h", "internal.h")
+# Sources the GEMM kernels and their launch plans are built from: a counter
+# summary holds for the kernels only while these are unchanged.
+KERNEL_SOURCES = ("gemm.hip", "tile.hip", "wide.hip", "device.h", "internal.h", "plan.h", "plan.cpp")
 COPY_KERNEL = "copyBuffer"
 
 
