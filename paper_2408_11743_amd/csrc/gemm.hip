@@ -653,10 +653,31 @@ constexpr int stream_depth()
     return NB == 8 ? 2 : NB == 4 ? 3 : 4;
 }
 
+// 2:4 sparse stages carry 3/4 of the dense bytes per column block (NB = 4:
+// 3 KiB per wave, NB = 2: 1.5 KiB), in 3 or 2 loads; up to 16 rows the
+// ring is deeper than the dense one so that as many bytes are in flight.
+// Bounded by the vmcnt range at four activation loads per stage.
+template <int MB, int NB, int AR, int KW>
+constexpr int sparse_depth()
+{
+    if constexpr (MB == 1) {
+        constexpr int d = NB == 4 ? 5 : NB == 2 ? 8 : 7;
+        return KW == 8 ? (d + 1) / 2 : d;
+    }
+    return stream_depth<MB, NB, AR, KW>();
+}
+
+template <int MB, int NB, int AR, int KW>
+constexpr int ring_depth(bool sparse)
+{
+    return sparse ? sparse_depth<MB, NB, AR, KW>() : stream_depth<MB, NB, AR, KW>();
+}
+
 template <int MB, int NB, int AR, int KW>
 hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream)
 {
     constexpr int D = stream_depth<MB, NB, AR, KW>();
+    constexpr int DS = sparse_depth<MB, NB, AR, KW>();
     GemmProblem arg = p;
     void *args[] = {&arg};
     const bool pc = p.group_units == 0;
@@ -664,8 +685,8 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
                         : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, false>;
     if constexpr (NB <= 4) {  // the 2:4 layout has 64-column tiles at most
         if (cfg.sparse)
-            fn = pc ? (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, true>
-                    : (const void *)&w4a16_sparse_kernel<MB, NB, D, AR, KW, false>;
+            fn = pc ? (const void *)&w4a16_sparse_kernel<MB, NB, DS, AR, KW, true>
+                    : (const void *)&w4a16_sparse_kernel<MB, NB, DS, AR, KW, false>;
     } else if (cfg.sparse) {
         return hipErrorInvalidValue;
     }
@@ -684,35 +705,35 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
     }
     int d = 0;
     switch (cfg.waves * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
-    case 4111: d = stream_depth<1, 1, 1, 4>(); break;
-    case 4112: d = stream_depth<1, 1, 2, 4>(); break;
-    case 4114: d = stream_depth<1, 1, 4, 4>(); break;
-    case 4121: d = stream_depth<1, 2, 1, 4>(); break;
-    case 4122: d = stream_depth<1, 2, 2, 4>(); break;
-    case 4124: d = stream_depth<1, 2, 4, 4>(); break;
-    case 4141: d = stream_depth<1, 4, 1, 4>(); break;
-    case 4142: d = stream_depth<1, 4, 2, 4>(); break;
-    case 4144: d = stream_depth<1, 4, 4, 4>(); break;
-    case 4218: d = stream_depth<2, 1, 8, 4>(); break;
-    case 4228: d = stream_depth<2, 2, 8, 4>(); break;
-    case 4248: d = stream_depth<2, 4, 8, 4>(); break;
-    case 8111: d = stream_depth<1, 1, 1, 8>(); break;
-    case 8112: d = stream_depth<1, 1, 2, 8>(); break;
-    case 8114: d = stream_depth<1, 1, 4, 8>(); break;
-    case 8121: d = stream_depth<1, 2, 1, 8>(); break;
-    case 8122: d = stream_depth<1, 2, 2, 8>(); break;
-    case 8124: d = stream_depth<1, 2, 4, 8>(); break;
-    case 8141: d = stream_depth<1, 4, 1, 8>(); break;
-    case 8142: d = stream_depth<1, 4, 2, 8>(); break;
-    case 8144: d = stream_depth<1, 4, 4, 8>(); break;
-    case 8218: d = stream_depth<2, 1, 8, 8>(); break;
-    case 4181: d = stream_depth<1, 8, 1, 4>(); break;
-    case 4182: d = stream_depth<1, 8, 2, 4>(); break;
-    case 4184: d = stream_depth<1, 8, 4, 4>(); break;
-    case 4288: d = stream_depth<2, 8, 8, 4>(); break;
-    case 8181: d = stream_depth<1, 8, 1, 8>(); break;
-    case 8182: d = stream_depth<1, 8, 2, 8>(); break;
-    case 8184: d = stream_depth<1, 8, 4, 8>(); break;
+    case 4111: d = ring_depth<1, 1, 1, 4>(cfg.sparse); break;
+    case 4112: d = ring_depth<1, 1, 2, 4>(cfg.sparse); break;
+    case 4114: d = ring_depth<1, 1, 4, 4>(cfg.sparse); break;
+    case 4121: d = ring_depth<1, 2, 1, 4>(cfg.sparse); break;
+    case 4122: d = ring_depth<1, 2, 2, 4>(cfg.sparse); break;
+    case 4124: d = ring_depth<1, 2, 4, 4>(cfg.sparse); break;
+    case 4141: d = ring_depth<1, 4, 1, 4>(cfg.sparse); break;
+    case 4142: d = ring_depth<1, 4, 2, 4>(cfg.sparse); break;
+    case 4144: d = ring_depth<1, 4, 4, 4>(cfg.sparse); break;
+    case 4218: d = ring_depth<2, 1, 8, 4>(cfg.sparse); break;
+    case 4228: d = ring_depth<2, 2, 8, 4>(cfg.sparse); break;
+    case 4248: d = ring_depth<2, 4, 8, 4>(cfg.sparse); break;
+    case 8111: d = ring_depth<1, 1, 1, 8>(cfg.sparse); break;
+    case 8112: d = ring_depth<1, 1, 2, 8>(cfg.sparse); break;
+    case 8114: d = ring_depth<1, 1, 4, 8>(cfg.sparse); break;
+    case 8121: d = ring_depth<1, 2, 1, 8>(cfg.sparse); break;
+    case 8122: d = ring_depth<1, 2, 2, 8>(cfg.sparse); break;
+    case 8124: d = ring_depth<1, 2, 4, 8>(cfg.sparse); break;
+    case 8141: d = ring_depth<1, 4, 1, 8>(cfg.sparse); break;
+    case 8142: d = ring_depth<1, 4, 2, 8>(cfg.sparse); break;
+    case 8144: d = ring_depth<1, 4, 4, 8>(cfg.sparse); break;
+    case 8218: d = ring_depth<2, 1, 8, 8>(cfg.sparse); break;
+    case 4181: d = ring_depth<1, 8, 1, 4>(cfg.sparse); break;
+    case 4182: d = ring_depth<1, 8, 2, 4>(cfg.sparse); break;
+    case 4184: d = ring_depth<1, 8, 4, 4>(cfg.sparse); break;
+    case 4288: d = ring_depth<2, 8, 8, 4>(cfg.sparse); break;
+    case 8181: d = ring_depth<1, 8, 1, 8>(cfg.sparse); break;
+    case 8182: d = ring_depth<1, 8, 2, 8>(cfg.sparse); break;
+    case 8184: d = ring_depth<1, 8, 4, 8>(cfg.sparse); break;
     default: break;
     }
     if (d == 0) {

@@ -94,11 +94,12 @@ inline bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks)
 }
 
 // Tuning and test override of the configuration (the cost model is the
-// default): MARLIN_FORCE_CONFIG="nb=<1|2|4>,grid=<n>,whole=<0|1>,
-// kind=<stream|tile|wide>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>" forces the column-tile
-// width, the work-group count, the partition, the kernel, the stream kernel's
-// waves per work-group and the tile kernel's waves and blocks per stage where
-// the shape allows it.  Fields left out are free (0, or -1 for whole/kind).
+// default): MARLIN_FORCE_CONFIG="nb=<1|2|4|8>,grid=<n>,whole=<0|1>,
+// kind=<stream|tile|wide>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>" forces the
+// column-tile width, the work-group count, the partition, the kernel, the
+// stream kernel's waves per work-group and the tile kernel's waves and blocks
+// per stage, where the shape allows it.  Fields left out are free (0, or -1
+// for whole/kind).
 struct Override {
     int nb = 0;
     int grid = 0;
