@@ -66,6 +66,20 @@ __device__ __forceinline__ half8_t dequant_scaled(uint32_t x, half2_t s2, const 
     return half8_t{r0.x, r0.y, r1.x, r1.y, r2.x, r2.y, r3.x, r3.y};
 }
 
+// One quarter (codes 2q and 2q + 1) of dequant_scaled (SCALED), or of the
+// exact magic-number conversion alone (per-channel scales multiply the sums).
+template <bool SCALED>
+__device__ __forceinline__ half2_t convert_quarter(uint32_t x, int q, half2_t s2, const DequantConsts &k)
+{
+    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
+    const half2_t mul = {(_Float16)0.0625f, (_Float16)0.0625f};
+    const half2_t add = {(_Float16)-72.0f, (_Float16)-72.0f};
+    const uint32_t y = (q >> 1) ? x >> 8 : x;
+    const half2_t r = (q & 1) == 0 ? as_h2((y & k.lo) | k.ex) - sub
+                                   : __builtin_elementwise_fma(as_h2((y & k.hi) | k.ex), mul, add);
+    return SCALED ? r * s2 : r;
+}
+
 template <int MBW, int NBW, int P, bool PER_CHANNEL>
 __global__ void __launch_bounds__(256, 1) w4a16_wide_kernel(GemmProblem p)
 {
@@ -250,15 +264,26 @@ __global__ void __launch_bounds__(256, 1) w4a16_wide_kernel(GemmProblem p)
                 }
             }
             if (t < 3) read_a(t + 1, a[(t + 1) & 1]);
+            // Column block b's MFMAs are interleaved with the conversion of
+            // block b + 1's word, one quarter after every other MFMA: the
+            // conversion does not depend on the MFMAs, so the SIMD issues
+            // it while the matrix core works (the wave issues in order, so
+            // a run of MFMAs would hold back the conversion behind them).
+            half2_t nx[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) nx[q] = convert_quarter<!PER_CHANNEL>(wr[j][0][t], q, s2[0], dq);
 #pragma unroll
             for (int b = 0; b < NBW; ++b) {
-                half8_t w;
-                if constexpr (PER_CHANNEL)
-                    w = dequant_magic(wr[j][b][t], dq);
-                else
-                    w = dequant_scaled(wr[j][b][t], s2[b], dq);
+                const half8_t w = {nx[0].x, nx[0].y, nx[1].x, nx[1].y, nx[2].x, nx[2].y, nx[3].x, nx[3].y};
 #pragma unroll
-                for (int mb = 0; mb < MBW; ++mb) acc[b][mb] = mfma(w, __builtin_bit_cast(half8_t, cur[mb]), acc[b][mb]);
+                for (int mb = 0; mb < MBW; ++mb) {
+                    acc[b][mb] = mfma(w, __builtin_bit_cast(half8_t, cur[mb]), acc[b][mb]);
+                    constexpr int kStep = MBW / 4;  // MFMAs per quarter
+                    if (b + 1 < NBW && mb % kStep == 0)
+                        nx[mb / kStep] = convert_quarter<!PER_CHANNEL>(wr[j][b + 1][t], mb / kStep,
+                                                                       s2[PER_CHANNEL ? 0 : b + 1], dq);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
     };
