@@ -60,7 +60,7 @@ HEADLINE = [(8192, 28672, 3, 128), (28672, 8192, 3, 128)]
 ATTENTION = [(4096, 4096, 1, 128)]
 MLP_7B = [(4096, 11008, 2, 128), (11008, 4096, 2, 128), (4096, 11008, 2, -1), (11008, 4096, 2, -1)]
 ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies per layer (Infinity Cache is 256 MB)
-CPU_MS = [1, 16, 128]
+CPU_MS = [1, 16, 64, 128]
 RAMP_S = 0.15  # untimed step replays before the warm-up steps (clock ramp)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a16_gemm_70b_layers_msweep_traffic.json")
 SECTIONS = ("attention_4096", "mlp_7b", "sparse_2of4", "prefill", "quantize")
@@ -594,11 +594,11 @@ def run_section(name, args, mk, R, synth, torch, np, dev):
 
 
 def single_thread_oracle():
-    """The oracle on one thread (the 4096 x 4096 attention projection at
-    M = 1), in a child process started with OMP_NUM_THREADS=1."""
+    """The oracle on one thread (the 8192 x 28672 layer at M = 1), in a child
+    process started with OMP_NUM_THREADS=1."""
     code = ("import json, time, oracle, synth\n"
-            "q, s = synth.weights(1, 4096, 4096, 128)\n"
-            "A = synth.activations(1, 1, 4096)\n"
+            "q, s = synth.weights(3, 8192, 28672, 128)\n"
+            "A = synth.activations(3, 1, 8192)\n"
             "oracle.gemm(A, q, s, 128)\n"
             "ts = []\n"
             "for _ in range(3):\n"
@@ -609,8 +609,8 @@ def single_thread_oracle():
     if r.returncode != 0:
         return {"error": r.stderr[-300:]}
     dt = float(r.stdout.strip().splitlines()[-1])
-    return {"K": 4096, "N": 4096, "M": 1, "threads": 1, "seconds": round(dt, 4),
-            "value": round(2.0 * 4096 * 4096 / dt / 1e12, 6), "unit": "TFLOP/s"}
+    return {"K": 8192, "N": 28672, "M": 1, "threads": 1, "seconds": round(dt, 4),
+            "value": round(2.0 * 8192 * 28672 / dt / 1e12, 6), "unit": "TFLOP/s"}
 
 
 def main():

@@ -51,8 +51,8 @@ def kernel_sources_digest() -> str:
 
 def _one(pattern: str) -> str:
     files = sorted(glob.glob(pattern, recursive=True))
-    if not files:
-        raise SystemExit("no file matches %s" % pattern)
+    if len(files) != 1:  # none, or results of several runs in one directory
+        raise SystemExit("%d files match %s (one run per output directory)" % (len(files), pattern))
     return files[0]
 
 
