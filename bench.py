@@ -91,7 +91,8 @@ def parse():
     ap.add_argument("--profile-cases", type=int, default=0,
                     help="counter runs: launch every (layer, M) case of --profile-layers this many times "
                          "eagerly, in sweep order, print the case list and stop")
-    ap.add_argument("--profile-layers", choices=("headline", "attention_4096", "mlp_7b"), default="headline")
+    ap.add_argument("--profile-layers", choices=("headline", "attention_4096", "mlp_7b", "sparse_2of4"),
+                    default="headline")
     ap.add_argument("--calibration-copy-mb", type=int, default=0,
                     help="run plain device-to-device copies of this many MB first, so hardware byte "
                          "counters can be scaled against a known size")
@@ -172,19 +173,14 @@ def clocks(obj, path=""):
 t_end = time.time() + 900
 parent = os.getppid()
 with open(out, "a") as f:
-    first = True
     while not os.path.exists(stop) and time.time() < t_end and os.getppid() == parent:
         rec = {"t": time.time()}
         try:
             r = subprocess.run(["amd-smi", "metric", "-g", "0", "-c", "--json"], capture_output=True,
                                text=True, timeout=20)
-            vals = clocks(json.loads(r.stdout))
-            rec["mhz"] = vals
-            if first or not vals:
-                rec["raw"] = (r.stdout + r.stderr)[:3000]
+            rec["mhz"] = clocks(json.loads(r.stdout))
         except Exception as e:
             rec["error"] = "%s: %s" % (type(e).__name__, str(e)[:200])
-        first = False
         f.write(json.dumps(rec) + "\n")
         f.flush()
         time.sleep(1.0)
@@ -218,10 +214,6 @@ class ClockSampler:
             recs = [json.loads(l) for l in open(self.out) if l.strip()]
         except (OSError, ValueError):
             pass
-        raw = next((r.get("raw") for r in recs if r.get("raw")), None)
-        if raw is not None:
-            os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
-            open(os.path.join(ROOT, "gpurun_out", "amd_smi_clock_raw.txt"), "w").write(raw)
         if self.window:
             recs = [r for r in recs if self.window[0] <= r["t"] <= self.window[1]]
         s = sorted(round(sum(r["mhz"]) / len(r["mhz"]), 1) for r in recs if r.get("mhz"))
@@ -464,6 +456,35 @@ def sparse_section(args, mk, R, synth, torch, np, dev):
             "bound": "hbm", "per_m": rows, "cpu_baseline": cpu}
 
 
+def sparse_profile_cases(args, mk, synth, torch, dev):
+    """Counter runs of the 2:4 kernel (--profile-cases C --profile-layers
+    sparse_2of4): at each M of the sweep, C launches in a row on 8192 x 8192,
+    each on the next of two packed copies, in sweep order."""
+    K, N, g = SPARSE_K, SPARSE_N, GROUP
+    q, keep, s = synth.sparse24_weights(SPARSE_WID, K, N, g)
+    qd, sd = torch.from_numpy(q).to(dev), torch.from_numpy(s).to(dev)
+    L = mk.lib()
+    wp, sp = mk.pack(qd, sd, group=g, sparse=True)
+    wps = [wp, wp.clone()]
+    ws = mk.Workspace(dev)
+    wsbuf = ws.ensure(max(mk.marlin_workspace_bytes(M, N, K, g) for M in M_SWEEP))
+    stream = torch.cuda.Stream(device=dev)
+    cases = []
+    with torch.cuda.stream(stream):
+        for M in M_SWEEP:
+            A = torch.from_numpy(synth.activations(SPARSE_WID, M, K)).to(dev)
+            C = torch.empty((M, N), dtype=torch.float16, device=dev)
+            for i in range(args.profile_cases):
+                st = L.marlin_gemm_sparse(A.data_ptr(), wps[i % 2].data_ptr(), sp.data_ptr(), C.data_ptr(),
+                                          wsbuf.data_ptr(), wsbuf.numel(), M, N, K, g, stream.cuda_stream)
+                if st != 0:
+                    raise mk.MarlinError("marlin_gemm_sparse", st)
+            cases.append({"K": K, "N": N, "group": g, "M": M, "sparse": True,
+                          "launch": mk.marlin_describe_sparse(M, N, K, g)})
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_cases": args.profile_cases, "layers": "sparse_2of4", "cases": cases}), flush=True)
+
+
 def prefill_section(args, mk, R, synth, torch, np, dev):
     """Large batches in one launch (Section 3.4, Striped Partitioning, on
     batches well above 64): the Llama-7B attention projection and the
@@ -648,6 +669,9 @@ def main():
         del src, dst
     if args.only:
         print(json.dumps({args.only: run_section(args.only, args, mk, R, synth, torch, np, dev)}), flush=True)
+        return
+    if args.profile_cases and args.profile_layers == "sparse_2of4":
+        sparse_profile_cases(args, mk, synth, torch, dev)
         return
 
     # ---- headline layers: pack once, replicate to >= 1 GiB per layer ----

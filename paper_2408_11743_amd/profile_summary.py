@@ -440,7 +440,8 @@ def case_traffic_summary(a, bench: dict) -> None:
         raise SystemExit("no calibration copies in the counter runs (--calibration-copy-mb)")
     f_scale = copy_bytes / (statistics.median(cf) * 1024.0)
     w_scale = copy_bytes / (statistics.median(cw) * 1024.0)
-    md = ["# HBM traffic: W4A16 GEMM, %s layers, M sweep (rocprofv3 counters)" % bench["layers"], "",
+    md = ["# HBM traffic: %s W4A16 GEMM, %s layers, M sweep (rocprofv3 counters)" % (
+              "2:4 sparse" if any(c.get("sparse") for c in cases) else "dense", bench["layers"]), "",
           "Commands (two counter passes, each its own run, `TMPDIR=/tmp`; every case launched",
           "%d times in a row, each launch on the next weight copy):" % C, "", "```",
           a.fetch_cmd, a.write_cmd, "```", "",
@@ -455,15 +456,18 @@ def case_traffic_summary(a, bench: dict) -> None:
     for c, f, w in zip(cases, gf, gw):
         fb = statistics.median(d["FETCH_SIZE"] for d in f) * 1024.0 * f_scale
         wb = statistics.median(d["WRITE_SIZE"] for d in w) * 1024.0 * w_scale
-        alg = R.w4a16_bytes(c["M"], c["N"], c["K"], c["group"])
+        alg = (R.sparse24_bytes if c.get("sparse") else R.w4a16_bytes)(c["M"], c["N"], c["K"], c["group"])
         md.append("| %d | %d | %s | %d | `%s` | %.2f | %.2f | %.2f | %.2f | %.3f |" % (
             c["K"], c["N"], "K" if c["group"] == -1 else c["group"], c["M"], f[0]["name"], fb / 1e6, wb / 1e6,
             (fb + wb) / 1e6, alg / 1e6, (fb + wb) / alg))
         hbm["K=%d N=%d g=%d M=%d" % (c["K"], c["N"], c["group"], c["M"])] = round(fb + wb)
         tot += fb + wb
     digest = kernel_sources_digest()
-    md += ["", "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N.", "",
-           "Average per launch over the cases: %.2f MB (bench.py reports it as `roofline.traffic`" %
+    md += ["", "Algorithmic bytes: K*N/2 + 2*(K/g)*N + 2*M*K + 2*M*N%s." % (
+               " (2:4 sparse: K*N/4 of kept codes and K*N/8 of row indices in place of K*N/2)"
+               if any(c.get("sparse") for c in cases) else ""), "",
+           ("Average per launch over the cases: %.2f MB (measured" if any(c.get("sparse") for c in cases) else
+            "Average per launch over the cases: %.2f MB (bench.py reports it as `roofline.traffic`") %
            (tot / len(cases) / 1e6),
            "while the kernel sources (%s under `paper_2408_11743_amd/csrc/`) hash to `%s...`)." %
            (", ".join(KERNEL_SOURCES), digest[:16]), ""]
