@@ -243,7 +243,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_wide_kernel(GemmProblem p)
                              : "v"(a_rd[t] + (uint32_t)(j * kStage)), "i"(mb * 4096));
         };
         read_a(0, a[0]);
-        half2_t s2[PER_CHANNEL ? 1 : NBW];
+        half2_t s2[NBW] = {};  // group scales (unused with per-channel scales)
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             u32x4_t(&cur)[MBW] = a[t & 1];
@@ -281,7 +281,7 @@ __global__ void __launch_bounds__(256, 1) w4a16_wide_kernel(GemmProblem p)
                     constexpr int kStep = MBW / 4;  // MFMAs per quarter
                     if (b + 1 < NBW && mb % kStep == 0)
                         nx[mb / kStep] = convert_quarter<!PER_CHANNEL>(wr[j][b + 1][t], mb / kStep,
-                                                                       s2[PER_CHANNEL ? 0 : b + 1], dq);
+                                                                       s2[b + 1], dq);
                     __builtin_amdgcn_sched_barrier(0);
                 }
             }
