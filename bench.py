@@ -874,8 +874,9 @@ def main():
                      "traffic_unit": "HBM bytes per launch (step average)",
                      "algorithmic_bytes_per_launch": round(step_bytes / len(cases)),
                      "avg_launch_us": round(avg_launch_us, 3),
-                     "kernel": "w4a16_stream_kernel (M <= 32) and w4a16_tile_kernel (M = 64, 128): every "
-                               "launch of the step",
+                     "kernel": "; ".join("%s at %s" % (k, ", ".join("%dx%d M=%d" % (r["K"], r["N"], r["M"])
+                                                                   for r in per_m if r["launch"].startswith(k + "<")))
+                                         for k in by_kernel) + ": every launch of the step",
                      "by_kernel": by_kernel},
         "roof_frac_step": round(sum(R.w4a16_t_roof(M, lay_n, lay_k, GROUP) for lay_k, lay_n, _, _ in HEADLINE
                                     for M in M_SWEEP) / (ms_per_step * 1e-3), 4),
