@@ -58,6 +58,14 @@ __device__ __forceinline__ half8_t dequant_sub(uint32_t x)
                                                y & 0x00F000F0u});
 }
 
+// Eight fp16 weights times one scale (in both halves of s2), one rounding each.
+__device__ __forceinline__ half8_t scale_pairs(half8_t w, half2_t s2)
+{
+    const u32x4_t u = __builtin_bit_cast(u32x4_t, w);
+    return __builtin_bit_cast(half8_t, u32x4_t{as_u32(as_h2(u[0]) * s2), as_u32(as_h2(u[1]) * s2),
+                                               as_u32(as_h2(u[2]) * s2), as_u32(as_h2(u[3]) * s2)});
+}
+
 // Activation operand matching dequant_sub: elements 2, 3, 6, 7 times 1/16.
 __device__ __forceinline__ half8_t prescale(half8_t a)
 {
@@ -126,25 +134,29 @@ __device__ __forceinline__ float4_t smfmac2(half8_t w0, half8_t w1, const half8_
 // Register-streaming kernel.
 //
 // A work-group owns a column tile of 16*NB columns (NB 16-column blocks; NB = 8
-// spans two 64-column tiles of the packed layout) over
-// a range of 128-row blocks of K (the striped partition); its KW waves take
-// consecutive 128-row blocks of each stage (waves split K), so no weight or
-// activation byte is shared between waves: each lane loads exactly its MFMA
-// operands (16-byte non-temporal buffer loads of the pre-shuffled weights,
-// 16-byte loads of activation rows, which hit L2) straight into a D-deep ring
-// of registers.  The loop is unrolled over the ring so register slots are
-// static and the compiler's vmcnt waits keep D-1 stages in flight while one
-// is computed.  A wave whose block lies past the end of a segment loads
-// through an empty buffer descriptor (no memory is touched, zeros return) and
-// skips the stage's arithmetic.
+// spans two 64-column tiles of the packed layout) of one row group (16*MB
+// rows: MB = 1, 2, or 4 with 128-column dense tiles) over a range of 128-row
+// blocks of K (the striped partition); its KW waves take consecutive 128-row
+// blocks of each stage (waves split K), so no weight or activation byte is
+// shared between waves: each lane loads exactly its MFMA weight operands
+// (16-byte non-temporal buffer loads of the pre-shuffled weights) into a
+// D-deep ring of registers, and the stage's activation rows (which hit L2)
+// arrive by direct-to-LDS loads in a D-deep per-wave LDS ring.  The loop is
+// unrolled over the ring so register slots are static and the vmcnt waits
+// keep D-1 stages in flight while one is computed.  A wave whose block lies
+// past the end of a segment loads through an empty buffer descriptor (no
+// memory is touched, zeros return) and skips the stage's arithmetic.
+//
+// Codes become MFMA operands as subnormal fp16 numbers with a separate
+// zero-point product and the group scale applied to each 128-row fp32
+// partial product (MB <= 2), or, with four row blocks, by the magic number
+// with the group scale on the fp16 weights: that path touches no fp32 value
+// per stage, so its 128 accumulators stay with the matrix cores.
 //
 // Cross-work-group combination, at the end: the work-group's first tile (if
-// shared) was written to slot 0 when its segment ended; it now bumps that
-// tile's counter.  Its last tile (if shared) stays in registers: the counter
-// is read first, and if every other contributor has arrived (the usual case:
-// they processed that tile at the start of their ranges) the work-group adds
-// their slots to its registers and writes C at once; otherwise it writes slot
-// 1 and arrives like the others.
+// shared) was written to slot 0 when its segment ended; its last tile (if
+// shared) is written to slot 1 now; it then arrives at both tiles' counters,
+// and whoever completes a count sums the slots (device.h, combine_tiles).
 //
 // 2:4 sparse weights (SPARSE, Section 4): the same schedule with the sparse
 // packed layout (per 64 x 128 unit: 2 KiB of kept codes, 1 KiB of 2-bit row
@@ -167,7 +179,10 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     // indices (sparse: 2 + 1 for NB = 4, else 1 + 1)
     constexpr int kWL = SPARSE ? (NB == 4 ? 3 : 2) : NB;
     constexpr uint32_t kUnitBytes = SPARSE ? 3072u : 4096u;  // per 64 x 128 unit
-    constexpr float kOutScale = SPARSE ? 1.0f : kTwo24;      // dense operands carry 2^-24
+    // Four row blocks (dense) convert codes with the magic number too (exact
+    // q - 8, group scales on the fp16 weights; see compute)
+    constexpr bool kMagic = SPARSE || MB == 4;
+    constexpr float kOutScale = kMagic ? 1.0f : kTwo24;      // subnormal operands carry 2^-24
     // Activation rows through LDS (one or two 16-row blocks): the 4*AR rows of
     // the tile's row group for the stage's 128-row block land in a per-wave
     // LDS ring by AR direct-to-LDS loads (only real rows are fetched; the
@@ -176,9 +191,14 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     constexpr int kAStage = kARows * 256;            // bytes per wave and stage
     constexpr int kLoads = AR + kWL + kSL;           // vector-memory ops per stage
     static_assert(KW == 4 || (KW == 8 && (MB == 1 || NB == 1)), "four waves, or eight with one row block or column block");
-    static_assert(MB <= 2 && AR >= 1 && kARows <= 16 * MB, "one or two row blocks, at least 4 rows");
+    static_assert(MB <= 2 || (MB == 4 && NB == 8 && KW == 4 && !SPARSE),
+                  "one or two row blocks; four only with 128-column dense tiles and four waves");
+    static_assert(AR >= 1 && kARows <= 16 * MB, "at least 4 rows");
     static_assert((D - 1) * kLoads + kWL + kSL < 64, "vmcnt range");
-    __shared__ float4_t red[KW * kBlocks * 64];
+    // The waves' tiles meet in LDS: in a buffer of their own up to two row
+    // blocks; with four (64 x 128 per wave, 32 KiB of fp32, beside a 128 KiB
+    // activation ring) in the ring slot of the stage that ends the segment.
+    __shared__ float4_t red[MB == 4 ? 1 : KW * kBlocks * 64];
     __shared__ __attribute__((aligned(16))) uint8_t a_lds[KW * D * kAStage + 256];
     __shared__ int flags[2];
 
@@ -195,8 +215,8 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     const int k0 = u0 - c_first * KU;  // first block in the first tile
     const int k1 = u1 - c_last * KU;   // end block in the last tile (1..KU)
 
-    // A tile c is column tile c / rg and row group c % rg (rows 32*(c % rg)
-    // onwards when M exceeds 32; one group otherwise).  Byte offsets of tile
+    // A tile c is column tile c / rg and row group c % rg (rows 16*MB*(c % rg)
+    // onwards when M exceeds 16*MB; one group otherwise).  Byte offsets of tile
     // c's block 0: weights (4 KiB per (64 columns x 128 rows) block, 1 KiB per
     // 16 columns; sparse: 3 KiB per block, this column block's codes at
     // 1 KiB * (q/2) + 8 * (q%2) for column block q of the 64) and scale rows
@@ -220,7 +240,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
         return (((nbg >> 2) * (uint32_t)p.G) << 7) + (nbg & 3u) * 8u;
     };
     // First row of tile c's row group, and the rows it has (1 .. 16*MB).
-    auto row0_of = [&](int c) -> int { return RG == 1 ? 0 : (int)((uint32_t)c - col_of(c) * RG) * 32; };
+    auto row0_of = [&](int c) -> int { return RG == 1 ? 0 : (int)((uint32_t)c - col_of(c) * RG) * (16 * MB); };
     auto rows_of = [&](int c) -> int {
         const int r = p.M - row0_of(c);
         return r < 16 * MB ? r : 16 * MB;
@@ -228,20 +248,33 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
 
     // Per-lane parts of the load addresses (fixed for the whole kernel).
     const uint32_t w_lane = (uint32_t)kw * kUnitBytes + (uint32_t)lane * 16u;
-    const uint32_t s_lane = (uint32_t)lg * 32u;
+    // Scale runs: lane group g of the packed 128-byte row holds, for each
+    // 16-column block, the scales of columns 4g .. 4g + 3 (the accumulator
+    // columns of lanes 16g .. 16g + 15, which the subnormal path scales); the
+    // magic path scales the weight operand, whose column is lane % 16, so a
+    // lane loads run (lane % 16) / 4 and keeps element lane % 4 of it.
+    const uint32_t s_lane = (MB == 4 ? (uint32_t)((lane & 15) >> 2) : (uint32_t)lg) * 32u;
+    const uint32_t s_sel = 0x01000100u + (uint32_t)(lane & 3) * 0x02020202u;  // v_perm: that half, twice
+    (void)s_sel;
     // Direct-to-LDS activation loads: load i, lane l fetches row r = 4i + l/16,
     // 16-byte chunk (l % 16) ^ r of the block (an XOR swizzle, so that the
     // MFMA-operand reads of 16 rows hit 16 different bank groups).
     // The MFMA operands are read back with ds_read_b128 at per-lane LDS
     // addresses fixed for each ring slot; lanes of rows past the 4*AR loaded
     // ones read a zero row (the 256 bytes after the ring) instead.
-    uint32_t a_dma[AR];
-    uint32_t a_rd[D][MB][4];
+    // Four row blocks: rows r and r + 16 share the swizzle, so loads i >= 4
+    // add 16 rows to the offset of load i % 4 when they are issued, and the
+    // operand reads take the ring slot and row block as instruction offsets
+    // from one address per k-step (fewer registers held across the loop).
+    constexpr int kADma = MB == 4 ? 4 : AR;
+    uint32_t a_dma[kADma];
+    uint32_t a_rd[MB == 4 ? 1 : D][MB == 4 ? 1 : MB][4];
 #pragma unroll
-    for (int i = 0; i < AR; ++i) {
+    for (int i = 0; i < kADma; ++i) {
         const int r = 4 * i + lg;
         a_dma[i] = (uint32_t)(r * p.K + (((lane & 15) ^ (r & 15)) * 8)) * 2u + (uint32_t)kw * 256u;
     }
+    const uint32_t a_rows16 = (uint32_t)p.K * 32u;  // 16 rows of A, bytes
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)a_lds;
     const uint32_t zero_row = lds0 + KW * D * kAStage;
     const uint32_t lds_wave = lds0 + (uint32_t)(kw * D * kAStage);  // this wave's ring
@@ -281,11 +314,17 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             uint32_t slot = lds_wave;
             asm volatile("" : "+s"(slot));
             slot += (uint32_t)(j * kAStage);
+            uint32_t dma[kADma];
+#pragma unroll
+            for (int i = 0; i < kADma; ++i) {
+                dma[i] = a_dma[i];
+                if constexpr (MB == 4) asm volatile("" : "+v"(dma[i]));  // formed per stage, not held
+            }
 #pragma unroll
             for (int i = 0; i < AR; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(
                     rd, (__attribute__((address_space(3))) void *)(uintptr_t)(slot + (uint32_t)(i * 1024)), 16,
-                    (int)a_dma[i], ld_ku * 256, 0, 0);
+                    (int)(dma[i % kADma] + (uint32_t)(i / kADma) * a_rows16), ld_ku * 256, 0, 0);
         }
         issue_order_point();  // the rows are the stage's oldest loads
         const __amdgpu_buffer_rsrc_t rw =
@@ -355,9 +394,9 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
                          : "memory");
     }
 #pragma unroll
-    for (int j = 0; j < D; ++j)
+    for (int j = 0; j < (MB == 4 ? 1 : D); ++j)
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+        for (int mb = 0; mb < (MB == 4 ? 1 : MB); ++mb)
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int am = mb * 16 + (lane & 15);
@@ -409,12 +448,23 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    asm volatile("ds_read_b128 %0, %1" : "=v"(v[mb * 4 + t]) : "v"(a_rd[j][mb][t]));
+                for (int t = 0; t < 4; ++t) {
+                    if constexpr (MB == 4)  // slot j, row block mb: 16 KiB and 4 KiB from the k-step's address
+                        asm volatile("ds_read_b128 %0, %1 offset:%2"
+                                     : "=v"(v[mb * 4 + t])
+                                     : "v"(a_rd[0][0][t]), "i"(j * kAStage + mb * 4096));
+                    else
+                        asm volatile("ds_read_b128 %0, %1" : "=v"(v[mb * 4 + t]) : "v"(a_rd[j][mb][t]));
+                }
             // The wait "redefines" the results, so no use of them can be
             // scheduled before the data has arrived.
             if constexpr (MB == 1) {
                 asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])::"memory");
+            } else if constexpr (MB == 4) {
+                asm volatile("s_waitcnt lgkmcnt(0)"
+                             : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
+                               "+v"(v[7]), "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]),
+                               "+v"(v[13]), "+v"(v[14]), "+v"(v[15])::"memory");
             } else {
                 asm volatile("s_waitcnt lgkmcnt(0)"
                              : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
@@ -422,9 +472,34 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             }
 #pragma unroll
             for (int i = 0; i < 4 * MB; ++i)
-                a[i] = SPARSE ? __builtin_bit_cast(half8_t, v[i]) : prescale(__builtin_bit_cast(half8_t, v[i]));
+                a[i] = kMagic ? __builtin_bit_cast(half8_t, v[i]) : prescale(__builtin_bit_cast(half8_t, v[i]));
         }
-        if constexpr (SPARSE) {
+        if constexpr (MB == 4) {
+            // Four row blocks: q - 8 exactly by the magic number, times the
+            // group scale in fp16 (one rounding per weight, the scale applied
+            // to the weights before the product: Section 3.4, "Groups and
+            // Instruction Ordering"), straight into the MFMA chains, which
+            // run over the whole segment; each converted weight feeds four
+            // MFMAs and no fp32 value is touched per stage.
+            half2_t s2[NB];
+            if constexpr (!PER_CHANNEL) {
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    const u32x4_t v = __builtin_bit_cast(u32x4_t, sr[j][b >> 1]);
+                    s2[b] = as_h2(__builtin_amdgcn_perm(v[2 * (b & 1) + 1], v[2 * (b & 1)], s_sel));
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    half8_t w = dequant_magic(wr[j][b][t], dq);
+                    if constexpr (!PER_CHANNEL) w = scale_pairs(w, s2[b]);
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) acc[b][mb] = mfma(w, a[mb * 4 + t], acc[b][mb]);
+                }
+            }
+        } else if constexpr (SPARSE) {
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const half8_t w0 = dequant_magic(sw[j].code(b, 0), dq);
@@ -537,8 +612,8 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     // A segment is complete: sum the waves' tiles in LDS, then write C
     // (whole column), keep the sum (shared last tile) or write slot 0
     // (shared first tile).
-    auto finish_segment = [&]() {
-        if constexpr (PER_CHANNEL && !SPARSE) {
+    auto finish_segment = [&](int j) {
+        if constexpr (PER_CHANNEL && !kMagic) {
 #pragma unroll
             for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -547,24 +622,52 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             for (int mb = 0; mb < MB; ++mb) bacc[mb] = zero4;
         }
         float4_t out[kOwn];
+        if constexpr (MB != 4) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
+            for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) red[(kw * kBlocks + b * MB + mb) * 64 + lane] = acc[b][mb];
-        lds_barrier();
+                for (int mb = 0; mb < MB; ++mb) red[(kw * kBlocks + b * MB + mb) * 64 + lane] = acc[b][mb];
+            lds_barrier();
 #pragma unroll
-        for (int j = 0; j < kOwn; ++j) {
-            const int blk = own(j);
-            if (blk < kBlocks) {
-                float4_t s = red[blk * 64 + lane];
+            for (int j = 0; j < kOwn; ++j) {
+                const int blk = own(j);
+                if (blk < kBlocks) {
+                    float4_t s = red[blk * 64 + lane];
 #pragma unroll
-                for (int k2 = 1; k2 < KW; ++k2) s += red[(k2 * kBlocks + blk) * 64 + lane];
-                out[j] = s;
-            } else {
-                out[j] = zero4;
+                    for (int k2 = 1; k2 < KW; ++k2) s += red[(k2 * kBlocks + blk) * 64 + lane];
+                    out[j] = s;
+                } else {
+                    out[j] = zero4;
+                }
+            }
+            lds_barrier();
+        } else {
+            // Every wave's ring slot j is free: the wave has read its rows
+            // (its later stages land in the other slot), and the stage's
+            // refill is issued after the last barrier here.  Two rounds of
+            // four column blocks, 16 KiB per wave: wave w keeps row block w
+            // (MB == KW), i.e. block own(b) of column block b.
+            const auto slot_of_wave = [&](int w) {
+                return reinterpret_cast<float4_t *>(a_lds + (w * D + j) * kAStage);
+            };
+            float4_t *const mine = slot_of_wave(kw);
+#pragma unroll
+            for (int h = 0; h < NB; h += 4) {
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) mine[(b * MB + mb) * 64 + lane] = acc[h + b][mb];
+                lds_barrier();
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    float4_t s = slot_of_wave(0)[(b * MB + kw) * 64 + lane];
+#pragma unroll
+                    for (int k2 = 1; k2 < KW; ++k2) s += slot_of_wave(k2)[(b * MB + kw) * 64 + lane];
+                    out[h + b] = s;
+                }
+                lds_barrier();
             }
         }
-        lds_barrier();
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -589,11 +692,15 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
         if (st < n_st) {
             if (cp_ku + kw < cp_end) compute(j, later);
             if (cp_ku + KW >= cp_end) {
-                finish_segment();
-                cp_c += 1;
-                cp_ku = 0;
-                cp_begin = 0;
-                cp_end = (cp_c < c_last) ? KU : k1;
+                // four row blocks: the last segment is closed after the loop,
+                // so that no sum is held across it
+                if (MB != 4 || cp_c != c_last) {
+                    finish_segment(j);
+                    cp_c += 1;
+                    cp_ku = 0;
+                    cp_begin = 0;
+                    cp_end = (cp_c < c_last) ? KU : k1;
+                }
             } else {
                 cp_ku += KW;
             }
@@ -615,6 +722,12 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) step(j, st_last + j, D - 1 - j);
+    if constexpr (MB == 4) {
+        // Stages past the range were issued (through empty descriptors) but
+        // never waited for: drain them before the ring is reused.
+        wait_vmcnt<0>();
+        finish_segment(0);
+    }
 
     // ---- combination of shared tiles ----
     auto own_slot = [&](int j) { return own(j) < kBlocks ? own(j) : -1; };
@@ -648,8 +761,8 @@ constexpr int stream_depth()
         return KW == 8 ? (d + 1) / 2 : d;
     }
     // LDS ring of 32 rows: 8 KiB per wave-stage (eight waves: 16-column
-    // tiles only, two stages, 128 KiB)
-    if constexpr (KW == 8) return 2;
+    // tiles only, two stages, 128 KiB); of 64 rows: 16 KiB, two stages
+    if constexpr (KW == 8 || MB == 4) return 2;
     return NB == 8 ? 2 : NB == 4 ? 3 : 4;
 }
 
@@ -734,6 +847,7 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
     case 8181: d = ring_depth<1, 8, 1, 8>(cfg.sparse); break;
     case 8182: d = ring_depth<1, 8, 2, 8>(cfg.sparse); break;
     case 8184: d = ring_depth<1, 8, 4, 8>(cfg.sparse); break;
+    case 4496: d = ring_depth<4, 8, 16, 4>(cfg.sparse); break;
     default: break;
     }
     if (d == 0) {
@@ -778,6 +892,7 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
     case 8181: return launch_stream<1, 8, 1, 8>(cfg, p, stream);
     case 8182: return launch_stream<1, 8, 2, 8>(cfg, p, stream);
     case 8184: return launch_stream<1, 8, 4, 8>(cfg, p, stream);
+    case 4496: return launch_stream<4, 8, 16, 4>(cfg, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -34,6 +34,9 @@ Override parse_override(const char *e)
     q = strstr(e, "waves=");
     if (q) f.waves = atoi(q + 6);
     if (f.waves != 4 && f.waves != 8) f.waves = 0;
+    q = strstr(e, "mb=");
+    if (q) f.mb = atoi(q + 3);
+    if (f.mb != 1 && f.mb != 2 && f.mb != 4) f.mb = 0;
     if (f.nb != 1 && f.nb != 2 && f.nb != 4 && f.nb != 8) f.nb = 0;
     if (f.grid < 0) f.grid = 0;
     return f;
@@ -71,11 +74,12 @@ size_t workspace_bytes_for(const GemmConfig &cfg)
 
 size_t workspace_bytes_used(const GemmConfig &cfg) { return cfg.whole ? 0 : workspace_bytes_for(cfg); }
 
-// Configuration by rows of A per pass (at most kPassRows): mb = 1 (M <= 16)
-// or 2 16-row blocks per row group; beyond 32 rows the pass is split into row
-// groups of 32 that are tiles of their own (a tile is a column tile of one
-// row group); 4 * ar activation rows per group arrive in LDS; 4 or (one row
-// block, or one column block) 8 waves split K, kStreamOcc work-groups per CU.
+// Configuration by rows of A per pass (at most kPassRows): mb = 1 (M <= 16),
+// 2 or (dense, beyond 32 rows) 4 16-row blocks per row group; beyond one
+// group's rows the pass is split into row groups that are tiles of their own
+// (a tile is a column tile of one row group); 4 * ar activation rows per
+// group arrive in LDS; 4 or (one row block, or one column block) 8 waves
+// split K, kStreamOcc work-groups per CU.
 //
 // Column tile width (nb 16-column blocks), waves and partition come from a
 // cost model fitted to MI355X measurements (218 whole-tile timings over the
@@ -115,6 +119,15 @@ constexpr double kChipBytesPerUs = 7.0e6;
 double stream_tail_us(int slot_kib) { return slot_kib > 4 ? 4.5 : 3.0; }
 constexpr double kStreamFreeContributors = 4.0;
 constexpr double kStreamTailPerExtraContributorUs = 0.45;
+// Four row blocks per wave (64 x 128 per wave, 32 KiB fp32 partial tiles):
+// weight bytes per microsecond one work-group streams (its waves convert
+// and multiply twice as much per weight byte as with two row blocks, with no
+// second wave per SIMD to overlap the two: measured 49 us for whole tiles
+// on 8192 x 28672 at 33..64 rows), and the combination (fixed, and per
+// contributor: the reducer reads one 32 KiB slot each).
+constexpr double kRate64Rows = 11.65e3;
+constexpr double kTail64RowsUs = 4.0;
+constexpr double kTail64RowsPerContributorUs = 1.0;
 
 // Bytes of weights per microsecond one work-group streams, by rows of A,
 // nb = 8, 4, 2, 1 and waves per work-group (measured; the activation rows
@@ -204,36 +217,52 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
     cfg.tile_nw = 0;
     cfg.waves = 4;
     cfg.sparse = sparse ? 1 : 0;
-    cfg.mb = (M <= 16) ? 1 : 2;
+    // Rows per row group: 16 (M <= 16), 32, or (dense, beyond 32 rows, or
+    // forced) 64 in four row blocks per wave, which read each weight once for
+    // twice the rows and take their activations in 16 KiB stages.
+    const int mb_small = (M <= 16) ? 1 : 2;
+    const bool mb4_ok = !sparse && (M > 32 || ov.mb == 4);
+    cfg.mb = mb_small;
     cfg.ar = (M <= 4) ? 1 : (M <= 8) ? 2 : (M <= 16) ? 4 : 8;
-    cfg.rg = (M + 31) / 32;  // row groups of 32 beyond M = 32, each a copy of the column tiles
-    if (cfg.rg < 1) cfg.rg = 1;
+    cfg.rg = (M + 16 * cfg.mb - 1) / (16 * cfg.mb);  // row groups, each a copy of the column tiles
     double best = 1e30;
     cfg.nb = 0;
     cfg.whole = 0;
     int64_t best_grid = grid;
-    if (ov.kind != kKindTile && ov.kind != kKindWide) {
+    for (int mb : {mb_small, 4}) {
+        if (ov.kind == kKindTile || ov.kind == kKindWide) break;
+        if (mb == 4 && !mb4_ok) continue;
+        if (ov.mb && mb != ov.mb && (ov.mb == 4 ? mb4_ok : ov.mb == mb_small)) continue;
+        const int ar = mb == 4 ? 16 : cfg.ar;
+        const int64_t rg = (M + 16 * mb - 1) / (16 * mb);
         // eight waves exist for one 16-row block, or two with one 16-column
         // block; an override to eight applies where they do
-        const int forced_waves = (ov.waves == 8 && cfg.mb != 1 && ov.nb > 1) ? 4 : ov.waves;
+        const int forced_waves = (ov.waves == 8 && mb != 1 && ov.nb > 1) ? 4 : ov.waves;
         for (int waves = 8; waves >= 4; waves -= 4) {
             if (forced_waves && waves != forced_waves) continue;
             for (int nb = sparse ? 4 : 8; nb >= 1; nb >>= 1) {
-                const double rate = wg_rate(cfg.mb, cfg.ar, nb, waves);
+                if (mb == 4 && (nb != 8 || waves != 4)) continue;  // the one four-row-block kernel
+                const double rate = mb == 4 ? kRate64Rows : wg_rate(mb, ar, nb, waves);
                 if (tiles16 % nb != 0 || rate <= 0.0) continue;
                 if (ov.nb && nb != ov.nb) continue;
-                const int64_t tiles = (int64_t)(tiles16 / nb) * cfg.rg;
+                const int64_t tiles = (int64_t)(tiles16 / nb) * rg;
                 // sparse units carry 3/4 of the dense bytes (codes and row indices)
                 const double unit_bytes = (double)nb * (sparse ? 768.0 : 1024.0);
                 const double layer_bytes = (double)KU * (double)(tiles16 / nb) * unit_bytes;
                 // fp32 partial tile: 16 x 16 x 4 bytes per block, two slots
-                const size_t slot_bytes = (size_t)2 * nb * cfg.mb * 256 * sizeof(float);
-                const Partition pt = best_partition(ov, tiles, KU, grid, unit_bytes / rate,
-                                                    stream_tail_us(nb * cfg.mb), 0.0,
-                                                    layer_bytes / kChipBytesPerUs, slot_bytes, partial_budget,
-                                                    kStreamFreeContributors, kStreamTailPerExtraContributorUs);
+                const size_t slot_bytes = (size_t)2 * nb * mb * 256 * sizeof(float);
+                const Partition pt =
+                    mb == 4 ? best_partition(ov, tiles, KU, grid, unit_bytes / rate, kTail64RowsUs,
+                                             kTail64RowsPerContributorUs, layer_bytes / kChipBytesPerUs, slot_bytes,
+                                             partial_budget)
+                            : best_partition(ov, tiles, KU, grid, unit_bytes / rate, stream_tail_us(nb * mb), 0.0,
+                                             layer_bytes / kChipBytesPerUs, slot_bytes, partial_budget,
+                                             kStreamFreeContributors, kStreamTailPerExtraContributorUs);
                 if (pt.t < best) {
                     best = pt.t;
+                    cfg.mb = mb;
+                    cfg.ar = ar;
+                    cfg.rg = (int)rg;
                     cfg.nb = nb;
                     cfg.waves = waves;
                     cfg.whole = pt.whole;
@@ -358,7 +387,7 @@ struct PlanKeyHash {
         mix((uint64_t)(k.gu * 4 + k.sparse * 2));
         mix((uint64_t)k.cus);
         mix((uint64_t)(k.ov.nb + 8 * (k.ov.whole + 2) + 64 * (k.ov.kind + 2) + 512 * k.ov.ks + 8192 * k.ov.nw +
-                       131072 * k.ov.waves));
+                       131072 * k.ov.waves + 2097152 * k.ov.mb));
         mix((uint64_t)k.ov.grid);
         mix((uint64_t)k.budget);
         return (size_t)h;

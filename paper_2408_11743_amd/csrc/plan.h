@@ -17,10 +17,12 @@ constexpr int kKindTile = 1;    // w4a16_tile_kernel (activation tile shared by 
 constexpr int kKindWide = 2;    // w4a16_wide_kernel (four waves along N, weights in registers)
 
 // One launch configuration of the GEMM kernel.
-//   mb   : 16-row blocks of A per row group (1 or 2)
-//   rg   : row groups of 32 rows (M > 32), each a separate set of tiles
+//   mb   : 16-row blocks of A per row group (1, 2, or 4: 128-column dense tiles
+//          with four waves)
+//   rg   : row groups of 16 * mb rows, each a separate set of tiles
 //   nb   : 16-column blocks per column tile (1, 2 or 4)
-//   ar   : 0, or (mb <= 2) the activation rows arrive in LDS, 4 * ar of them
+//   ar   : 0 (tile and wide kernels), or the activation rows that arrive in
+//          LDS per row group, 4 * ar of them
 //   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
 //   grid : work-groups
 //   waves: stream kernel waves per work-group (they split K): 4, or 8 (two per
@@ -95,11 +97,12 @@ inline bool tile_config_supported(int nw, int wm, int mbw, int nbw, int ks)
 
 // Tuning and test override of the configuration (the cost model is the
 // default): MARLIN_FORCE_CONFIG="nb=<1|2|4|8>,grid=<n>,whole=<0|1>,
-// kind=<stream|tile|wide>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>" forces the
-// column-tile width, the work-group count, the partition, the kernel, the
-// stream kernel's waves per work-group and the tile kernel's waves and blocks
-// per stage, where the shape allows it.  Fields left out are free (0, or -1
-// for whole/kind).
+// kind=<stream|tile|wide>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>,mb=<1|2|4>" forces
+// the column-tile width, the work-group count, the partition, the kernel, the
+// stream kernel's waves per work-group, the tile kernel's waves and blocks
+// per stage and the stream kernel's 16-row blocks per row group, where the
+// shape allows it (mb = 4: dense weights; mb = 1 and 2 follow from M).
+// Fields left out are free (0, or -1 for whole/kind).
 struct Override {
     int nb = 0;
     int grid = 0;
@@ -108,10 +111,11 @@ struct Override {
     int ks = 0;
     int nw = 0;
     int waves = 0;
+    int mb = 0;
     bool operator==(const Override &o) const
     {
         return nb == o.nb && grid == o.grid && whole == o.whole && kind == o.kind && ks == o.ks && nw == o.nw &&
-               waves == o.waves;
+               waves == o.waves && mb == o.mb;
     }
 };
 Override parse_override(const char *spec);  // NULL: no override

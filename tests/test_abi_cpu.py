@@ -137,8 +137,10 @@ def test_describe_reports_a_launchable_configuration(L):
         assert "partition=whole" in text or "partition=streamk" in text, text
         cols = int(text.split("cols=")[1].split()[0])
         assert cols in (16, 32, 64, 128, 256, 512) and N % cols == 0, text
-        if text.startswith("w4a16_stream_kernel<"):
-            rows = 32
+        if text.startswith("w4a16_stream_kernel<"):  # <row blocks, ...>: row groups of 32, or of 64 rows
+            mb = int(text.split("<")[1].split(",")[0])
+            assert mb in (1, 2, 4) and (mb == 4) <= (cols == 128), text
+            rows = 32 if mb < 4 else 64
         elif text.startswith("w4a16_wide_kernel<"):  # <row blocks, column blocks per wave, ring, ...>, 4 waves
             mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:2])
             assert mbw * nbw == 32 and cols == 4 * 16 * nbw, text

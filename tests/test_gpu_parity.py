@@ -187,6 +187,24 @@ def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
 
 
+@pytest.mark.parametrize("part", ["", "whole=1", "whole=0,grid=7", "whole=0,grid=96", "whole=0,grid=300"])
+@pytest.mark.parametrize("M", [1, 20, 33, 48, 64, 65, 100, 128, 129])
+@pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
+def test_stream_kernel_four_row_blocks(mk, force, part, M, K, N, g):
+    # The stream kernel with 64 x 128 outputs per wave (row groups of 64, the
+    # magic-number conversion with group scales on the fp16 weights, the
+    # waves' tiles combined in the activation ring's slot): ragged and
+    # several row groups, whole tiles and Stream-K splits (7 work-groups:
+    # ranges over several tiles and both row groups of a column; 96 and 300:
+    # several contributors per tile, segments ending in either ring slot).
+    spec = "kind=stream,mb=4" + ("," + part if part else "")
+    force(spec)
+    assert mk.marlin_describe(M, N, K, g).startswith("w4a16_stream_kernel<4, 8, "), mk.marlin_describe(M, N, K, g)
+    q, s = synth.weights(16, K, N, None if g == -1 else g)
+    A = synth.activations(16, M, K)
+    check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
+
+
 @pytest.mark.parametrize("spec", ["", "kind=tile,nw=8,whole=1", "kind=tile,nw=8,whole=0,grid=7",
                                   "kind=tile,nw=4,whole=0,grid=96", "kind=stream,whole=1",
                                   "kind=stream,nb=2,whole=0,grid=7"])
@@ -250,22 +268,26 @@ _TILE_IDENTITY = ([(spec, M) for M in (1, 16, 32, 64, 128)
                    for spec in ("kind=tile", "kind=tile,whole=1", "kind=tile,whole=0,grid=7")]
                   + [("kind=tile,nw=8", 64), ("kind=tile,nw=8", 128), ("kind=tile,nw=8,whole=0,grid=7", 128),
                      ("kind=tile,nb=2,ks=4", 1), ("kind=tile,nb=4,ks=2,whole=0,grid=7", 16),
-                     ("kind=tile,nb=1,ks=4", 32), ("kind=tile,nb=2,ks=2,whole=0,grid=7", 32)])
+                     ("kind=tile,nb=1,ks=4", 32), ("kind=tile,nb=2,ks=2,whole=0,grid=7", 32)]
+                  + [("kind=stream,mb=4" + part, M) for M in (1, 33, 64, 128)
+                     for part in ("", ",whole=1", ",whole=0,grid=7")])
 
 
 @pytest.mark.parametrize("spec,M", _TILE_IDENTITY)
 def test_identity_weights_bit_exact_on_the_tile_kernel(mk, force, spec, M):
-    # The tile kernel decodes q - 8 exactly (the magic-number subtraction),
-    # so identity weights with s = 1 give C == A bit for bit: one product
-    # A[m][n] * 1 per output, exact in the fp32 accumulation, the fold and the
-    # fp16 rounding (Section 3.4, "Dequantization and Tensor Cores").
+    # The tile kernel, and the stream kernel with four row blocks, decode
+    # q - 8 exactly (the magic-number subtraction), so identity weights with
+    # s = 1 give C == A bit for bit: one product A[m][n] * 1 per output, exact
+    # in the fp32 accumulation, the fold and the fp16 rounding (Section 3.4,
+    # "Dequantization and Tensor Cores").
     force(spec)
     K = N = 512
     q = np.full((K, N), 8, dtype=np.uint8) + np.eye(K, dtype=np.uint8)
     A = synth.activations(6, M, K)
     for g in (128, -1):
         s = np.ones((1 if g == -1 else K // g, N), dtype=np.float16)
-        assert mk.marlin_describe(M, N, K, g).startswith("w4a16_tile_kernel<")
+        d = mk.marlin_describe(M, N, K, g)
+        assert d.startswith("w4a16_tile_kernel<" if "tile" in spec else "w4a16_stream_kernel<4, "), d
         C = run_gemm(mk, A, q, s, g)
         assert np.array_equal(C.view(np.uint16), A.view(np.uint16)), (spec, M, g)
 
@@ -287,13 +309,14 @@ def test_identity_weights_bit_exact_on_the_sparse_kernel(mk, M):
 @pytest.mark.parametrize("dist", ["uniform_0_8", "outlier_columns"])
 @pytest.mark.parametrize("g", [128, -1])
 @pytest.mark.parametrize("K", [4096, 28672])
-@pytest.mark.parametrize("spec", ["", "kind=stream"])
+@pytest.mark.parametrize("spec", ["", "kind=stream", "kind=stream,mb=2"])
 def test_non_centred_and_outlier_activations(mk, force, dist, g, K, spec):
     # The stream kernel's zero point is a separate fp32 product, 8 * sum A,
     # subtracted from sum A * q: with A >= 0 both sums are large next to their
     # difference, and with outlier columns a few terms dominate them.  Every
-    # output against the oracle, the stream kernel forced and in the library's
-    # own choice, at M = 1, 16, 32, 128.
+    # output against the oracle, the stream kernel forced (beyond 32 rows in
+    # its own choice of row blocks, and with the subnormal path's two) and in
+    # the library's own choice, at M = 1, 16, 32, 128.
     force(spec)
     N = 1024
     q, s = synth.weights(14, K, N, None if g == -1 else g)
