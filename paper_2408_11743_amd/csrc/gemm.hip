@@ -193,12 +193,19 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     static_assert(KW == 4 || (KW == 8 && (MB == 1 || NB == 1)), "four waves, or eight with one row block or column block");
     static_assert(MB <= 2 || (MB == 4 && NB == 8 && KW == 4 && !SPARSE),
                   "one or two row blocks; four only with 128-column dense tiles and four waves");
+    // Tiles too large for a reduction buffer beside the activation ring (64 x
+    // 128 per wave) meet in the ring slot of the stage that ends the segment;
+    // that configuration also loads every row of its group, and holds fewer
+    // activation addresses.
     static_assert(AR >= 1 && kARows <= 16 * MB, "at least 4 rows");
     static_assert((D - 1) * kLoads + kWL + kSL < 64, "vmcnt range");
     // The waves' tiles meet in LDS: in a buffer of their own up to two row
     // blocks; with four (64 x 128 per wave, 32 KiB of fp32, beside a 128 KiB
     // activation ring) in the ring slot of the stage that ends the segment.
-    __shared__ float4_t red[MB == 4 ? 1 : KW * kBlocks * 64];
+    constexpr bool kRingRed = MB == 4;
+    static_assert(!kRingRed || (kARows == 16 * MB && (kAStage / 1024) % KW == 0 && kBlocks % (kAStage / 1024) == 0),
+                  "ring-slot reduction: whole row groups, rounds of whole slots");
+    __shared__ float4_t red[kRingRed ? 1 : KW * kBlocks * 64];
     __shared__ __attribute__((aligned(16))) uint8_t a_lds[KW * D * kAStage + 256];
     __shared__ int flags[2];
 
@@ -266,9 +273,9 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     // add 16 rows to the offset of load i % 4 when they are issued, and the
     // operand reads take the ring slot and row block as instruction offsets
     // from one address per k-step (fewer registers held across the loop).
-    constexpr int kADma = MB == 4 ? 4 : AR;
+    constexpr int kADma = kRingRed ? 4 : AR;
     uint32_t a_dma[kADma];
-    uint32_t a_rd[MB == 4 ? 1 : D][MB == 4 ? 1 : MB][4];
+    uint32_t a_rd[kRingRed ? 1 : D][kRingRed ? 1 : MB][4];
 #pragma unroll
     for (int i = 0; i < kADma; ++i) {
         const int r = 4 * i + lg;
@@ -318,7 +325,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
 #pragma unroll
             for (int i = 0; i < kADma; ++i) {
                 dma[i] = a_dma[i];
-                if constexpr (MB == 4) asm volatile("" : "+v"(dma[i]));  // formed per stage, not held
+                if constexpr (kRingRed) asm volatile("" : "+v"(dma[i]));  // formed per stage, not held
             }
 #pragma unroll
             for (int i = 0; i < AR; ++i)
@@ -394,9 +401,9 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
                          : "memory");
     }
 #pragma unroll
-    for (int j = 0; j < (MB == 4 ? 1 : D); ++j)
+    for (int j = 0; j < (kRingRed ? 1 : D); ++j)
 #pragma unroll
-        for (int mb = 0; mb < (MB == 4 ? 1 : MB); ++mb)
+        for (int mb = 0; mb < (kRingRed ? 1 : MB); ++mb)
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int am = mb * 16 + (lane & 15);
@@ -449,7 +456,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    if constexpr (MB == 4)  // slot j, row block mb: 16 KiB and 4 KiB from the k-step's address
+                    if constexpr (kRingRed)  // slot j, row block mb: kAStage and 4 KiB from the k-step's address
                         asm volatile("ds_read_b128 %0, %1 offset:%2"
                                      : "=v"(v[mb * 4 + t])
                                      : "v"(a_rd[0][0][t]), "i"(j * kAStage + mb * 4096));
@@ -564,7 +571,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
                             acc[c0 + b][mb][i] = __builtin_fmaf(tmp[b][mb][i] - tb[mb][i],
-                                                                (float)sv[(b & 1) * 4 + i], acc[c0 + b][mb][i]);
+                                                                (float)sv[((c0 + b) & 1) * 4 + i], acc[c0 + b][mb][i]);
                 }
             }
         }
@@ -622,7 +629,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             for (int mb = 0; mb < MB; ++mb) bacc[mb] = zero4;
         }
         float4_t out[kOwn];
-        if constexpr (MB != 4) {
+        if constexpr (!kRingRed) {
 #pragma unroll
             for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -643,27 +650,31 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             lds_barrier();
         } else {
             // Every wave's ring slot j is free: the wave has read its rows
-            // (its later stages land in the other slot), and the stage's
-            // refill is issued after the last barrier here.  Two rounds of
-            // four column blocks, 16 KiB per wave: wave w keeps row block w
-            // (MB == KW), i.e. block own(b) of column block b.
+            // (its later stages land in other slots), and the stage's refill
+            // is issued after the last barrier here.  Rounds of kR blocks
+            // (one slot, 1 KiB each): every wave writes its blocks
+            // r*kR .. r*kR + kR-1, then sums its own among them over the
+            // waves (block blk belongs to wave blk % KW, as own(j)).
+            constexpr int kR = kAStage / 1024;
             const auto slot_of_wave = [&](int w) {
                 return reinterpret_cast<float4_t *>(a_lds + (w * D + j) * kAStage);
             };
             float4_t *const mine = slot_of_wave(kw);
 #pragma unroll
-            for (int h = 0; h < NB; h += 4) {
+            for (int r = 0; r < kBlocks / kR; ++r) {
 #pragma unroll
-                for (int b = 0; b < 4; ++b)
+                for (int b = 0; b < NB; ++b)
 #pragma unroll
-                    for (int mb = 0; mb < MB; ++mb) mine[(b * MB + mb) * 64 + lane] = acc[h + b][mb];
+                    for (int mb = 0; mb < MB; ++mb)
+                        if ((b * MB + mb) / kR == r) mine[((b * MB + mb) % kR) * 64 + lane] = acc[b][mb];
                 lds_barrier();
 #pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    float4_t s = slot_of_wave(0)[(b * MB + kw) * 64 + lane];
+                for (int i = 0; i < kR / KW; ++i) {
+                    const int at = (kw + i * KW) * 64 + lane;
+                    float4_t s = slot_of_wave(0)[at];
 #pragma unroll
-                    for (int k2 = 1; k2 < KW; ++k2) s += slot_of_wave(k2)[(b * MB + kw) * 64 + lane];
-                    out[h + b] = s;
+                    for (int k2 = 1; k2 < KW; ++k2) s += slot_of_wave(k2)[at];
+                    out[r * (kR / KW) + i] = s;
                 }
                 lds_barrier();
             }
@@ -694,7 +705,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
             if (cp_ku + KW >= cp_end) {
                 // four row blocks: the last segment is closed after the loop,
                 // so that no sum is held across it
-                if (MB != 4 || cp_c != c_last) {
+                if (!kRingRed || cp_c != c_last) {
                     finish_segment(j);
                     cp_c += 1;
                     cp_ku = 0;
@@ -722,7 +733,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) step(j, st_last + j, D - 1 - j);
-    if constexpr (MB == 4) {
+    if constexpr (kRingRed) {
         // Stages past the range were issued (through empty descriptors) but
         // never waited for: drain them before the ring is reused.
         wait_vmcnt<0>();

@@ -174,11 +174,11 @@ def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
     # The stream kernel with four and with eight waves per work-group, every
     # column-tile width (nb = 8: two packed 64-column tiles per wave) and
     # activation-row class (4, 8, 16, 32 rows in LDS;
-    # 70 rows: three row groups), whole tiles and Stream-K splits (7
+    # 70 rows: three row groups of 32), whole tiles and Stream-K splits (7
     # work-groups: long ranges over several tiles; 96: several contributors
     # per tile), grouped and per-channel.  Eight waves with two row blocks
     # exist for 16-column tiles only; elsewhere the override gives four.
-    spec = "kind=stream,waves=%d,nb=%d,%s" % (waves, nb, part)
+    spec = "kind=stream,waves=%d,nb=%d,%s" % (waves, nb, part) + (",mb=2" if M > 16 else "")
     force(spec)
     w = waves if (M <= 16 or nb == 1) else 4
     assert (", %d, %s>" % (w, "true" if g == -1 else "false")) in mk.marlin_describe(M, N, K, g)
