@@ -97,8 +97,9 @@ struct SparseWords {
     u32x4_t c[NB == 4 ? 2 : 1];
     u32x4_t m;
     __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t codes_off,
-                                         uint32_t meta_off)
+                                         uint32_t meta_off, uint32_t next = 0)
     {
+        (void)next;
         if constexpr (NB == 4) {
             c[0] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, codes_off, kAuxNonTemporal));
             c[1] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + 1024, codes_off, kAuxNonTemporal));
@@ -116,6 +117,21 @@ struct SparseWords {
     // kept codes of column block b, rows 64h .. 64h + 63
     __device__ __forceinline__ uint32_t code(int b, int h) const { return c[(2 * b + h) >> 2][(2 * b + h) & 3]; }
     __device__ __forceinline__ uint32_t meta(int b) const { return m[b]; }
+};
+
+// NB = 8 (two packed 64-column units, the second `next` bytes on): the
+// NB = 4 loads of each, six per stage.
+template <>
+struct SparseWords<8> {
+    SparseWords<4> u[2];
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t lane_off, uint32_t codes_off,
+                                         uint32_t meta_off, uint32_t next)
+    {
+        u[0].load(r, lane_off, codes_off, meta_off);
+        u[1].load(r, lane_off, codes_off + next, meta_off + next);
+    }
+    __device__ __forceinline__ uint32_t code(int b, int h) const { return u[b >> 2].code(b & 3, h); }
+    __device__ __forceinline__ uint32_t meta(int b) const { return u[b >> 2].meta(b & 3); }
 };
 
 // Sparse product of one column block and one 16-row block over 128 rows of
@@ -177,7 +193,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     constexpr int kSL = PER_CHANNEL ? 0 : kSLoads;
     // weight loads per stage: NB 16-byte words (dense), or codes and row
     // indices (sparse: 2 + 1 for NB = 4, else 1 + 1)
-    constexpr int kWL = SPARSE ? (NB == 4 ? 3 : 2) : NB;
+    constexpr int kWL = SPARSE ? (NB == 8 ? 6 : NB == 4 ? 3 : 2) : NB;
     constexpr uint32_t kUnitBytes = SPARSE ? 3072u : 4096u;  // per 64 x 128 unit
     // Four row blocks (dense) convert codes with the magic number too (exact
     // q - 8, group scales on the fp16 weights; see compute)
@@ -292,7 +308,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
     // NB = 8: the wave's column blocks 4..7 lie in the next 64-column tile of
     // the packed layout, KU * 4 KiB further on (weights) and G * 128 bytes
     // further on (scales)
-    const uint32_t w_next = (uint32_t)KU * 4096u;
+    const uint32_t w_next = (uint32_t)KU * kUnitBytes;
     const uint32_t s_next = (uint32_t)p.G * 128u;
 
     u32x4_t wr[SPARSE ? 1 : D][NB];   // dense weights
@@ -337,7 +353,7 @@ __device__ __forceinline__ void stream_body(const GemmProblem &p)
         const __amdgpu_buffer_rsrc_t rw =
             __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, on ? w_bytes : 0u, kBufferFlags);
         if constexpr (SPARSE) {
-            sw[j].load(rw, w_lane, ld_w, ld_w + ld_md);
+            sw[j].load(rw, w_lane, ld_w, ld_w + ld_md, w_next);
         } else {
 #pragma unroll
             for (int b = 0; b < NB; ++b)
@@ -807,7 +823,7 @@ hipError_t launch_stream(const GemmConfig &cfg, const GemmProblem &p, hipStream_
     const bool pc = p.group_units == 0;
     const void *fn = pc ? (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, true>
                         : (const void *)&w4a16_stream_kernel<MB, NB, D, AR, KW, false>;
-    if constexpr (NB <= 4) {  // the 2:4 layout has 64-column tiles at most
+    if constexpr (NB <= 4 || (NB == 8 && MB == 2)) {  // 2:4: 128-column tiles with two row blocks only
         if (cfg.sparse)
             fn = pc ? (const void *)&w4a16_sparse_kernel<MB, NB, DS, AR, KW, true>
                     : (const void *)&w4a16_sparse_kernel<MB, NB, DS, AR, KW, false>;

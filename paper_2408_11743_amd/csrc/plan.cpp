@@ -240,7 +240,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
         const int forced_waves = (ov.waves == 8 && mb != 1 && ov.nb > 1) ? 4 : ov.waves;
         for (int waves = 8; waves >= 4; waves -= 4) {
             if (forced_waves && waves != forced_waves) continue;
-            for (int nb = sparse ? 4 : 8; nb >= 1; nb >>= 1) {
+            for (int nb = (sparse && mb != 2) ? 4 : 8; nb >= 1; nb >>= 1) {
                 if (mb == 4 && (nb != 8 || waves != 4)) continue;  // the one four-row-block kernel
                 const double rate = mb == 4 ? kRate64Rows : wg_rate(mb, ar, nb, waves);
                 if (tiles16 % nb != 0 || rate <= 0.0) continue;

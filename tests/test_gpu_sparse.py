@@ -85,10 +85,11 @@ def force(monkeypatch):
 
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("spec", ["nb=1,whole=1", "nb=2,whole=0,grid=7", "nb=4,whole=0,grid=96", "whole=0,grid=7",
-                                  "nb=4,whole=1"])
+                                  "nb=4,whole=1", "nb=8,whole=1", "nb=8,whole=0,grid=7", "nb=8,whole=0,grid=96"])
 @pytest.mark.parametrize("M", [1, 6, 16, 32, 100, 257])
 def test_sparse_each_partition(mk, force, waves, spec, M):
-    # eight waves apply up to 16 rows; beyond, the override falls back to four
+    # eight waves apply up to 16 rows; beyond, the override falls back to four;
+    # 128-column tiles (two packed units per wave) exist beyond 16 rows
     force("%s,waves=%d" % (spec, waves))
     K, N, g = 2048, 1024, 128
     q, keep, s = synth.sparse24_weights(43, K, N, g)

@@ -72,7 +72,7 @@ def _expected_group(kind, ints, per_channel):
         dma_a, dma_w, scale = TR // (4 * NW), NBW // WM, (2 if NBW == 4 else 1)
         return "L" * (KS * (dma_a + dma_w)) + "R" * (scale if per_channel else KS * scale)
     MB, NB, D, AR, KW = ints
-    weights = (3 if NB == 4 else 2) if kind == "w4a16_sparse_kernel" else NB
+    weights = (6 if NB == 8 else 3 if NB == 4 else 2) if kind == "w4a16_sparse_kernel" else NB
     return "L" * AR + "R" * (weights + (0 if per_channel else (NB + 1) // 2))
 
 
