@@ -8,7 +8,8 @@ tolerance of the fp64 definition always.  Two calls in a row, the second on
 a smaller input, check that the shared array is left ready for the next
 call.  Cases: Stream-K splits of the stream kernel, per-channel scales on the
 tile kernel, a 70B-class layer whose preferred split needs more than the
-array (planned to fit), and a shape with many contributors per shared tile.
+array (planned to fit), a shape with many contributors per shared tile, and
+a Stream-K split of the stream kernel's 64-row groups.
 The file is collected last; it passes alone in a fresh process and after
 every other GPU test.
 """
@@ -66,6 +67,7 @@ CASES = [
     (11008, 4096, -1, [128, 1], True),      # per-channel scales, tile kernel then one row
     (8192, 28672, 128, [128, 65], False),   # eight-wave tile split (64 MiB of slots): planned to fit
     (8192, 1280, 128, [32, 8], True),       # many contributors per shared tile
+    (8192, 10240, 128, [128, 40], True),    # 64-row groups split (32 KiB slots), then 32-row groups
 ]
 
 
