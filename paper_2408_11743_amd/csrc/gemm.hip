@@ -17,16 +17,18 @@
 //    k-step against the codes 8 (shared by all column blocks, subtracted),
 //    and 2^24 into the final conversion.  This is the magic-number idea of
 //    the "Dequantization and Tensor Cores" paragraph with the magic number 0:
-//    no subtraction is needed per weight at all.
+//    no subtraction is needed per weight at all.  (Row groups of 64 rows use
+//    the paper's magic number itself, below.)
 //  * Group scales multiply each 128-row fp32 partial product once, fused
-//    with the bias add (v_fma_mix_f32 reads the fp16 scale directly);
-//    per-channel scales multiply the final sum ("Groups and Instruction
-//    Ordering").
+//    with the bias add (v_fma_mix_f32 reads the fp16 scale directly), or,
+//    with 64-row groups, the fp16 weights before the product; per-channel
+//    scales multiply the final sum ("Groups and Instruction Ordering").
 //  * The waves of a work-group (four; eight, two per SIMD, with a single
 //    16-row block of A or a single 16-column block, so that one wave's
-//    dependent MFMA chain and LDS latency overlap the other's) take consecutive 128-row blocks of one
-//    column tile per stage and meet in LDS when a tile segment ends
-//    (Algorithm 1's reduction over waves that share an output tile).
+//    dependent MFMA chain and LDS latency overlap the other's) take
+//    consecutive 128-row blocks of one column tile per stage and meet in LDS
+//    when a tile segment ends (Algorithm 1's reduction over waves that share
+//    an output tile).
 //  * Stream-K style striped partitioning over a persistent grid: work-group w
 //    owns the contiguous range [w*T/grid, (w+1)*T/grid) of (column tile,
 //    128-row block) units, column-major, wrapping into the next column
