@@ -146,7 +146,7 @@ double wg_rate(int mb, int ar, int nb, int waves)
     static const double r8[3][4] = {
         {30.0e3, 38.8e3, 34.2e3, 20.2e3},  // M <= 4
         {32.0e3, 32.7e3, 22.1e3, 15.6e3},  // M <= 8
-        {27.0e3, 26.0e3, 16.4e3, 11.0e3},  // M <= 16
+        {27.0e3, 26.0e3, 17.6e3, 11.0e3},  // M <= 16
     };
     const int row = (mb == 1) ? (ar == 1 ? 0 : ar == 2 ? 1 : 2) : 3;
     const int col = (nb == 8) ? 0 : (nb == 4) ? 1 : (nb == 2) ? 2 : 3;
