@@ -787,7 +787,9 @@ constexpr int stream_depth()
 {
     if constexpr (MB == 1) {
         constexpr int d = NB == 8 ? 3 : NB == 4 ? 4 : NB == 2 ? 5 : 8;
-        return KW == 8 ? (d + 1) / 2 : d;
+        // (32-column tiles with eight waves measured 2-5% faster with two
+        // stages than with three)
+        return KW == 8 ? (NB == 2 ? 2 : (d + 1) / 2) : d;
     }
     // LDS ring of 32 rows: 8 KiB per wave-stage (eight waves: 16-column
     // tiles only, two stages, 128 KiB); of 64 rows: 16 KiB, two stages
@@ -804,7 +806,7 @@ constexpr int sparse_depth()
 {
     if constexpr (MB == 1) {
         constexpr int d = NB == 4 ? 5 : NB == 2 ? 8 : 7;
-        return KW == 8 ? (d + 1) / 2 : d;
+        return KW == 8 ? (NB == 2 ? 2 : (d + 1) / 2) : d;  // as the dense kernel's
     }
     return stream_depth<MB, NB, AR, KW>();
 }
