@@ -792,9 +792,11 @@ constexpr int stream_depth()
         return KW == 8 ? (NB == 2 ? 2 : (d + 1) / 2) : d;
     }
     // LDS ring of 32 rows: 8 KiB per wave-stage (eight waves: 16-column
-    // tiles only, two stages, 128 KiB); of 64 rows: 16 KiB, two stages
+    // tiles only, two stages, 128 KiB); of 64 rows: 16 KiB, two stages.
+    // (64-column tiles measured 3-6% faster with two stages than with three
+    // at 32..128 rows, 32-column tiles 1-2% with three than with four.)
     if constexpr (KW == 8 || MB == 4) return 2;
-    return NB == 8 ? 2 : NB == 4 ? 3 : 4;
+    return NB >= 4 ? 2 : 3;
 }
 
 // 2:4 sparse stages carry 3/4 of the dense bytes per column block (NB = 4:
