@@ -808,7 +808,9 @@ constexpr int sparse_depth()
 {
     if constexpr (MB == 1) {
         constexpr int d = NB == 4 ? 5 : NB == 2 ? 8 : 7;
-        return KW == 8 ? (NB == 2 ? 2 : (d + 1) / 2) : d;  // as the dense kernel's
+        // eight waves: half as deep, and two stages with 32- and 64-column
+        // tiles (3-4% faster than three on 8192 x 28672 at M = 1..16)
+        return KW == 8 ? (NB >= 2 ? 2 : (d + 1) / 2) : d;
     }
     return stream_depth<MB, NB, AR, KW>();
 }
