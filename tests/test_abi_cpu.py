@@ -203,7 +203,7 @@ def test_override_selects_the_kernel(monkeypatch):
     # two row blocks: eight waves with 16-column tiles only (two-stage ring)
     assert B.marlin_describe(32, 4096, 4096, 128).startswith("w4a16_stream_kernel<2, 1, 2, 8, 8, false>")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=1,waves=8")
-    assert B.marlin_describe(32, 4096, 4096, 128).startswith("w4a16_stream_kernel<2, 2, 4, 8, 4, false>")
+    assert B.marlin_describe(32, 4096, 4096, 128).startswith("w4a16_stream_kernel<2, 2, 3, 8, 4, false>")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=1,whole=1,waves=4")
     assert B.marlin_describe(1, 4096, 4096, 128).startswith("w4a16_stream_kernel<1, 1, 8, 1, 4, false> cols=16")
     monkeypatch.setenv("MARLIN_FORCE_CONFIG", "kind=stream,nb=2,whole=0,grid=7")
