@@ -62,6 +62,7 @@ MLP_7B = [(4096, 11008, 2, 128), (11008, 4096, 2, 128), (4096, 11008, 2, -1), (1
 ROTATION_BYTES = 1 << 30  # >= 1 GiB of weight copies per layer (Infinity Cache is 256 MB)
 CPU_MS = [1, 16, 64, 128]
 RAMP_S = 0.15  # untimed step replays before the warm-up steps (clock ramp)
+CLOCK_S = 4.0  # untimed step replays after the timed region, while the shader clock is read
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "w4a16_gemm_70b_layers_msweep_traffic.json")
 SECTIONS = ("attention_4096", "mlp_7b", "sparse_2of4", "prefill", "quantize")
 
@@ -218,7 +219,7 @@ class ClockSampler:
             recs = [r for r in recs if self.window[0] <= r["t"] <= self.window[1]]
         s = sorted(round(sum(r["mhz"]) / len(r["mhz"]), 1) for r in recs if r.get("mhz"))
         rec = {"source": "amd-smi metric -g 0 -c --json (current shader clock, MHz, mean over the XCDs), "
-                         "about once a second during the per-case measurements of the headline layers",
+                         "about once a second during %.0f s of untimed step replays after the timed region" % CLOCK_S,
                "samples": len(s)}
         if s:
             rec.update({"min_mhz": s[0], "median_mhz": s[len(s) // 2], "max_mhz": s[-1]})
@@ -763,6 +764,18 @@ def main():
             e1.record(stream)
             torch.cuda.synchronize()
             t1 = time.perf_counter()
+    if clock:
+        # the shader clock under the step's own load: CLOCK_S seconds of
+        # untimed step replays, the window whose amd-smi readings are reported
+        w0 = time.time()
+        k = 0
+        with torch.cuda.stream(stream):
+            while time.time() - w0 < CLOCK_S:
+                for _ in range(8):
+                    graphs[k % ngraphs].replay()
+                    k += 1
+                stream.synchronize()
+        clock.mark(w0, time.time())
     del graphs
     ev_ms = e0.elapsed_time(e1)
     wall_ms = (t1 - t0) * 1e3
@@ -775,13 +788,10 @@ def main():
 
     # ---- per case: graph of one launch per weight copy, eager latency, fp16 ----
     per_m = []
-    w0 = time.time()
     for lay in layers:
         la = {M: acts[(lay.K, lay.N, M)] for M in M_SWEEP}
         lo = {M: outs[(lay.K, lay.N, M)] for M in M_SWEEP}
         per_m += measure_cases(args, mk, R, torch, np, dev, lay, M_SWEEP, stream, L, ws, la, lo, "70b")
-    if clock:
-        clock.mark(w0, time.time())
     for lay in layers:
         lay.w16s = []
     torch.cuda.synchronize()
