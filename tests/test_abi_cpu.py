@@ -277,3 +277,18 @@ def test_cost_model_avoids_many_contributor_splits():
     # the 7B / 70B layer shapes keep their measured-best choices
     assert "cols=128 rg=1 partition=whole" in B.marlin_describe(16, 28672, 8192, 128)
     assert "cols=64 rg=1 partition=streamk" in B.marlin_describe(32, 4096, 11008, 128)
+
+
+def test_row_groups_follow_the_layer_shape(L):
+    # Beyond 32 rows the stream kernel takes row groups of 64 (four 16-row
+    # blocks per wave, each weight read once for all the rows) where the cost
+    # model finds them faster -- the 70B up-projection, whose 224 column
+    # tiles of 128 fit the chip whole -- and row groups of 32 elsewhere;
+    # 2:4 weights always take groups of up to 32 rows.
+    for M in (33, 48, 64):
+        assert B.marlin_describe(M, 28672, 8192, 128).startswith("w4a16_stream_kernel<4, 8, 2, 16, 4, false>")
+        assert B.marlin_describe(M, 8192, 28672, 128).startswith("w4a16_stream_kernel<2, 8, 2, 8, 4, false>")
+        assert B.marlin_describe(M, 11008, 4096, 128).startswith("w4a16_stream_kernel<2, ")
+        assert B.marlin_describe_sparse(M, 28672, 8192, 128).startswith("w4a16_sparse_kernel<2, ")
+    assert "rg=1 " in B.marlin_describe(64, 28672, 8192, 128)
+    assert "rg=2 " in B.marlin_describe(64, 8192, 28672, 128)
