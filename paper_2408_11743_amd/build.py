@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libmarlin_mi355x.so")
-SOURCES = ["api.cpp", "plan.cpp", "gemm.hip", "tile.hip", "wide.hip", "pack.hip", "quant.hip", "noalloc.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "gemm.hip", "pair.hip", "tile.hip", "wide.hip", "pack.hip", "quant.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 instructions are disabled for all device code: plain float code

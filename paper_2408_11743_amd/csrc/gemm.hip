@@ -851,6 +851,10 @@ void kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n)
         wide_kernel_name(cfg, per_channel, buf, n);
         return;
     }
+    if (cfg.mb == 4 && cfg.waves == 8) {
+        pair_kernel_name(per_channel, buf, n);
+        return;
+    }
     int d = 0;
     switch (cfg.waves * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
     case 4111: d = ring_depth<1, 1, 1, 4>(cfg.sparse); break;
@@ -897,6 +901,7 @@ hipError_t launch_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t 
 {
     if (cfg.kind == kKindTile) return launch_tile_gemm(cfg, p, stream);
     if (cfg.kind == kKindWide) return launch_wide_gemm(cfg, p, stream);
+    if (cfg.mb == 4 && cfg.waves == 8) return launch_pair_gemm(cfg, p, stream);
     switch (cfg.waves * 1000 + cfg.mb * 100 + cfg.nb * 10 + cfg.ar) {
     case 4111: return launch_stream<1, 1, 1, 4>(cfg, p, stream);
     case 4112: return launch_stream<1, 1, 2, 4>(cfg, p, stream);

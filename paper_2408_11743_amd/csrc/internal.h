@@ -59,6 +59,9 @@ hipError_t launch_tile_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStre
 void tile_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
 hipError_t launch_wide_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
 void wide_kernel_name(const GemmConfig &cfg, bool per_channel, char *buf, size_t n);
+// The stream kernel's 64-row tiles with eight waves (pair.hip).
+hipError_t launch_pair_gemm(const GemmConfig &cfg, const GemmProblem &p, hipStream_t stream);
+void pair_kernel_name(bool per_channel, char *buf, size_t n);
 
 hipError_t launch_pack(const uint8_t *q, const uint16_t *s, int K, int N, int G,
                        uint32_t *w_packed, uint16_t *s_packed, hipStream_t stream);

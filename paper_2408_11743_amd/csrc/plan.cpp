@@ -126,6 +126,15 @@ constexpr double kStreamTailPerExtraContributorUs = 0.45;
 // on 8192 x 28672 at 33..64 rows), and the combination (fixed, and per
 // contributor: the reducer reads one 32 KiB slot each).
 constexpr double kRate64Rows = 11.65e3;
+// ... with eight waves, each pair sharing the activations of one 128-deep
+// block of K (pair.hip): a SIMD's two waves overlap one's conversion with
+// the other's MFMAs (measured 10-20% faster than four waves).  It is chosen
+// for whole tiles only, up to 512 rows: its Stream-K ranges were measured no
+// faster than those of 32-row groups at 33..64 rows (K = 28672, N = 8192)
+// and slower than the model predicts beyond 64 (K = 4096, N = 11008 at
+// M = 128: 29.8 against 24.4 us whole), and at 1024 rows the wide kernel
+// leads.
+constexpr double kRatePair = 12.7e3;
 constexpr double kTail64RowsUs = 4.0;
 constexpr double kTail64RowsPerContributorUs = 1.0;
 
@@ -237,12 +246,12 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
         const int64_t rg = (M + 16 * mb - 1) / (16 * mb);
         // eight waves exist for one 16-row block, or two with one 16-column
         // block; an override to eight applies where they do
-        const int forced_waves = (ov.waves == 8 && mb != 1 && ov.nb > 1) ? 4 : ov.waves;
+        const int forced_waves = (ov.waves == 8 && mb == 2 && ov.nb > 1) ? 4 : ov.waves;
         for (int waves = 8; waves >= 4; waves -= 4) {
             if (forced_waves && waves != forced_waves) continue;
             for (int nb = (sparse && mb != 2) ? 4 : 8; nb >= 1; nb >>= 1) {
-                if (mb == 4 && (nb != 8 || waves != 4)) continue;  // the one four-row-block kernel
-                const double rate = mb == 4 ? kRate64Rows : wg_rate(mb, ar, nb, waves);
+                if (mb == 4 && nb != 8) continue;  // four row blocks: 128-column tiles
+                const double rate = mb == 4 ? (waves == 8 ? kRatePair : kRate64Rows) : wg_rate(mb, ar, nb, waves);
                 if (tiles16 % nb != 0 || rate <= 0.0) continue;
                 if (ov.nb && nb != ov.nb) continue;
                 const int64_t tiles = (int64_t)(tiles16 / nb) * rg;
@@ -251,8 +260,14 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
                 const double layer_bytes = (double)KU * (double)(tiles16 / nb) * unit_bytes;
                 // fp32 partial tile: 16 x 16 x 4 bytes per block, two slots
                 const size_t slot_bytes = (size_t)2 * nb * mb * 256 * sizeof(float);
+                // the eight-wave kernel: whole tiles, up to 512 rows, unless forced
+                Override ovp = ov;
+                if (mb == 4 && waves == 8) {
+                    if (M > 512 && ov.waves != 8) continue;
+                    if (ov.whole != 0) ovp.whole = 1;
+                }
                 const Partition pt =
-                    mb == 4 ? best_partition(ov, tiles, KU, grid, unit_bytes / rate, kTail64RowsUs,
+                    mb == 4 ? best_partition(ovp, tiles, KU, grid, unit_bytes / rate, kTail64RowsUs,
                                              kTail64RowsPerContributorUs, layer_bytes / kChipBytesPerUs, slot_bytes,
                                              partial_budget)
                             : best_partition(ov, tiles, KU, grid, unit_bytes / rate, stream_tail_us(nb * mb), 0.0,

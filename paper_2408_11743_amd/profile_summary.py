@@ -37,7 +37,7 @@ import statistics
 HERE = os.path.dirname(os.path.abspath(__file__))
 # Sources the GEMM kernels and their launch plans are built from: a counter
 # summary holds for the kernels only while these are unchanged.
-KERNEL_SOURCES = ("gemm.hip", "tile.hip", "wide.hip", "device.h", "internal.h", "plan.h", "plan.cpp")
+KERNEL_SOURCES = ("gemm.hip", "pair.hip", "tile.hip", "wide.hip", "device.h", "internal.h", "plan.h", "plan.cpp")
 COPY_KERNEL = "copyBuffer"
 
 

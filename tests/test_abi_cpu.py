@@ -132,7 +132,8 @@ def test_describe_reports_a_launchable_configuration(L):
                        (4096, 28672, 8192, -1), (5000, 11008, 4096, 128)]:
         assert L.marlin_describe(M, N, K, g, buf, len(buf)) == 0
         text = buf.value.decode()
-        assert text.startswith(("w4a16_stream_kernel<", "w4a16_tile_kernel<", "w4a16_wide_kernel<")), text
+        assert text.startswith(("w4a16_stream_kernel<", "w4a16_pair_kernel<", "w4a16_tile_kernel<",
+                                "w4a16_wide_kernel<")), text
         assert ("true>" in text) == (g == -1 or g == K), text
         assert "partition=whole" in text or "partition=streamk" in text, text
         cols = int(text.split("cols=")[1].split()[0])
@@ -141,6 +142,9 @@ def test_describe_reports_a_launchable_configuration(L):
             mb = int(text.split("<")[1].split(",")[0])
             assert mb in (1, 2, 4) and (mb == 4) <= (cols == 128), text
             rows = 32 if mb < 4 else 64
+        elif text.startswith("w4a16_pair_kernel<"):  # eight waves, 64-row groups, 128-column tiles
+            assert cols == 128, text
+            rows = 64
         elif text.startswith("w4a16_wide_kernel<"):  # <row blocks, column blocks per wave, ring, ...>, 4 waves
             mbw, nbw = (int(x) for x in text.split("<")[1].split(",")[:2])
             assert mbw * nbw == 32 and cols == 4 * 16 * nbw, text
@@ -280,15 +284,18 @@ def test_cost_model_avoids_many_contributor_splits():
 
 
 def test_row_groups_follow_the_layer_shape(L):
-    # Beyond 32 rows the stream kernel takes row groups of 64 (four 16-row
-    # blocks per wave, each weight read once for all the rows) where the cost
-    # model finds them faster -- the 70B up-projection, whose 224 column
-    # tiles of 128 fit the chip whole -- and row groups of 32 elsewhere;
-    # 2:4 weights always take groups of up to 32 rows.
+    # Beyond 32 rows the 70B up-projection, whose 224 column tiles of 128 fit
+    # the chip whole, takes row groups of 64 (each weight read once for all
+    # the rows) in the eight-wave kernel; its down-projection (64 column
+    # tiles, Stream-K ranges) and the 7B down-projection keep row groups of
+    # 32, and 2:4 weights always take groups of up to 32 rows.
     for M in (33, 48, 64):
-        assert B.marlin_describe(M, 28672, 8192, 128).startswith("w4a16_stream_kernel<4, 8, 2, 16, 4, false>")
-        assert B.marlin_describe(M, 8192, 28672, 128).startswith("w4a16_stream_kernel<2, 8, 2, 8, 4, false>")
+        d = B.marlin_describe(M, 28672, 8192, 128)
+        assert d.startswith("w4a16_pair_kernel<false>") and "rg=1 partition=whole" in d, d
+        d = B.marlin_describe(M, 8192, 28672, 128)
+        assert d.startswith("w4a16_stream_kernel<2, 8, 2, 8, 4, false>") and "rg=2 partition=streamk" in d, d
         assert B.marlin_describe(M, 11008, 4096, 128).startswith("w4a16_stream_kernel<2, ")
         assert B.marlin_describe_sparse(M, 28672, 8192, 128).startswith("w4a16_sparse_kernel<2, ")
-    assert "rg=1 " in B.marlin_describe(64, 28672, 8192, 128)
-    assert "rg=2 " in B.marlin_describe(64, 8192, 28672, 128)
+    # beyond 64 rows, whole tiles of the eight-wave kernel where they fill the chip
+    assert B.marlin_describe(128, 11008, 4096, 128).startswith("w4a16_pair_kernel<false> cols=128 rg=2 partition=whole")
+    assert not B.marlin_describe(1024, 4096, 4096, 128).startswith("w4a16_pair_kernel<")

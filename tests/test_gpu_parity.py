@@ -187,19 +187,22 @@ def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
 
 
+@pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("part", ["", "whole=1", "whole=0,grid=7", "whole=0,grid=96", "whole=0,grid=300"])
 @pytest.mark.parametrize("M", [1, 20, 33, 48, 64, 65, 100, 128, 129])
 @pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
-def test_stream_kernel_four_row_blocks(mk, force, part, M, K, N, g):
+def test_stream_kernel_four_row_blocks(mk, force, waves, part, M, K, N, g):
     # The stream kernel with 64 x 128 outputs per wave (row groups of 64, the
     # magic-number conversion with group scales on the fp16 weights, the
     # waves' tiles combined in the activation ring's slot): ragged and
     # several row groups, whole tiles and Stream-K splits (7 work-groups:
     # ranges over several tiles and both row groups of a column; 96 and 300:
     # several contributors per tile, segments ending in either ring slot).
-    spec = "kind=stream,mb=4" + ("," + part if part else "")
+    # Eight waves: each pair of waves shares the activations of one 128-deep block of K (pair.hip).
+    spec = "kind=stream,mb=4,waves=%d" % waves + ("," + part if part else "")
     force(spec)
-    assert mk.marlin_describe(M, N, K, g).startswith("w4a16_stream_kernel<4, 8, "), mk.marlin_describe(M, N, K, g)
+    d = mk.marlin_describe(M, N, K, g)
+    assert d.startswith("w4a16_stream_kernel<4, 8, " if waves == 4 else "w4a16_pair_kernel<"), d
     q, s = synth.weights(16, K, N, None if g == -1 else g)
     A = synth.activations(16, M, K)
     check_close(run_gemm(mk, A, q, s, g), oracle.gemm(A, q, s, g), "%s M=%d K=%d N=%d g=%d" % (spec, M, K, N, g))
@@ -269,13 +272,13 @@ _TILE_IDENTITY = ([(spec, M) for M in (1, 16, 32, 64, 128)
                   + [("kind=tile,nw=8", 64), ("kind=tile,nw=8", 128), ("kind=tile,nw=8,whole=0,grid=7", 128),
                      ("kind=tile,nb=2,ks=4", 1), ("kind=tile,nb=4,ks=2,whole=0,grid=7", 16),
                      ("kind=tile,nb=1,ks=4", 32), ("kind=tile,nb=2,ks=2,whole=0,grid=7", 32)]
-                  + [("kind=stream,mb=4" + part, M) for M in (1, 33, 64, 128)
+                  + [("kind=stream,mb=4,waves=%d%s" % (w, part), M) for M in (1, 33, 64, 128) for w in (4, 8)
                      for part in ("", ",whole=1", ",whole=0,grid=7")])
 
 
 @pytest.mark.parametrize("spec,M", _TILE_IDENTITY)
 def test_identity_weights_bit_exact_on_the_tile_kernel(mk, force, spec, M):
-    # The tile kernel, and the stream kernel with four row blocks, decode
+    # The tile kernel, and the stream and pair kernels with four row blocks, decode
     # q - 8 exactly (the magic-number subtraction), so identity weights with
     # s = 1 give C == A bit for bit: one product A[m][n] * 1 per output, exact
     # in the fp32 accumulation, the fold and the fp16 rounding (Section 3.4,
@@ -287,7 +290,9 @@ def test_identity_weights_bit_exact_on_the_tile_kernel(mk, force, spec, M):
     for g in (128, -1):
         s = np.ones((1 if g == -1 else K // g, N), dtype=np.float16)
         d = mk.marlin_describe(M, N, K, g)
-        assert d.startswith("w4a16_tile_kernel<" if "tile" in spec else "w4a16_stream_kernel<4, "), d
+        kernel = ("w4a16_tile_kernel<" if "tile" in spec else
+                  "w4a16_pair_kernel<" if "waves=8" in spec else "w4a16_stream_kernel<4, ")
+        assert d.startswith(kernel), d
         C = run_gemm(mk, A, q, s, g)
         assert np.array_equal(C.view(np.uint16), A.view(np.uint16)), (spec, M, g)
 
@@ -315,7 +320,8 @@ def test_non_centred_and_outlier_activations(mk, force, dist, g, K, spec):
     # subtracted from sum A * q: with A >= 0 both sums are large next to their
     # difference, and with outlier columns a few terms dominate them.  Every
     # output against the oracle, the stream kernel forced (beyond 32 rows in
-    # its own choice of row blocks, and with the subnormal path's two) and in
+    # its own choice of row blocks and waves -- with four row blocks possibly
+    # the pair kernel -- and with the subnormal path's two) and in
     # the library's own choice, at M = 1, 16, 32, 128.
     force(spec)
     N = 1024
@@ -326,7 +332,7 @@ def test_non_centred_and_outlier_activations(mk, force, dist, g, K, spec):
         A = (synth.activations_uniform(14, M, K) if dist == "uniform_0_8"
              else synth.activations_outlier_columns(14, M, K))
         if spec:
-            assert mk.marlin_describe(M, N, K, g).startswith("w4a16_stream_kernel<")
+            assert mk.marlin_describe(M, N, K, g).startswith(("w4a16_stream_kernel<", "w4a16_pair_kernel<"))
         C = mk.gemm(dev(A), wp, sp, K, N, group=g, workspace=ws).cpu().numpy()
         check_close(C, oracle.gemm(A, q, s, g), "%s g=%d K=%d M=%d %s" % (dist, g, K, M, spec))
 

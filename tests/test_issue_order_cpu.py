@@ -41,7 +41,7 @@ def assembly(tmp_path_factory):
     d = tmp_path_factory.mktemp("asm")
     procs = {}
     from paper_2408_11743_amd import build as B
-    for src in ("gemm", "tile", "wide"):
+    for src in ("gemm", "pair", "tile", "wide"):
         out = str(d / (src + ".s"))
         flags = B.SOURCE_FLAGS.get(src + ".hip", B.DEVICE_FLAGS)
         cmd = [hipcc, "--offload-arch=gfx950", "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
@@ -56,13 +56,16 @@ def assembly(tmp_path_factory):
 
 
 def _kernels(text):
-    for m in re.finditer(r"^(_ZN6marlin\S*(w4a16_(?:stream|sparse|tile|wide)_kernel)I((?:Li\d+E)+)Lb(\d)E\S*):", text, re.M):
+    for m in re.finditer(r"^(_ZN6marlin\S*(w4a16_(?:stream|sparse|tile|wide|pair)_kernel)I((?:Li\d+E)*)Lb(\d)E\S*):",
+                         text, re.M):
         body = text[m.end():text.index(".Lfunc_end", m.end())]
         ints = [int(x) for x in re.findall(r"Li(\d+)E", m.group(3))]
         yield m.group(1), m.group(2), ints, m.group(4) == "1", body
 
 
 def _expected_group(kind, ints, per_channel):
+    if kind == "w4a16_pair_kernel":  # half of a block's 16 row loads, 4 weight words, 2 scale runs
+        return "L" * 8 + "R" * (4 + (0 if per_channel else 2))
     if kind == "w4a16_wide_kernel":
         MBW, NBW, P = ints
         return "L" * (MBW + (0 if per_channel else 1)) + "R" * NBW
