@@ -143,8 +143,8 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  *
  * Accumulation is fp32.  Group scales multiply each 128-row fp32 partial
  * product (stream kernel with row groups of up to 32 rows, tile kernel) or,
- * in the wide kernel that serves large batches and the stream kernel with
- * 64-row groups, the fp16 weights before the product (one fp16 rounding per
+ * in the wide kernel that serves large batches and the stream and pair
+ * kernels with 64-row groups, the fp16 weights before the product (one fp16 rounding per
  * weight, as Section 3.4's "Groups and Instruction Ordering" does);
  * per-channel scales multiply the final sum once.  Any M up to 4096
  * runs in one launch: the rows are cut into segments (32 or 64 rows for the
@@ -159,8 +159,9 @@ marlin_status_t marlin_unpack_weights(const void *w_packed, const void *s_packed
  * MARLIN_FORCE_CONFIG="kind=<stream|tile|wide>,nb=<1|2|4|8>,whole=<0|1>,
  * grid=<n>,waves=<4|8>,nw=<4|8>,ks=<1|2|4>,mb=<1|2|4>" (any subset: kernel,
  * column blocks per tile (per wave for the tile and wide kernels), partition,
- * work-groups, stream-kernel waves per work-group, tile-kernel waves and
- * 128-row blocks per stage, stream-kernel 16-row blocks per row group)
+ * work-groups, stream-kernel waves per work-group (eight with mb=4: the
+ * pair kernel), tile-kernel waves and 128-row blocks per stage,
+ * stream-kernel 16-row blocks per row group)
  * overrides it where the shape allows,
  * read at every call (parsed again only when its text changes);
  * configurations are memoised per shape, device and override, so a repeated

@@ -18,15 +18,16 @@ constexpr int kKindWide = 2;    // w4a16_wide_kernel (four waves along N, weight
 
 // One launch configuration of the GEMM kernel.
 //   mb   : 16-row blocks of A per row group (1, 2, or 4: 128-column dense tiles
-//          with four waves)
+//          with four waves, or eight in the pair kernel)
 //   rg   : row groups of 16 * mb rows, each a separate set of tiles
-//   nb   : 16-column blocks per column tile (1, 2 or 4)
+//   nb   : 16-column blocks per column tile (1, 2, 4 or 8)
 //   ar   : 0 (tile and wide kernels), or the activation rows that arrive in
 //          LDS per row group, 4 * ar of them
 //   whole: work-groups own whole column tiles (else 128-row blocks: Stream-K)
 //   grid : work-groups
 //   waves: stream kernel waves per work-group (they split K): 4, or 8 (two per
-//          SIMD) with one 16-row block or one 16-column block
+//          SIMD) with one 16-row block, one 16-column block, or four row
+//          blocks (the pair kernel, pair.hip)
 struct GemmConfig {
     int kind;
     int mb;
