@@ -190,14 +190,16 @@ def test_stream_kernel_waves(mk, force, waves, nb, part, M, K, N, g):
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("part", ["", "whole=1", "whole=0,grid=7", "whole=0,grid=96", "whole=0,grid=300"])
 @pytest.mark.parametrize("M", [1, 20, 33, 48, 64, 65, 100, 128, 129])
-@pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256)])
+@pytest.mark.parametrize("K,N,g", [(2048, 1024, 128), (1408, 768, -1), (1024, 512, 256), (128, 256, 128),
+                                   (384, 384, -1)])
 def test_stream_kernel_four_row_blocks(mk, force, waves, part, M, K, N, g):
     # The stream kernel with 64 x 128 outputs per wave (row groups of 64, the
     # magic-number conversion with group scales on the fp16 weights, the
     # waves' tiles combined in the activation ring's slot): ragged and
     # several row groups, whole tiles and Stream-K splits (7 work-groups:
     # ranges over several tiles and both row groups of a column; 96 and 300:
-    # several contributors per tile, segments ending in either ring slot).
+    # several contributors per tile, segments ending in either ring slot;
+    # K = 128 and 384: fewer 128-row blocks than the waves that split K).
     # Eight waves: each pair of waves shares the activations of one 128-deep block of K (pair.hip).
     spec = "kind=stream,mb=4,waves=%d" % waves + ("," + part if part else "")
     force(spec)
