@@ -128,8 +128,9 @@ constexpr double kStreamTailPerExtraContributorUs = 0.45;
 constexpr double kRate64Rows = 11.65e3;
 // ... with eight waves, each pair sharing the activations of one 128-deep
 // block of K (pair.hip): a SIMD's two waves overlap one's conversion with
-// the other's MFMAs (measured 10-20% faster than four waves).  It is chosen
-// for whole tiles only, up to 512 rows: its Stream-K ranges were measured no
+// the other's MFMAs (measured 10-20% faster than four waves).  At this rate
+// it is weighed for whole tiles only, up to 512 rows (elsewhere it runs in
+// place of the four-wave kernel, below): its Stream-K ranges were measured no
 // faster than those of 32-row groups at 33..64 rows (K = 28672, N = 8192)
 // and slower than the model predicts beyond 64 (K = 4096, N = 11008 at
 // M = 128: 29.8 against 24.4 us whole), and at 1024 rows the wide kernel
@@ -286,6 +287,10 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
             }
         }
     }
+    // Four row blocks with four waves are modelled as measured, but run with
+    // eight (the pair kernel, measured 7-15% faster at every partition and
+    // row-group count tried) unless four are forced.
+    if (cfg.kind == kKindStream && cfg.mb == 4 && cfg.waves == 4 && ov.waves != 4) cfg.waves = 8;
     // tile kernel: the activation tile is shared by the waves of a
     // work-group.  Beyond 32 rows each wave owns 64 x 64 outputs (four waves:
     // 2x2 beyond 64 rows, else 4x1; eight waves, two per SIMD: 4x2), one
