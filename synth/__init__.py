@@ -110,11 +110,12 @@ def activations_outlier_columns(wid: int, M: int, K: int, frac: float = 0.01, fa
 def sparse24_weights(wid: int, K: int, N: int, g: int | None):
     """Draw a 2:4-structured weight along K.
 
-    Returns (q_dense, keep): q_dense uint8 [K, N] with pruned positions set
+    Returns (q_dense, keep, s): q_dense uint8 [K, N] with pruned positions set
     to the code 8 (weight 0), and keep bool [K, N] marking the two kept
     positions in every group of 4 consecutive k of each column.  The kept
     codes are U{0..15} (a kept code may itself be 8).  The two positions
-    are uniform over the six 2-of-4 patterns.
+    are uniform over the six 2-of-4 patterns.  s is fp16 [G, N] (G groups
+    of g rows, one for g None), U[0.5, 1.5] / (8 sqrt(K)).
     """
     if K % 4:
         raise ValueError("K must be a multiple of 4 for 2:4 sparsity")
