@@ -288,7 +288,7 @@ GemmConfig choose_config(int M, int N, int K, int group_units, int cus, bool spa
         }
     }
     // Four row blocks with four waves are modelled as measured, but run with
-    // eight (the pair kernel, measured 7-15% faster at every partition and
+    // eight (the pair kernel, measured 7-22% faster at every partition and
     // row-group count tried) unless four are forced.
     if (cfg.kind == kKindStream && cfg.mb == 4 && cfg.waves == 4 && ov.waves != 4) cfg.waves = 8;
     // tile kernel: the activation tile is shared by the waves of a
