@@ -4,7 +4,8 @@
   Stream-K split puts dozens of work-groups on one tile);
 * the largest N (2^20, K = 128: a single block of K per tile);
 * K*N just below 2^32 (65536 x 65472: 2.1 GB of packed weights, the byte
-  offsets of the weights close to 2^31).
+  offsets of the weights close to 2^31), and the largest of 128-column
+  tiles (65536 x 65408) for the pair kernel's 64-row groups.
 
 Each runs in the library's own configuration and under forced whole-tile and
 Stream-K partitions, against the oracle (in full where it is cheap, else on
@@ -50,6 +51,8 @@ def samples(M, N, count, seed):
 
 
 SPECS = ["", "kind=stream,whole=1", "kind=stream,whole=0,grid=256"]
+# 64-row groups in the eight-wave pair kernel (128-column tiles)
+PAIR_SPECS = ["kind=stream,mb=4,waves=8,whole=1", "kind=stream,mb=4,waves=8,whole=0,grid=256"]
 
 
 @pytest.mark.parametrize("g", [128, -1])
@@ -70,11 +73,11 @@ def test_largest_N(mk, monkeypatch):
     K, N, g = 128, 1 << 20, 128
     q, s = synth.weights(42, K, N, g)
     wp, sp = mk.pack(dev(q), dev(s), group=g)
-    for M in (1, 33):
+    for M in (1, 33, 64):
         A = synth.activations(42, M, K)
         mi, ni = samples(M, N, 3000, [42, M])
         ref = oracle.gemm_sampled(A, q, s, g, mi, ni)
-        for spec in SPECS:
+        for spec in SPECS + (PAIR_SPECS if M > 32 else []):
             monkeypatch.setenv("MARLIN_FORCE_CONFIG", spec)
             C = mk.gemm(dev(A), wp, sp, K, N, group=g).cpu().numpy()
             close(C[mi, ni], ref, "K=128 N=2^20 M=%d %s" % (M, spec))
@@ -93,3 +96,23 @@ def test_largest_weight_matrix(mk, monkeypatch):
             monkeypatch.setenv("MARLIN_FORCE_CONFIG", spec)
             C = mk.gemm(dev(A), wp, sp, K, N, group=g).cpu().numpy()
             close(C[mi, ni], ref, "K=65536 N=65472 M=%d %s" % (M, spec))
+
+
+def test_largest_weight_matrix_of_128_column_tiles(mk, monkeypatch):
+    # The pair kernel's tiles are 128 columns wide: the largest such matrix
+    # under 2^32 codes (511 tiles of 128 columns, weight byte offsets up to
+    # 2^31), at 64 rows.
+    K, N, g = 65536, 65408, 128
+    assert K * N < (1 << 32) and N % 128 == 0 and K * (N + 128) >= (1 << 32)
+    q, s = synth.weights(44, K, N, g)
+    wp, sp = mk.pack(dev(q), dev(s), group=g)
+    M = 64
+    A = synth.activations(44, M, K)
+    mi, ni = samples(M, N, 600, [44, M])
+    ref = oracle.gemm_sampled(A, q, s, g, mi, ni)
+    for spec in [""] + PAIR_SPECS:
+        monkeypatch.setenv("MARLIN_FORCE_CONFIG", spec)
+        if spec:
+            assert mk.marlin_describe(M, N, K, g).startswith("w4a16_pair_kernel<"), spec
+        C = mk.gemm(dev(A), wp, sp, K, N, group=g).cpu().numpy()
+        close(C[mi, ni], ref, "K=65536 N=65408 M=%d %s" % (M, spec))
